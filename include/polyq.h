@@ -1,0 +1,190 @@
+/*
+ * polyq.h -- C ABI of the MI355X (gfx950) mixed-bit linear-layer library.
+ *
+ * The operation (PolyQ, Sec. 3-4): a linear layer y = x W^T whose input
+ * channels each carry a bit-width from {2, 3, 4, 8, 16}.  At compile time the
+ * input channels are permuted and clustered into bit-homogeneous blocks in
+ * ascending bit order (Sec. 4.1, Eq. 9: O = A W = (A P^T)(P W)); every block of
+ * b <= 8 bits is group-quantized (Sec. 3.4) with one fp16 scale s and one fp16
+ * zero point z per output row and per group of 128 channels counted from the
+ * block start; 16-bit channels are plain fp16 weights (Sec. 3.1: unquantized).
+ * One kernel handles all blocks and accumulates them into one output
+ * (Sec. 4.2):
+ *
+ *     y[m][n] = sum over clustered channels k' of  w_hat[n][k'] * x[m][perm[k']]
+ *     w_hat[n][k'] = s[n][g] * (q[n][k'] - z[n][g])   (b <= 8)
+ *     w_hat[n][k'] = fp16 weight                      (b = 16)
+ *
+ * Conventions for every call:
+ *   - Shapes: W is n x k (out x in); codes, x and y are row-major.
+ *   - Ownership: every array argument is caller-owned memory; the library
+ *     allocates nothing, frees nothing and keeps no state between calls, so
+ *     calls on different streams may run concurrently.  polyq_plan takes and
+ *     writes host memory; every other pointer is device memory unless stated.
+ *   - Streams: `stream` is a hipStream_t passed as void* (NULL = null stream).
+ *     Device calls only enqueue work on it: they never synchronize the host.
+ *   - Errors: argument, shape and capacity errors are detected on the host
+ *     before any launch and return a non-zero status with no side effects.
+ *     A failed launch returns POLYQ_ERR_DEVICE.  Device-side faults cannot be
+ *     reported synchronously; indices read from device memory (perm) are
+ *     range-checked in the kernels (an out-of-range entry reads as 0).
+ *   - Aliasing: outputs must not overlap inputs.
+ */
+#ifndef POLYQ_H
+#define POLYQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define POLYQ_MAX_BLOCKS 5    /* one block per bit-width in {2,3,4,8,16}            */
+#define POLYQ_QUANTUM 32      /* every block length is a multiple of this (Sec. 3.3) */
+#define POLYQ_GROUP 128       /* quantization group, counted from each block start   */
+#define POLYQ_TILE_ROWS 64    /* output rows per packed tile                         */
+#define POLYQ_MAX_M_GEMV 16   /* tokens per polyq_gemv call                          */
+#define POLYQ_MAX_K (1 << 20) /* input channels                                      */
+#define POLYQ_MAX_N (1 << 24) /* output channels                                     */
+
+typedef enum {
+  POLYQ_OK = 0,
+  POLYQ_ERR_ARG = 1,         /* null pointer, negative or zero size, bad enum value   */
+  POLYQ_ERR_BITS = 2,        /* bit-width not in {2,3,4,8,16} or blocks not ascending */
+  POLYQ_ERR_QUANTUM = 3,     /* a block length is not a positive multiple of 32      */
+  POLYQ_ERR_SHAPE = 4,       /* block lengths do not sum to k, or n/k out of range    */
+  POLYQ_ERR_CAPACITY = 5,    /* m too large, or workspace too small                   */
+  POLYQ_ERR_UNSUPPORTED = 6, /* valid request this build cannot serve                 */
+  POLYQ_ERR_DEVICE = 7       /* a HIP call failed                                     */
+} polyq_status;
+
+typedef struct {
+  int32_t bits; /* 2, 3, 4, 8 or 16 */
+  int32_t len;  /* channels, a positive multiple of POLYQ_QUANTUM */
+} polyq_block;
+
+/*
+ * Layout of one packed linear (host POD, filled by polyq_plan).
+ *
+ * Packed buffer (device, 256-byte aligned base): the regions of the blocks in
+ * block order, region i at block_offset[i].  A region holds n_tiles tiles of
+ * 64 output rows (rows >= n are zero padding), tile t at
+ * block_offset[i] + t * tile_bytes[i].  A tile holds the block's groups of 128
+ * channels in order (the last one may hold 32, 64 or 96); group j of a tile
+ * starts at j * record_bytes[i] and is
+ *     [meta: 64 rows x {fp16 s, fp16 z} = 256 B, only for b <= 8]
+ *     [chunk 0][chunk 1]...   up to 4 chunks of 32 channels,
+ * and chunk c holds 64 rows x (4*b) bytes, row r at c*64*4b + r*4b.  So one
+ * 32-channel chunk of 64 rows is one contiguous 512 B/768 B/1 KB/2 KB/4 KB run.
+ * Inside a row's 4b bytes (32-bit words, little endian) code i of the chunk is:
+ *   b = 2, 4, 8, 16: word i / (32/b); inside the word the even codes fill the
+ *        low half and the odd codes the high half, in order: code 2p+h of the
+ *        word sits at bits [16h + b*p, 16h + b*p + b).
+ *   b = 3: word d (d = 0,1,2) holds codes 10d .. 10d+9 as five pairs; pair p
+ *        (codes 10d+2p, 10d+2p+1) sits at bits F..F+2 and 16+F..18+F with
+ *        F = {0, 3, 6, 10, 13}[p]; codes 30 and 31 keep bit j in bit 9
+ *        (code 30) and bit 25 (code 31) of word j.
+ *   b = 16: the raw fp16 bits.
+ */
+typedef struct {
+  int32_t n;        /* output channels (rows)                          */
+  int32_t k;        /* input channels                                  */
+  int32_t nblocks;  /* 1 .. POLYQ_MAX_BLOCKS                           */
+  int32_t n_groups; /* sum over blocks with b <= 8 of ceil(len / 128)  */
+  int32_t n_tiles;  /* ceil(n / 64)                                    */
+  int32_t n_chunks; /* k / 32                                          */
+  polyq_block block[POLYQ_MAX_BLOCKS];
+  int32_t k_begin[POLYQ_MAX_BLOCKS];     /* first clustered channel of the block     */
+  int32_t group_begin[POLYQ_MAX_BLOCKS]; /* first group index of the block (b <= 8)   */
+  int64_t block_offset[POLYQ_MAX_BLOCKS];/* byte offset of the block region           */
+  int64_t tile_bytes[POLYQ_MAX_BLOCKS];  /* bytes per 64-row tile in the region       */
+  int64_t record_bytes[POLYQ_MAX_BLOCKS];/* bytes of a full (4-chunk) group record    */
+  int64_t packed_bytes;                  /* total packed-buffer size                  */
+  int64_t code_bits;   /* n * sum_b b * len_b: B_real (Eq. 7) = code_bits / (n k) */
+  int64_t weight_bytes;/* algorithmic bytes of one pass: code_bits/8 + n*n_groups*4 */
+} polyq_layout;
+
+/*
+ * polyq_plan -- validate a block list and compute the packed layout (host only,
+ * no HIP call).  blocks: host array of nblocks entries with strictly ascending
+ * bits from {2,3,4,8,16} and lengths that are positive multiples of 32 summing
+ * to k (the quanta-matched block sizes of Sec. 3.3).  On error *out is left
+ * unchanged.
+ */
+polyq_status polyq_plan(int32_t n, int32_t k, const polyq_block* blocks, int32_t nblocks,
+                        polyq_layout* out);
+
+/*
+ * polyq_pack -- write the packed buffer of a layer (compile-time step of
+ * Sec. 4.1: only the clustered weight P W is materialized).
+ *   codes  [n][k] uint16, clustered channel order: the code q for b <= 8
+ *          (only the low b bits are stored), the fp16 bit pattern for b = 16.
+ *   scales [n][n_groups] fp16 bits, zeros [n][n_groups] fp16 bits
+ *          (ignored when n_groups == 0).
+ *   packed layout->packed_bytes bytes, 256-byte aligned; fully overwritten.
+ */
+polyq_status polyq_pack(const polyq_layout* layout, const uint16_t* codes, const uint16_t* scales,
+                        const uint16_t* zeros, void* packed, void* stream);
+
+/*
+ * polyq_unpack -- inverse of polyq_pack: writes codes [n][k], scales and zeros
+ * [n][n_groups] (fp16 bits) from a packed buffer.  Any of the three outputs may
+ * be NULL to skip it.  Codes of b <= 8 come back masked to b bits.
+ */
+polyq_status polyq_unpack(const polyq_layout* layout, const void* packed, uint16_t* codes,
+                          uint16_t* scales, uint16_t* zeros, void* stream);
+
+/*
+ * polyq_permute -- the explicit activation shuffle of Sec. 4.1 / Eq. 9:
+ * x_out[i][k'] = x[i][perm[k']] for i < m, k' < k, for any 2-byte element type
+ * (fp16 or bf16).  perm: int32 [k] (device).  An entry outside [0, k) yields 0.
+ */
+polyq_status polyq_permute(const int32_t* perm, const uint16_t* x, uint16_t* x_out, int32_t m,
+                           int32_t k, void* stream);
+
+/*
+ * polyq_gemv -- decode / small-batch product, 1 <= m <= 16 tokens:
+ *   y[i][n] = sum_k' w_hat[n][k'] * x[i][perm[k']]   (fp32 accumulation)
+ *   packed  buffer written by polyq_pack for `layout`.
+ *   perm    int32 [k] (device), or NULL when x is already in clustered order.
+ *   x       fp16 [m][k] bits.   y fp32 [m][n], fully overwritten.
+ *   workspace / workspace_bytes: device scratch of at least
+ *           polyq_gemv_workspace_bytes(layout, m) bytes (may be NULL when that
+ *           is 0).  It must be zero-filled before its first use and is left
+ *           zero-filled by every completed call; calls that share a workspace
+ *           must be ordered (same stream).
+ * Precision: every w_hat * x product is exact in fp32 (q - z is an exact
+ * integer, s is applied once per group); |y - y_ref| stays far inside
+ * 1e-3 * sum |w_hat x| for integer zero points.
+ */
+size_t polyq_gemv_workspace_bytes(const polyq_layout* layout, int32_t m);
+polyq_status polyq_gemv(const polyq_layout* layout, const void* packed, const int32_t* perm,
+                        const uint16_t* x, int32_t m, float* y, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/*
+ * polyq_gemm -- prefill product for any m >= 1 (bf16 activations):
+ *   y[i][n] = sum_k' w_hat[n][k'] * x[i][perm[k']]
+ *   x bf16 [m][k] bits, original channel order if perm != NULL, else clustered.
+ *   y fp32 [m][n], fully overwritten.
+ *   workspace: at least polyq_gemm_workspace_bytes(layout, m) bytes of device
+ *   scratch (holds the permuted activations when perm != NULL); contents on
+ *   entry are ignored.
+ * Computed with bf16 MFMA and fp32 accumulation: (q - z) is exact in bf16 and
+ * the group scale is applied in fp32; a 16-bit channel enters as the exact
+ * bf16 pair hi + lo of its fp16 weight.
+ */
+size_t polyq_gemm_workspace_bytes(const polyq_layout* layout, int32_t m, int perm_given);
+polyq_status polyq_gemm(const polyq_layout* layout, const void* packed, const int32_t* perm,
+                        const uint16_t* x, int32_t m, float* y, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/* Static description of a status code (never NULL). */
+const char* polyq_status_str(polyq_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* POLYQ_H */

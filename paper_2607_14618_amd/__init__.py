@@ -1,0 +1,8 @@
+"""MI355X (gfx950) mixed-bit linear layer: PolyQ's decode GEMV and prefill GEMM.
+
+Python binding of libpolyq.so (include/polyq.h).  The functions take torch
+tensors for device memory and run on torch's current HIP stream.
+"""
+from ._lib import (Block, Layout, PolyQError, EXPORTS, LIB_PATH, lib, plan, pack, unpack,  # noqa
+                   permute, gemv, gemm, gemv_workspace_bytes, gemm_workspace_bytes)
+from .layer import PackedLinear  # noqa: F401

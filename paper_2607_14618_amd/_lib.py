@@ -1,0 +1,266 @@
+"""ctypes binding of libpolyq.so: argument marshalling only.
+
+Every step of the computation runs in the library's HIP kernels; torch supplies
+device memory and the current HIP stream.  There is no fallback: if the library
+is missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Dict, Optional, Sequence, Tuple
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpolyq.so")
+
+MAX_BLOCKS = 5
+QUANTUM = 32
+GROUP = 128
+TILE_ROWS = 64
+MAX_M_GEMV = 16
+
+STATUS = {0: "POLYQ_OK", 1: "POLYQ_ERR_ARG", 2: "POLYQ_ERR_BITS", 3: "POLYQ_ERR_QUANTUM",
+          4: "POLYQ_ERR_SHAPE", 5: "POLYQ_ERR_CAPACITY", 6: "POLYQ_ERR_UNSUPPORTED",
+          7: "POLYQ_ERR_DEVICE"}
+
+# every symbol include/polyq.h declares
+EXPORTS = ("polyq_plan", "polyq_pack", "polyq_unpack", "polyq_permute", "polyq_gemv_workspace_bytes",
+           "polyq_gemv", "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_status_str")
+
+
+class Block(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_int32), ("len", ctypes.c_int32)]
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [
+        ("n", ctypes.c_int32), ("k", ctypes.c_int32), ("nblocks", ctypes.c_int32),
+        ("n_groups", ctypes.c_int32), ("n_tiles", ctypes.c_int32), ("n_chunks", ctypes.c_int32),
+        ("block", Block * MAX_BLOCKS),
+        ("k_begin", ctypes.c_int32 * MAX_BLOCKS),
+        ("group_begin", ctypes.c_int32 * MAX_BLOCKS),
+        ("block_offset", ctypes.c_int64 * MAX_BLOCKS),
+        ("tile_bytes", ctypes.c_int64 * MAX_BLOCKS),
+        ("record_bytes", ctypes.c_int64 * MAX_BLOCKS),
+        ("packed_bytes", ctypes.c_int64),
+        ("code_bits", ctypes.c_int64),
+        ("weight_bytes", ctypes.c_int64),
+    ]
+
+    @property
+    def blocks(self):
+        return [(self.block[i].bits, self.block[i].len) for i in range(self.nblocks)]
+
+    def __repr__(self):
+        return (f"Layout(n={self.n}, k={self.k}, blocks={self.blocks}, n_groups={self.n_groups}, "
+                f"packed_bytes={self.packed_bytes}, weight_bytes={self.weight_bytes})")
+
+
+class PolyQError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {_status_str(status)}")
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def lib() -> ctypes.CDLL:
+    """Load libpolyq.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise ImportError(f"{LIB_PATH} is missing: run __graft_entry__.build() "
+                                  "(or python -m paper_2607_14618_amd.build) first")
+            L = ctypes.CDLL(LIB_PATH)
+            vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+            lp = ctypes.POINTER(Layout)
+            L.polyq_plan.argtypes = [i32, i32, ctypes.POINTER(Block), i32, lp]
+            L.polyq_pack.argtypes = [lp, vp, vp, vp, vp, vp]
+            L.polyq_unpack.argtypes = [lp, vp, vp, vp, vp, vp]
+            L.polyq_permute.argtypes = [vp, vp, vp, i32, i32, vp]
+            L.polyq_gemv_workspace_bytes.argtypes = [lp, i32]
+            L.polyq_gemv_workspace_bytes.restype = sz
+            L.polyq_gemv.argtypes = [lp, vp, vp, vp, i32, vp, vp, sz, vp]
+            L.polyq_gemm_workspace_bytes.argtypes = [lp, i32, ctypes.c_int]
+            L.polyq_gemm_workspace_bytes.restype = sz
+            L.polyq_gemm.argtypes = [lp, vp, vp, vp, i32, vp, vp, sz, vp]
+            L.polyq_status_str.argtypes = [ctypes.c_int]
+            L.polyq_status_str.restype = ctypes.c_char_p
+            for name in ("polyq_plan", "polyq_pack", "polyq_unpack", "polyq_permute",
+                         "polyq_gemv", "polyq_gemm"):
+                getattr(L, name).restype = ctypes.c_int
+            _lib = L
+    return _lib
+
+
+def _status_str(status: int) -> str:
+    try:
+        return lib().polyq_status_str(status).decode()
+    except Exception:  # library not loadable
+        return "?"
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        raise PolyQError(status, where)
+
+
+# --------------------------------------------------------------------------- helpers
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(dev: torch.device) -> int:
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def _need_cuda(*ts: Optional[torch.Tensor]) -> torch.device:
+    dev = None
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("polyq device calls take GPU tensors")
+        if not t.is_contiguous():
+            raise ValueError("polyq device calls take contiguous tensors")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError("all tensors must be on the same device")
+    return dev
+
+
+def _as_u16(t: torch.Tensor) -> torch.Tensor:
+    if t.element_size() != 2:
+        raise ValueError(f"expected a 2-byte dtype, got {t.dtype}")
+    return t
+
+
+def _aligned_empty(nbytes: int, dev, align: int = 256) -> torch.Tensor:
+    buf = torch.empty(nbytes + align, dtype=torch.uint8, device=dev)
+    off = (-buf.data_ptr()) % align
+    return buf[off:off + nbytes]
+
+
+# --------------------------------------------------------------------------- API
+def plan(n: int, k: int, blocks: Sequence[Tuple[int, int]]) -> Layout:
+    """Validate a block list and return the packed layout (host only)."""
+    blocks = [(int(b), int(l)) for b, l in blocks]
+    arr = (Block * max(1, len(blocks)))(*[Block(b, l) for b, l in blocks])
+    out = Layout()
+    _check(lib().polyq_plan(int(n), int(k), arr, len(blocks), ctypes.byref(out)), "polyq_plan")
+    return out
+
+
+def pack(layout: Layout, codes: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor
+         ) -> torch.Tensor:
+    """Packed buffer (uint8, 256-byte aligned) on the codes' device."""
+    dev = _need_cuda(codes, scales, zeros)
+    _as_u16(codes), _as_u16(scales), _as_u16(zeros)
+    if tuple(codes.shape) != (layout.n, layout.k):
+        raise ValueError(f"codes shape {tuple(codes.shape)} != ({layout.n}, {layout.k})")
+    if tuple(scales.shape) != (layout.n, layout.n_groups) or scales.shape != zeros.shape:
+        raise ValueError("scales/zeros must be [n][n_groups]")
+    packed = _aligned_empty(layout.packed_bytes, dev)
+    _check(lib().polyq_pack(ctypes.byref(layout), _ptr(codes), _ptr(scales) if layout.n_groups else None,
+                            _ptr(zeros) if layout.n_groups else None, _ptr(packed), _stream(dev)),
+           "polyq_pack")
+    return packed
+
+
+def unpack(layout: Layout, packed: torch.Tensor):
+    """(codes int16 [n][k], scales fp16 [n][G], zeros fp16 [n][G]) from a packed buffer."""
+    dev = _need_cuda(packed)
+    codes = torch.empty((layout.n, layout.k), dtype=torch.int16, device=dev)
+    scales = torch.empty((layout.n, layout.n_groups), dtype=torch.float16, device=dev)
+    zeros = torch.empty((layout.n, layout.n_groups), dtype=torch.float16, device=dev)
+    g = layout.n_groups > 0
+    _check(lib().polyq_unpack(ctypes.byref(layout), _ptr(packed), _ptr(codes),
+                              _ptr(scales) if g else None, _ptr(zeros) if g else None, _stream(dev)),
+           "polyq_unpack")
+    return codes, scales, zeros
+
+
+def permute(perm: torch.Tensor, x: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """x_out[i][k'] = x[i][perm[k']] for 2-byte x (fp16 / bf16)."""
+    x2 = x if x.dim() == 2 else x.reshape(1, -1)
+    dev = _need_cuda(perm, x2)
+    _as_u16(x2)
+    if perm.dtype != torch.int32 or perm.numel() != x2.shape[1]:
+        raise ValueError("perm must be int32 [k]")
+    out = torch.empty_like(x2) if out is None else out
+    _check(lib().polyq_permute(_ptr(perm), _ptr(x2), _ptr(out), x2.shape[0], x2.shape[1],
+                               _stream(dev)), "polyq_permute")
+    return out if x.dim() == 2 else out.reshape(x.shape)
+
+
+_ws: Dict[Tuple[str, int, int], torch.Tensor] = {}
+
+
+def _workspace(kind: str, nbytes: int, dev: torch.device, zero: bool) -> Optional[torch.Tensor]:
+    if nbytes == 0:
+        return None
+    key = (kind, dev.index if dev.index is not None else torch.cuda.current_device(), _stream(dev))
+    buf = _ws.get(key)
+    if buf is None or buf.numel() < nbytes:
+        size = max(nbytes, 2 * (buf.numel() if buf is not None else 0))
+        raw = torch.zeros(size + 256, dtype=torch.uint8, device=dev) if zero else \
+            torch.empty(size + 256, dtype=torch.uint8, device=dev)
+        off = (-raw.data_ptr()) % 256
+        buf = raw[off:off + size]
+        _ws[key] = buf
+    return buf
+
+
+def gemv_workspace_bytes(layout: Layout, m: int) -> int:
+    return int(lib().polyq_gemv_workspace_bytes(ctypes.byref(layout), int(m)))
+
+
+def gemm_workspace_bytes(layout: Layout, m: int, perm_given: bool) -> int:
+    return int(lib().polyq_gemm_workspace_bytes(ctypes.byref(layout), int(m), int(bool(perm_given))))
+
+
+def gemv(layout: Layout, packed: torch.Tensor, perm: Optional[torch.Tensor], x: torch.Tensor,
+         y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """y fp32 [m][n] = x (fp16 [m][k]) times the packed layer; perm None = x pre-permuted."""
+    x2 = x if x.dim() == 2 else x.reshape(1, -1)
+    dev = _need_cuda(packed, perm, x2, y, workspace)
+    if x2.dtype != torch.float16 or x2.shape[1] != layout.k:
+        raise ValueError("x must be fp16 [m][k]")
+    m = x2.shape[0]
+    if perm is not None and (perm.dtype != torch.int32 or perm.numel() != layout.k):
+        raise ValueError("perm must be int32 [k]")
+    if y is None:
+        y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
+    need = gemv_workspace_bytes(layout, m) if 1 <= m <= MAX_M_GEMV else 0
+    ws = workspace if workspace is not None else _workspace("gemv", need, dev, zero=True)
+    _check(lib().polyq_gemv(ctypes.byref(layout), _ptr(packed), _ptr(perm), _ptr(x2), m, _ptr(y),
+                            _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                            _stream(dev)), "polyq_gemv")
+    return y
+
+
+def gemm(layout: Layout, packed: torch.Tensor, perm: Optional[torch.Tensor], x: torch.Tensor,
+         y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """y fp32 [m][n] = x (bf16 [m][k]) times the packed layer (prefill)."""
+    x2 = x if x.dim() == 2 else x.reshape(1, -1)
+    dev = _need_cuda(packed, perm, x2, y, workspace)
+    if x2.dtype != torch.bfloat16 or x2.shape[1] != layout.k:
+        raise ValueError("x must be bf16 [m][k]")
+    m = x2.shape[0]
+    if y is None:
+        y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
+    need = gemm_workspace_bytes(layout, m, perm is not None)
+    ws = workspace if workspace is not None else _workspace("gemm", need, dev, zero=False)
+    _check(lib().polyq_gemm(ctypes.byref(layout), _ptr(packed), _ptr(perm), _ptr(x2), m, _ptr(y),
+                            _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                            _stream(dev)), "polyq_gemm")
+    return y

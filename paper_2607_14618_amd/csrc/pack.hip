@@ -1,0 +1,222 @@
+// Pack / unpack of the clustered quantized weight (Sec. 4.1: the clustered
+// weight P W is materialized once, at compile time) and the explicit activation
+// shuffle of Eq. 9.  Memory-bound helper kernels; the packed layout is the one
+// declared in include/polyq.h.
+#include <hip/hip_runtime.h>
+
+#include "codec.h"
+#include "internal.h"
+
+namespace polyq {
+namespace {
+
+constexpr int kThreads = 256;
+
+inline unsigned grid_for(int64_t items) {
+  return static_cast<unsigned>((items + kThreads - 1) / kThreads);
+}
+
+// One thread per (tile, chunk, lane slice): gathers the slice's 4 rows x 8
+// channels from the row-major codes and writes its 4*B bytes.
+template <int B>
+__global__ __launch_bounds__(kThreads) void pack_codes_kernel(
+    const uint16_t* __restrict__ codes, int n, int k, int k0, int nch, int n_tiles,
+    int64_t tile_bytes, int64_t record_bytes, uint8_t* __restrict__ region) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(n_tiles) * nch * 64) return;
+  const int lane = static_cast<int>(idx % 64);
+  const int64_t rest = idx / 64;
+  const int t = static_cast<int>(rest % n_tiles), c = static_cast<int>(rest / n_tiles);
+  uint16_t q[32];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int R = t * 64 + 16 * r + (lane % 16);
+    if (R < n) {
+      const uint4 u = *reinterpret_cast<const uint4*>(codes + static_cast<int64_t>(R) * k + k0 +
+                                                      c * 32 + 8 * (lane / 16));
+      const uint32_t wd[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        q[slice_index(r, 2 * j)] = static_cast<uint16_t>(wd[j] & 0xFFFFu);
+        q[slice_index(r, 2 * j + 1)] = static_cast<uint16_t>(wd[j] >> 16);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) q[slice_index(r, j)] = 0;
+    }
+  }
+  uint32_t w[B];
+  encode_slice<B>(q, w);
+  uint32_t* dst = reinterpret_cast<uint32_t*>(
+      region + slice_offset(tile_bytes, record_bytes, B <= 8 ? kMetaBytes : 0, B, t, c, lane));
+#pragma unroll
+  for (int d = 0; d < B; ++d) dst[d] = w[d];
+}
+
+template <int B>
+__global__ __launch_bounds__(kThreads) void unpack_codes_kernel(
+    const uint8_t* __restrict__ region, int n, int k, int k0, int nch, int n_tiles,
+    int64_t tile_bytes, int64_t record_bytes, uint16_t* __restrict__ codes) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(n_tiles) * nch * 64) return;
+  const int lane = static_cast<int>(idx % 64);
+  const int64_t rest = idx / 64;
+  const int t = static_cast<int>(rest % n_tiles), c = static_cast<int>(rest / n_tiles);
+  const uint32_t* src = reinterpret_cast<const uint32_t*>(
+      region + slice_offset(tile_bytes, record_bytes, B <= 8 ? kMetaBytes : 0, B, t, c, lane));
+  uint32_t w[B];
+#pragma unroll
+  for (int d = 0; d < B; ++d) w[d] = src[d];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int R = t * 64 + 16 * r + (lane % 16);
+    if (R >= n) continue;
+    uint32_t out[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      out[j] = slice_code<B>(w, slice_index(r, 2 * j)) | (slice_code<B>(w, slice_index(r, 2 * j + 1)) << 16);
+    *reinterpret_cast<uint4*>(codes + static_cast<int64_t>(R) * k + k0 + c * 32 + 8 * (lane / 16)) =
+        uint4{out[0], out[1], out[2], out[3]};
+  }
+}
+
+// One thread per (row, block-local group): scale and zero point into the group's metadata.
+__global__ __launch_bounds__(kThreads) void pack_meta_kernel(
+    const uint16_t* __restrict__ scales, const uint16_t* __restrict__ zeros, int n, int G, int g0,
+    int ng, int64_t tile_bytes, int64_t record_bytes, int rows_total, uint8_t* __restrict__ region) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(rows_total) * ng) return;
+  const int R = static_cast<int>(idx % rows_total);
+  const int g = static_cast<int>(idx / rows_total);
+  uint16_t sv = 0, zv = 0;
+  if (R < n) {
+    const int64_t at = static_cast<int64_t>(R) * G + g0 + g;
+    sv = scales[at];
+    zv = zeros[at];
+  }
+  uint16_t* meta = reinterpret_cast<uint16_t*>(region + (R / 64) * tile_bytes + g * record_bytes);
+  meta[meta_z_half(R % 64)] = zv;
+  meta[meta_s_half(R % 64)] = sv;
+}
+
+__global__ __launch_bounds__(kThreads) void unpack_meta_kernel(
+    const uint8_t* __restrict__ region, int n, int G, int g0, int ng, int64_t tile_bytes,
+    int64_t record_bytes, uint16_t* __restrict__ scales, uint16_t* __restrict__ zeros) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(n) * ng) return;
+  const int R = static_cast<int>(idx % n);
+  const int g = static_cast<int>(idx / n);
+  const uint16_t* meta =
+      reinterpret_cast<const uint16_t*>(region + (R / 64) * tile_bytes + g * record_bytes);
+  const int64_t at = static_cast<int64_t>(R) * G + g0 + g;
+  if (scales) scales[at] = meta[meta_s_half(R % 64)];
+  if (zeros) zeros[at] = meta[meta_z_half(R % 64)];
+}
+
+__global__ __launch_bounds__(kThreads) void permute_kernel(const int32_t* __restrict__ perm,
+                                                           const uint16_t* __restrict__ x,
+                                                           uint16_t* __restrict__ out, int m, int k) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(m) * k) return;
+  const int i = static_cast<int>(idx / k), kp = static_cast<int>(idx % k);
+  const int p = perm[kp];
+  out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
+}
+
+template <int B>
+void launch_pack(const polyq_layout& L, int i, const uint16_t* codes, uint8_t* region,
+                 hipStream_t st) {
+  const int nch = L.block[i].len / kChunk;
+  hipLaunchKernelGGL(pack_codes_kernel<B>,
+                     dim3(grid_for(static_cast<int64_t>(L.n_tiles) * nch * 64)), dim3(kThreads), 0,
+                     st, codes, L.n, L.k, L.k_begin[i], nch, L.n_tiles, L.tile_bytes[i],
+                     L.record_bytes[i], region);
+}
+
+template <int B>
+void launch_unpack(const polyq_layout& L, int i, const uint8_t* region, uint16_t* codes,
+                   hipStream_t st) {
+  const int nch = L.block[i].len / kChunk;
+  hipLaunchKernelGGL(unpack_codes_kernel<B>,
+                     dim3(grid_for(static_cast<int64_t>(L.n_tiles) * nch * 64)), dim3(kThreads), 0,
+                     st, region, L.n, L.k, L.k_begin[i], nch, L.n_tiles, L.tile_bytes[i],
+                     L.record_bytes[i], codes);
+}
+
+}  // namespace
+}  // namespace polyq
+
+using namespace polyq;
+
+extern "C" polyq_status polyq_pack(const polyq_layout* layout, const uint16_t* codes,
+                                   const uint16_t* scales, const uint16_t* zeros, void* packed,
+                                   void* stream) {
+  if (!layout_is_valid(layout)) return POLYQ_ERR_ARG;
+  const polyq_layout& L = *layout;
+  if (codes == nullptr || packed == nullptr) return POLYQ_ERR_ARG;
+  if (L.n_groups > 0 && (scales == nullptr || zeros == nullptr)) return POLYQ_ERR_ARG;
+  if (reinterpret_cast<uintptr_t>(packed) % 256 != 0 || reinterpret_cast<uintptr_t>(codes) % 16 != 0)
+    return POLYQ_ERR_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* base = static_cast<uint8_t*>(packed);
+  const int rows_total = L.n_tiles * kTileRows;
+  for (int i = 0; i < L.nblocks; ++i) {
+    uint8_t* region = base + L.block_offset[i];
+    switch (L.block[i].bits) {
+      case 2: launch_pack<2>(L, i, codes, region, st); break;
+      case 3: launch_pack<3>(L, i, codes, region, st); break;
+      case 4: launch_pack<4>(L, i, codes, region, st); break;
+      case 8: launch_pack<8>(L, i, codes, region, st); break;
+      case 16: launch_pack<16>(L, i, codes, region, st); break;
+      default: return POLYQ_ERR_BITS;
+    }
+    if (L.block[i].bits <= 8) {
+      const int ng = (L.block[i].len + kGroup - 1) / kGroup;
+      hipLaunchKernelGGL(pack_meta_kernel, dim3(grid_for(static_cast<int64_t>(rows_total) * ng)),
+                         dim3(kThreads), 0, st, scales, zeros, L.n, L.n_groups, L.group_begin[i],
+                         ng, L.tile_bytes[i], L.record_bytes[i], rows_total, region);
+    }
+  }
+  return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
+}
+
+extern "C" polyq_status polyq_unpack(const polyq_layout* layout, const void* packed,
+                                     uint16_t* codes, uint16_t* scales, uint16_t* zeros,
+                                     void* stream) {
+  if (!layout_is_valid(layout)) return POLYQ_ERR_ARG;
+  const polyq_layout& L = *layout;
+  if (packed == nullptr || reinterpret_cast<uintptr_t>(packed) % 256 != 0) return POLYQ_ERR_ARG;
+  if (codes != nullptr && reinterpret_cast<uintptr_t>(codes) % 16 != 0) return POLYQ_ERR_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const uint8_t* base = static_cast<const uint8_t*>(packed);
+  for (int i = 0; i < L.nblocks; ++i) {
+    const uint8_t* region = base + L.block_offset[i];
+    if (codes != nullptr) {
+      switch (L.block[i].bits) {
+        case 2: launch_unpack<2>(L, i, region, codes, st); break;
+        case 3: launch_unpack<3>(L, i, region, codes, st); break;
+        case 4: launch_unpack<4>(L, i, region, codes, st); break;
+        case 8: launch_unpack<8>(L, i, region, codes, st); break;
+        case 16: launch_unpack<16>(L, i, region, codes, st); break;
+        default: return POLYQ_ERR_BITS;
+      }
+    }
+    if (L.block[i].bits <= 8 && (scales != nullptr || zeros != nullptr)) {
+      const int ng = (L.block[i].len + kGroup - 1) / kGroup;
+      hipLaunchKernelGGL(unpack_meta_kernel, dim3(grid_for(static_cast<int64_t>(L.n) * ng)),
+                         dim3(kThreads), 0, st, region, L.n, L.n_groups, L.group_begin[i], ng,
+                         L.tile_bytes[i], L.record_bytes[i], scales, zeros);
+    }
+  }
+  return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
+}
+
+extern "C" polyq_status polyq_permute(const int32_t* perm, const uint16_t* x, uint16_t* x_out,
+                                      int32_t m, int32_t k, void* stream) {
+  if (perm == nullptr || x == nullptr || x_out == nullptr) return POLYQ_ERR_ARG;
+  if (m < 1 || k < 1 || k > POLYQ_MAX_K) return POLYQ_ERR_ARG;
+  if (static_cast<int64_t>(m) * k > (static_cast<int64_t>(1) << 40)) return POLYQ_ERR_CAPACITY;
+  hipLaunchKernelGGL(permute_kernel, dim3(grid_for(static_cast<int64_t>(m) * k)), dim3(kThreads), 0,
+                     static_cast<hipStream_t>(stream), perm, x, x_out, m, k);
+  return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
+}

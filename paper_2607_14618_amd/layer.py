@@ -1,0 +1,44 @@
+"""A packed mixed-bit linear layer on one GPU (thin holder around the C ABI)."""
+from __future__ import annotations
+
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+from . import _lib
+
+
+class PackedLinear:
+    """Clustered, packed weights of one linear plus its channel permutation.
+
+    Built once from logical codes (clustered order), fp16 scales and zeros and
+    the permutation; ``decode`` runs polyq_gemv and ``prefill`` runs polyq_gemm.
+    """
+
+    def __init__(self, blocks: Sequence[Tuple[int, int]], codes: torch.Tensor,
+                 scales: torch.Tensor, zeros: torch.Tensor, perm, device="cuda"):
+        n, k = codes.shape
+        self.layout = _lib.plan(n, k, blocks)
+        dev = torch.device(device)
+        codes = codes.to(dev).contiguous()
+        scales = scales.to(dev, torch.float16).contiguous()
+        zeros = zeros.to(dev, torch.float16).contiguous()
+        self.packed = _lib.pack(self.layout, codes, scales, zeros)
+        self.perm = torch.as_tensor(np.asarray(perm, dtype=np.int32)).to(dev)
+        self.n, self.k = n, k
+
+    @property
+    def weight_bytes(self) -> int:
+        return int(self.layout.weight_bytes)
+
+    def decode(self, x: torch.Tensor, pre_permuted: bool = False,
+               y: Optional[torch.Tensor] = None) -> torch.Tensor:
+        return _lib.gemv(self.layout, self.packed, None if pre_permuted else self.perm, x, y)
+
+    def prefill(self, x: torch.Tensor, pre_permuted: bool = False,
+                y: Optional[torch.Tensor] = None) -> torch.Tensor:
+        return _lib.gemm(self.layout, self.packed, None if pre_permuted else self.perm, x, y)
+
+    def permute(self, x: torch.Tensor) -> torch.Tensor:
+        return _lib.permute(self.perm, x)

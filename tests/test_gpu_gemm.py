@@ -1,0 +1,97 @@
+"""Prefill GEMM (bf16 MFMA, fp32 accumulation) on the GPU against the fp64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_14618_amd as pq
+from synth import make_layer, random_quant_linear, MIX_PREFILL_4
+from gpu_util import dev, np_, packed_linear, oracle_ref, assert_parity
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [
+    (64, [(2, 128)]),
+    (1, [(3, 32)]),
+    (100, [(2, 160), (3, 96), (4, 128), (8, 96), (16, 32)]),
+    (130, [(2, 992), (3, 704), (4, 256), (8, 64), (16, 32)]),
+    (37, [(2, 32), (3, 32), (4, 32), (8, 32), (16, 32)]),
+    (257, [(4, 480), (16, 96)]),
+    (64, [(16, 256)]),
+]
+
+
+def _xb(m, k, seed):
+    g = torch.Generator().manual_seed(seed)
+    x = torch.randn((m, k), generator=g)
+    idx = torch.randperm(k, generator=g)[: max(1, k // 100)]
+    x[:, idx] *= 50
+    return x.bfloat16()
+
+
+@pytest.mark.parametrize("n,blocks", SHAPES)
+@pytest.mark.parametrize("m", [1, 7, 128, 300])
+def test_gemm_parity_small(n, blocks, m):
+    k = sum(l for _, l in blocks)
+    lin = random_quant_linear(n, k, blocks, seed=2000 + n + k + m, mode="codes")
+    pl = packed_linear(lin)
+    x = _xb(m, k, seed=n + m)
+    y = pl.prefill(x.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, x)
+    assert_parity(y, y_ref, bound, f"gemm n={n} blocks={blocks} m={m}")
+    xp = pl.permute(x.to(dev()))
+    y2 = pl.prefill(xp, pre_permuted=True)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+
+
+def test_gemm_one_hot_rows_are_exact():
+    """(q - z) is exact in bf16, s is applied once in fp32, 16-bit weights enter as
+    hi + lo: a one-hot activation row selects one dequantized weight exactly."""
+    import oracle
+    blocks = [(2, 160), (3, 96), (4, 128), (8, 96), (16, 32)]
+    lin = random_quant_linear(100, 512, blocks, seed=9, mode="codes")
+    pl = packed_linear(lin)
+    cols = [0, 3, 200, 511]
+    x = torch.zeros((len(cols), 512), dtype=torch.bfloat16)
+    for i, j in enumerate(cols):
+        x[i, j] = 1.0
+    y = pl.prefill(x.to(dev()))
+    torch.cuda.synchronize()
+    w_hat = oracle.dequantize(lin.blocks, np_(lin.codes).view(np.uint16), np_(lin.scales),
+                              np_(lin.zeros))
+    inv = np.argsort(lin.perm)
+    for i, j in enumerate(cols):
+        assert np.array_equal(np_(y)[i].astype(np.float64), w_hat[:, inv[j]]), j
+
+
+def test_gemm_rows_match_gemv():
+    """Each GEMM row equals the GEMV of that token within the tolerance (the
+    activations are bf16 values, exactly representable in fp16 here)."""
+    blocks = [(2, 992), (3, 704), (4, 256), (8, 64), (16, 32)]
+    lin = random_quant_linear(200, 2048, blocks, seed=4, mode="gauss")
+    pl = packed_linear(lin)
+    x = (torch.randn((5, 2048), generator=torch.Generator().manual_seed(3)) * 4).bfloat16()
+    assert torch.equal(x.half().bfloat16(), x)
+    yg = pl.prefill(x.to(dev()))
+    yv = pl.decode(x.half().to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, x)
+    assert_parity(yg, y_ref, bound, "gemm")
+    assert_parity(yv, y_ref, bound, "gemv")
+    assert np.all(np.abs(np_(yg) - np_(yv)) <= 2e-3 * bound)
+
+
+def test_gemm_config3_llama2_13b_prefill():
+    """Llama2-13B layer at M=512, 4.0-bit mix: 512 seeded rows of each linear."""
+    lins, groups = make_layer(3, m=512, x_dtype=torch.bfloat16, device=dev())
+    rng = np.random.default_rng(3)
+    for lin in lins:
+        x = groups[lin.group].x
+        pl = packed_linear(lin)
+        assert pl.layout.code_bits == 4 * lin.n * lin.k
+        y = pl.prefill(x.to(dev()))
+        torch.cuda.synchronize()
+        rows = np.sort(rng.choice(lin.n, 512, replace=False))
+        y_ref, bound = oracle_ref(lin, x, rows=rows)
+        assert_parity(np_(y)[:, rows], y_ref, bound, f"config 3 {lin.name}")

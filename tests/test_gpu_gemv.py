@@ -1,0 +1,197 @@
+"""Decode / small-batch GEMV on the GPU against the fp64 oracle (element by element)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_14618_amd as pq
+from synth import (make_layer, random_quant_linear, SWEEP_MIXES, QWEN3_32B_LAYER,
+                   LLAMA2_13B_LAYER)
+from gpu_util import dev, np_, packed_linear, oracle_ref, assert_parity
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [
+    (64, [(2, 128)]),
+    (1, [(3, 32)]),
+    (100, [(2, 160), (3, 96), (4, 128), (8, 96), (16, 32)]),
+    (130, [(2, 992), (3, 704), (4, 256), (8, 64), (16, 32)]),
+    (37, [(2, 32), (3, 32), (4, 32), (8, 32), (16, 32)]),
+    (257, [(4, 480), (16, 96)]),
+    (64, [(16, 256)]),
+    (640, [(2, 2400), (3, 1728), (4, 768), (8, 160), (16, 64)]),
+]
+
+
+def _x(m, k, seed, outliers=True):
+    g = torch.Generator().manual_seed(seed)
+    x = torch.randn((m, k), generator=g)
+    if outliers:
+        idx = torch.randperm(k, generator=g)[: max(1, k // 100)]
+        x[:, idx] *= 50
+    return x.half()
+
+
+@pytest.mark.parametrize("n,blocks", SMALL)
+@pytest.mark.parametrize("m", [1, 3, 4, 16])
+@pytest.mark.parametrize("mode", ["gauss", "codes"])
+def test_gemv_parity_small(n, blocks, m, mode):
+    k = sum(l for _, l in blocks)
+    lin = random_quant_linear(n, k, blocks, seed=1000 + n + k + m, mode=mode)
+    pl = packed_linear(lin)
+    x = _x(m, k, seed=n + m)
+    y = pl.decode(x.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, x)
+    assert_parity(y, y_ref, bound, f"n={n} blocks={blocks} m={m} {mode}")
+    # pre-permuted activations (variant P) give the same result
+    xp = pl.permute(x.to(dev()))
+    y2 = pl.decode(xp, pre_permuted=True)
+    assert torch.equal(y, y2)
+
+
+@pytest.mark.parametrize("m", [1, 2, 5])
+def test_gemv_is_deterministic_and_reuses_its_workspace(m):
+    lin = random_quant_linear(384, 5120, [(2, 2400), (3, 1728), (4, 768), (8, 160), (16, 64)],
+                              seed=5, mode="codes")
+    pl = packed_linear(lin)
+    x1, x2 = _x(m, 5120, 1).to(dev()), _x(m, 5120, 2).to(dev())
+    ya = pl.decode(x1)
+    yb = pl.decode(x2)
+    yc = pl.decode(x1)
+    torch.cuda.synchronize()
+    assert torch.equal(ya, yc)
+    for x, y in ((x1, ya), (x2, yb)):
+        y_ref, bound = oracle_ref(lin, x.cpu())
+        assert_parity(y, y_ref, bound)
+
+
+def test_gemv_zero_and_one_hot_inputs_are_exact():
+    blocks = [(2, 160), (3, 96), (4, 128), (8, 96), (16, 32)]
+    lin = random_quant_linear(100, 512, blocks, seed=77, mode="codes")
+    pl = packed_linear(lin)
+    y0 = pl.decode(torch.zeros((1, 512), dtype=torch.float16, device=dev()))
+    torch.cuda.synchronize()
+    assert torch.all(y0 == 0)
+    w_hat = oracle.dequantize(lin.blocks, np_(lin.codes).view(np.uint16), np_(lin.scales),
+                              np_(lin.zeros))
+    inv = np.argsort(lin.perm)
+    for j in (0, 5, 200, 511):
+        x = torch.zeros((1, 512), dtype=torch.float16)
+        x[0, j] = 1.0
+        y = pl.decode(x.to(dev()))
+        torch.cuda.synchronize()
+        # (q - z) is exact and s is applied once in fp32: the product is exact
+        assert np.array_equal(np_(y)[0].astype(np.float64), w_hat[:, inv[j]]), j
+
+
+def test_gemv_zero_weights_give_exact_zero():
+    blocks = [(2, 128), (4, 96), (16, 32)]
+    lin = random_quant_linear(64, 256, blocks, seed=3, mode="codes")
+    codes = np_(lin.codes).view(np.uint16).copy()
+    z = np_(lin.zeros)
+    for b, k0, k1, g0 in oracle.block_table(blocks):
+        for j in range(k0, k1):
+            codes[:, j] = 0 if b == 16 else z[:, g0 + (j - k0) // 128].astype(np.uint16)
+    lin.codes = torch.from_numpy(codes.view(np.int16))
+    pl = packed_linear(lin)
+    y = pl.decode(_x(2, 256, 9).to(dev()))
+    torch.cuda.synchronize()
+    assert torch.all(y == 0)
+
+
+def test_gemv_non_integer_zero_points():
+    blocks = [(2, 128), (3, 128), (8, 128)]
+    lin = random_quant_linear(96, 384, blocks, seed=8, mode="codes")
+    rng = np.random.default_rng(0)
+    lin.zeros = torch.from_numpy(rng.uniform(0, 3, size=lin.zeros.shape).astype(np.float16))
+    pl = packed_linear(lin)
+    x = _x(2, 384, 4)
+    y = pl.decode(x.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, x)
+    assert_parity(y, y_ref, bound, "non-integer z")
+
+
+def test_gemv_adversarial_outliers_inside_2bit_groups():
+    """One huge activation inside each 2-bit group, zero points at both ends."""
+    blocks = [(2, 512), (16, 32)]
+    lin = random_quant_linear(128, 544, blocks, seed=21, mode="codes")
+    z = np_(lin.zeros).copy()
+    z[::2] = 0
+    z[1::2] = 3
+    lin.zeros = torch.from_numpy(z)
+    x = torch.full((1, 544), 1e-3, dtype=torch.float16)
+    x[0, ::128] = 6e4
+    pl = packed_linear(lin)
+    y = pl.decode(x.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, x)
+    assert_parity(y, y_ref, bound, "outliers")
+
+
+def test_gemv_config0_single_layer():
+    lins, groups = make_layer(0)
+    lin, x = lins[0], groups["in"].x
+    pl = packed_linear(lin)
+    y = pl.decode(x.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, x)
+    assert_parity(y, y_ref, bound, "config 0")
+
+
+def test_gemv_config1_llama2_13b_layer():
+    lins, groups = make_layer(1, device=dev())
+    for lin in lins:
+        x = groups[lin.group].x
+        pl = packed_linear(lin)
+        y = pl.decode(x.to(dev()))
+        y2 = pl.decode(pl.permute(x.to(dev())), pre_permuted=True)
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2)
+        y_ref, bound = oracle_ref(lin, x)
+        assert_parity(y, y_ref, bound, f"config 1 {lin.name}")
+
+
+@pytest.mark.parametrize("bits", [3, 4, 5, 6])
+@pytest.mark.parametrize("m", [1, 4, 16])
+def test_gemv_config2_budget_sweep(bits, m):
+    """Llama2-13B layer at B in {3,4,5,6}, M in {1,4,16}: 256 seeded rows per linear."""
+    lins, groups = make_layer(2, mix=SWEEP_MIXES[bits], target_bits=bits, m=m, device=dev())
+    rng = np.random.default_rng(bits * 100 + m)
+    for lin in lins:
+        x = groups[lin.group].x
+        pl = packed_linear(lin)
+        assert pl.layout.code_bits == bits * lin.n * lin.k
+        y = pl.decode(x.to(dev()))
+        torch.cuda.synchronize()
+        rows = np.sort(rng.choice(lin.n, 256, replace=False))
+        y_ref, bound = oracle_ref(lin, x, rows=rows)
+        assert_parity(np_(y)[:, rows], y_ref, bound, f"config 2 B={bits} m={m} {lin.name}")
+
+
+@pytest.mark.parametrize("layer", [0, 63])
+def test_gemv_config4_qwen3_32b_layers(layer):
+    """Qwen3-32B layer shapes, both activation variants; layer 0: all rows of the linears up to
+    8192x5120 and 2048 seeded rows of the larger ones; layer 63: 256 seeded rows."""
+    lins, groups = make_layer(4, layer=layer, device=dev())
+    rng = np.random.default_rng(layer)
+    for lin in lins:
+        x = groups[lin.group].x
+        pl = packed_linear(lin)
+        y = pl.decode(x.to(dev()))
+        yp = pl.decode(pl.permute(x.to(dev())), pre_permuted=True)
+        torch.cuda.synchronize()
+        assert torch.equal(y, yp)
+        nrows = lin.n if (layer == 0 and lin.n * lin.k <= 8192 * 5120) else (2048 if layer == 0 else 256)
+        rows = None if nrows == lin.n else np.sort(rng.choice(lin.n, nrows, replace=False))
+        y_ref, bound = oracle_ref(lin, x, rows=rows)
+        yy = np_(y) if rows is None else np_(y)[:, rows]
+        assert_parity(yy, y_ref, bound, f"config 4 layer {layer} {lin.name}")
+
+
+def test_gemv_capacity_errors():
+    lin = random_quant_linear(64, 64, [(2, 64)], seed=1, mode="codes")
+    pl = packed_linear(lin)
+    with pytest.raises(pq.PolyQError):
+        pl.decode(torch.zeros((17, 64), dtype=torch.float16, device=dev()))

@@ -1,0 +1,79 @@
+"""The C-ABI library on the host (no GPU): it loads, exports every symbol the
+header declares, and its planner validates block lists before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_14618_amd as pq
+from paper_2607_14618_amd._lib import Layout, Block
+import oracle
+from synth import snap_counts, MIX_3
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "polyq.h")
+
+
+def test_library_exports_every_declared_symbol():
+    text = open(HEADER).read()
+    declared = set(re.findall(r"\b(polyq_[a-z_]+)\s*\(", text))
+    assert declared == set(pq.EXPORTS)
+    L = pq.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_layout_struct_size_matches_c():
+    # 6 int32, 5 blocks, 2x5 int32, 3x5 int64, 3 int64
+    assert ctypes.sizeof(Layout) == 6 * 4 + 5 * 8 + 10 * 4 + 15 * 8 + 3 * 8
+
+
+@pytest.mark.parametrize("n,k,blocks,err", [
+    (64, 64, [(5, 64)], 2),
+    (64, 64, [(3, 32), (2, 32)], 2),
+    (64, 64, [(2, 32), (2, 32)], 2),
+    (64, 64, [(2, 48), (3, 16)], 3),
+    (64, 64, [(2, 0), (3, 64)], 3),
+    (64, 96, [(2, 64)], 4),
+    (0, 64, [(2, 64)], 4),
+    (64, 64, [], 1),
+])
+def test_plan_rejects_bad_block_lists(n, k, blocks, err):
+    with pytest.raises(pq.PolyQError) as e:
+        pq.plan(n, k, blocks)
+    assert e.value.status == err
+
+
+def test_plan_null_pointers():
+    L = pq.lib()
+    out = Layout()
+    assert L.polyq_plan(64, 64, None, 1, ctypes.byref(out)) == 1
+    arr = (Block * 1)(Block(2, 64))
+    assert L.polyq_plan(64, 64, arr, 1, None) == 1
+
+
+@pytest.mark.parametrize("n,k", [(2048, 2048), (5120, 5120), (13824, 5120), (5120, 13824),
+                                 (1024, 5120), (100, 2048)])
+def test_plan_accounting_matches_the_oracle(n, k):
+    blocks = [(b, c) for b, c in snap_counts(k, MIX_3, 3) if c]
+    L = pq.plan(n, k, blocks)
+    assert L.code_bits == oracle.code_bits(n, blocks)
+    assert L.n_groups == oracle.num_groups(blocks)
+    assert L.weight_bytes == oracle.effective_weight_bytes(n, blocks)
+    tiles = -(-n // 64)
+    assert L.packed_bytes == L.weight_bytes * tiles * 64 // n
+    assert all(o % 256 == 0 for o in L.block_offset[:L.nblocks])
+
+
+def test_workspace_query_is_host_only():
+    L = pq.plan(5120, 5120, [(b, c) for b, c in snap_counts(5120, MIX_3, 3)])
+    for m in (1, 4, 16):
+        assert pq.gemv_workspace_bytes(L, m) >= 0
+    assert pq.gemv_workspace_bytes(L, 17) == 0
+    assert pq.gemm_workspace_bytes(L, 512, True) >= 512 * 5120 * 2
+
+
+def test_status_strings():
+    for s in range(8):
+        assert pq.lib().polyq_status_str(s)
