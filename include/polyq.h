@@ -147,8 +147,9 @@ polyq_status polyq_permute(const int32_t* perm, const uint16_t* x, uint16_t* x_o
  * polyq_gemv -- decode / small-batch product, 1 <= m <= 16 tokens:
  *   y[i][n] = sum_k' w_hat[n][k'] * x[i][perm[k']]   (fp32 accumulation)
  *   packed  buffer written by polyq_pack for `layout`.
- *   perm    int32 [k] (device), or NULL when x is already in clustered order.
- *   x       fp16 [m][k] bits.   y fp32 [m][n], fully overwritten.
+ *   perm    int32 [k] (device, 16-byte aligned), or NULL when x is already in
+ *           clustered order.
+ *   x       fp16 [m][k] bits (16-byte aligned).   y fp32 [m][n], fully overwritten.
  *   workspace / workspace_bytes: device scratch of at least
  *           polyq_gemv_workspace_bytes(layout, m) bytes (may be NULL when that
  *           is 0).  It must be zero-filled before its first use and is left

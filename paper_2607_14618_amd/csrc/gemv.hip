@@ -147,78 +147,77 @@ template <> struct Unpack<8> {
   }
 };
 
-// Load one lane slice (4*B bytes).
+typedef unsigned int u2v __attribute__((ext_vector_type(2)));
+typedef unsigned int u3v __attribute__((ext_vector_type(3)));
+typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+
+// Buffer resource over one tile of one block region (raw, byte-addressed): reads
+// past `bytes` return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint8_t* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), static_cast<short>(0),
+                                           static_cast<int>(bytes), 0x00020000);
+}
+
+// Load one lane slice (4*B bytes) at byte offset voff (per lane) + soff (uniform).
 template <int B>
-__device__ __forceinline__ void load_slice(const uint8_t* p, uint32_t* w) {
+__device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t r, int voff, int soff, uint32_t* w) {
   if constexpr (B == 2) {
-    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    const u2v u = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
     w[0] = u.x; w[1] = u.y;
   } else if constexpr (B == 3) {
-    const uint32_t* q = reinterpret_cast<const uint32_t*>(p);
-    w[0] = q[0]; w[1] = q[1]; w[2] = q[2];
+    const u3v u = __builtin_amdgcn_raw_buffer_load_b96(r, voff, soff, 0);
+    w[0] = u.x; w[1] = u.y; w[2] = u.z;
   } else {
 #pragma unroll
     for (int i = 0; i < B / 4; ++i) {
-      const uint4 u = reinterpret_cast<const uint4*>(p)[i];
+      const u4v u = __builtin_amdgcn_raw_buffer_load_b128(r, voff + 16 * i, soff, 0);
       w[4 * i + 0] = u.x; w[4 * i + 1] = u.y; w[4 * i + 2] = u.z; w[4 * i + 3] = u.w;
     }
   }
 }
 
-// Batch geometry per bit-width: a batch is up to NB chunks of one group whose
-// slices (16 dwords at most) are loaded together; two batches are in flight per
-// wave (the next one is loaded while the current one is unpacked).
+// Ring geometry per bit-width: a slot holds the lane slices of up to NS chunks
+// (at most 16 dwords per lane); slots end on multiples of NS chunks of the
+// block's group grid, so every slot but a segment's first starts aligned.
 template <int B>
 struct Geo {
-  static constexpr int NB = B <= 4 ? 4 : (B == 8 ? 2 : 1);  // chunks per batch
-  static constexpr int CB = 4 * B;                           // bytes per lane slice
+  static constexpr int NS = B == 2 ? 8 : (B <= 4 ? 4 : (B == 8 ? 2 : 1));  // chunks per slot
+  static constexpr int CB = 4 * B;                                          // bytes per lane slice
   static constexpr int META = B <= 8 ? kMetaBytes : 0;
 };
 
-struct Buf {
-  uint32_t w[16];  // NB slices of B dwords each
-  uint32_t z[2];   // z of the lane's 4 dequantized rows (fp16), b <= 8
-  uint32_t s[8];   // s of the lane's 16 accumulator rows (fp16), b <= 8
+struct Slot {
+  uint32_t w[16];
 };
 
-// End (exclusive) of the batch that starts at block-local chunk c.
+// End (exclusive) of the slot that starts at block-local chunk c.
 template <int B>
-__device__ __forceinline__ int batch_end(int c, int l1) {
-  if constexpr (B == 16) {
-    return c + 1;
-  } else {
-    return min(min(c + Geo<B>::NB, (c | 3) + 1), l1);
-  }
+__device__ __forceinline__ int slot_end(int c, int l1) {
+  constexpr int NS = Geo<B>::NS;
+  return min((c / NS) * NS + NS, l1);
 }
 
-// Issue the loads of the batch [c, cend) of one tile (slots past cend re-read chunk c).
+// Issue the loads of the slot [c, ce) of one tile.  Register slice j holds
+// aligned position (c/NS)*NS + j; positions outside [c, ce) re-read chunk c.
 template <int B>
-__device__ __forceinline__ void issue(Buf& b, const uint8_t* __restrict__ tile_base,
-                                      int64_t record_bytes, int c, int cend, int lane) {
+__device__ __forceinline__ void issue(Slot& sl, __amdgpu_buffer_rsrc_t r, int record_bytes, int c,
+                                      int ce, int lane) {
   using G = Geo<B>;
-  const uint8_t* rec = tile_base + (c >> 2) * record_bytes;
-  if constexpr (B <= 8) {
-    const uint2 zz = *reinterpret_cast<const uint2*>(rec + (lane & 15) * 8);
-    b.z[0] = zz.x; b.z[1] = zz.y;
-    const uint4* sp = reinterpret_cast<const uint4*>(rec + 128 + (lane >> 4) * 32);
-    const uint4 s0 = sp[0], s1 = sp[1];
-    b.s[0] = s0.x; b.s[1] = s0.y; b.s[2] = s0.z; b.s[3] = s0.w;
-    b.s[4] = s1.x; b.s[5] = s1.y; b.s[6] = s1.z; b.s[7] = s1.w;
-  }
-  const uint8_t* slices = rec + G::META + lane * G::CB;
+  const int base = (c / G::NS) * G::NS;
 #pragma unroll
-  for (int j = 0; j < G::NB; ++j) {
-    const int cj = (c + j < cend) ? c + j : c;
-    load_slice<B>(slices + (cj & 3) * (64 * G::CB), &b.w[j * B]);
+  for (int j = 0; j < G::NS; ++j) {
+    const int pos = base + j;
+    const int cj = (pos >= c && pos < ce) ? pos : c;
+    load_slice<B>(r, lane * G::CB, (cj >> 2) * record_bytes + G::META + (cj & 3) * (64 * G::CB),
+                  &sl.w[j * B]);
   }
 }
 
 struct Group {
-  h2 c1[16];     // per pair: -(offset + z_row) (integer z) or -offset
-  h2 c2[4];      // per row: -z (non-integer z only)
-  float s[16];   // scale of each accumulator row
+  h2 c1[16];  // per pair: -(offset + z_row) (integer z) or -offset
+  h2 nz[4];   // per row: -z
   bool exact;
-  f4 part[4];    // this group's accumulators, one per 16-row sub-tile
+  f4 part[4];  // this group's accumulators, one per 16-row sub-tile
 };
 
 __device__ __forceinline__ h8 frag(const uint32_t* w4) {
@@ -237,7 +236,7 @@ __device__ __forceinline__ void quant_slice(const uint32_t* w, h8 xb, Group& gs)
 #pragma unroll
   for (int P = 0; P < 16; ++P) {
     h2 t = as_h2(v[P]) + gs.c1[P];
-    if constexpr (!kExactZ) t = t + gs.c2[P >> 2];
+    if constexpr (!kExactZ) t = t + gs.nz[P >> 2];
     d[P] = as_u32(t);
   }
 #pragma unroll
@@ -245,140 +244,263 @@ __device__ __forceinline__ void quant_slice(const uint32_t* w, h8 xb, Group& gs)
     gs.part[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(frag(&d[4 * r]), xb, gs.part[r], 0, 0, 0);
 }
 
-// Unpack and accumulate the batch [c, cend) of a segment [l0, l1).  `xlane`
-// points at this lane's activation fragment of block-local chunk l0 (LDS).
+// Unpack and accumulate the slot [c, ce) of a segment [l0, l1).  `xlane` is
+// this lane's activation fragment of block-local chunk 0 (LDS); `meta` is the
+// LDS copy of the metadata of block-local group 0.
 template <int B>
-__device__ __forceinline__ void compute(const Buf& b, int c, int cend, int l0, int l1,
-                                        const uint32_t* xlane, Group& gs, f4 (&acc)[4]) {
+__device__ __forceinline__ void compute(const Slot& sl, int c, int ce, int l0, int l1,
+                                        const uint32_t* xlane, const uint8_t* meta, int lane,
+                                        Group& gs, f4 (&acc)[4]) {
   using G = Geo<B>;
-  if constexpr (B == 16) {
-    const h8 xb = __builtin_bit_cast(h8, *reinterpret_cast<const uint4*>(xlane + (c - l0) * 16));
+  const int base = (c / G::NS) * G::NS;
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(frag(&b.w[4 * r]), xb, acc[r], 0, 0, 0);
-  } else {
-    using U = Unpack<B>;
-    if ((c & 3) == 0 || c == l0) {  // first batch of a group (or of the segment)
-      float z[4];
+  for (int j = 0; j < G::NS; ++j) {
+    const int pos = base + j;
+    if (pos < c || pos >= ce) continue;
+    const h8 xb = __builtin_bit_cast(h8, *reinterpret_cast<const uint4*>(xlane + pos * 16));
+    if constexpr (B == 16) {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        z[r] = static_cast<float>(__builtin_bit_cast(
-            _Float16, static_cast<uint16_t>(b.z[r >> 1] >> (16 * (r & 1)))));
-      bool ok = true;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) ok = ok && (z[r] == truncf(z[r])) && fabsf(z[r]) <= 1023.f;
-      // integer zero points (the asymmetric quantizer's): one exact add per pair
-      gs.exact = __all(ok);
-#pragma unroll
-      for (int P = 0; P < 16; ++P)
-        gs.c1[P] = gs.exact ? splat(-(U::offset[U::which[P]] + z[P >> 2])) : splat(-U::offset[U::which[P]]);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) gs.c2[r] = splat(-z[r]);
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        gs.s[i] = static_cast<float>(__builtin_bit_cast(
-            _Float16, static_cast<uint16_t>(b.s[i >> 1] >> (16 * (i & 1)))));
-#pragma unroll
-      for (int r = 0; r < 4; ++r) gs.part[r] = f4{0.f, 0.f, 0.f, 0.f};
-    }
-    if (gs.exact) {
-#pragma unroll
-      for (int j = 0; j < G::NB; ++j) {
-        if (c + j < cend) {
-          const h8 xb = __builtin_bit_cast(h8, *reinterpret_cast<const uint4*>(xlane + (c + j - l0) * 16));
-          quant_slice<B, true>(&b.w[j * B], xb, gs);
-        }
-      }
+        acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(frag(&sl.w[j * B + 4 * r]), xb, acc[r], 0, 0, 0);
     } else {
+      using U = Unpack<B>;
+      const uint8_t* gm = meta + (pos >> 2) * kMetaBytes;
+      if ((pos & 3) == 0 || pos == l0) {  // group start: zero points -> pair constants
+        const uint2 zz = *reinterpret_cast<const uint2*>(gm + (lane & 15) * 8);
+        float z[4];
 #pragma unroll
-      for (int j = 0; j < G::NB; ++j) {
-        if (c + j < cend) {
-          const h8 xb = __builtin_bit_cast(h8, *reinterpret_cast<const uint4*>(xlane + (c + j - l0) * 16));
-          quant_slice<B, false>(&b.w[j * B], xb, gs);
-        }
+        for (int r = 0; r < 4; ++r)
+          z[r] = static_cast<float>(__builtin_bit_cast(
+              _Float16, static_cast<uint16_t>((r < 2 ? zz.x : zz.y) >> (16 * (r & 1)))));
+        bool ok = true;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ok = ok && (z[r] == truncf(z[r])) && fabsf(z[r]) <= 1023.f;
+        // integer zero points (the asymmetric quantizer's): one exact add per pair
+        gs.exact = __all(ok);
+#pragma unroll
+        for (int P = 0; P < 16; ++P)
+          gs.c1[P] = gs.exact ? splat(-(U::offset[U::which[P]] + z[P >> 2]))
+                              : splat(-U::offset[U::which[P]]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gs.nz[r] = splat(-z[r]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gs.part[r] = f4{0.f, 0.f, 0.f, 0.f};
       }
-    }
-    if ((cend & 3) == 0 || cend == l1) {  // group complete: apply its scales once
+      if (gs.exact)
+        quant_slice<B, true>(&sl.w[j * B], xb, gs);
+      else
+        quant_slice<B, false>(&sl.w[j * B], xb, gs);
+      if ((pos & 3) == 3 || pos == l1 - 1) {  // group end: apply the row scales once
+        const uint4* sp = reinterpret_cast<const uint4*>(gm + 128 + (lane >> 4) * 32);
+        const uint4 s0 = sp[0], s1 = sp[1];
+        const uint32_t sw[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+        for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[r][e] = fmaf(gs.s[4 * r + e], gs.part[r][e], acc[r][e]);
+          for (int e = 0; e < 4; ++e) {
+            const int i = 4 * r + e;
+            const float sc = static_cast<float>(
+                __builtin_bit_cast(_Float16, static_cast<uint16_t>(sw[i >> 1] >> (16 * (i & 1)))));
+            acc[r][e] = fmaf(sc, gs.part[r][e], acc[r][e]);
+          }
+      }
     }
   }
 }
 
-// Block-local chunks [l0, l1) of one tile: two batches in flight (ping-pong).
-// `b0` already holds the first batch when `preloaded`.  The next batch is always
-// issued (at the segment end it re-reads the current one, an L1/L2 hit), so the
-// number of loads between a batch's issue and its use is fixed and the wait
-// before each compute covers only the older batch.
+// Block-local chunks [l0, l1) of one tile through a three-slot ring: while a
+// slot is unpacked the next two are in flight.  A slot is always issued (past
+// the segment end it re-reads the last chunk, an L1/L2 hit), so the number of
+// loads between a slot's issue and its use is fixed and each wait leaves the
+// two younger slots outstanding.  `sa`/`sb` already hold the first two slots
+// when `preloaded`.
 template <int B>
-__device__ __forceinline__ void run_segment(const uint8_t* __restrict__ tile_base,
-                                            int64_t record_bytes, int l0, int l1,
-                                            const uint32_t* xlane, int lane, Buf& b0,
-                                            bool preloaded, f4 (&acc)[4]) {
-  Buf b1;
+__device__ __forceinline__ void run_segment(__amdgpu_buffer_rsrc_t rs, int record_bytes, int l0,
+                                            int l1, const uint32_t* xlane, const uint8_t* meta,
+                                            int lane, Slot& sa, Slot& sb, bool preloaded,
+                                            f4 (&acc)[4]) {
+  Slot sc;
   Group gs;
-  int c = l0;
-  int ce = batch_end<B>(c, l1);
-  if (!preloaded) issue<B>(b0, tile_base, record_bytes, c, ce, lane);
+  int c0 = l0, e0 = slot_end<B>(c0, l1);
+  int c1 = e0 < l1 ? e0 : c0, e1 = e0 < l1 ? slot_end<B>(c1, l1) : e0;
+  if (!preloaded) {
+    issue<B>(sa, rs, record_bytes, c0, e0, lane);
+    issue<B>(sb, rs, record_bytes, c1, e1, lane);
+  }
   for (;;) {
-    int cn = ce < l1 ? ce : c;
-    int cne = ce < l1 ? batch_end<B>(cn, l1) : ce;
-    issue<B>(b1, tile_base, record_bytes, cn, cne, lane);
-    compute<B>(b0, c, ce, l0, l1, xlane, gs, acc);
-    if (ce >= l1) break;
-    c = cn;
-    ce = cne;
-    cn = ce < l1 ? ce : c;
-    cne = ce < l1 ? batch_end<B>(cn, l1) : ce;
-    issue<B>(b0, tile_base, record_bytes, cn, cne, lane);
-    compute<B>(b1, c, ce, l0, l1, xlane, gs, acc);
-    if (ce >= l1) break;
-    c = cn;
-    ce = cne;
+    int c2 = e1 < l1 ? e1 : c1, e2 = e1 < l1 ? slot_end<B>(c2, l1) : e1;
+    issue<B>(sc, rs, record_bytes, c2, e2, lane);
+    compute<B>(sa, c0, e0, l0, l1, xlane, meta, lane, gs, acc);
+    if (e0 >= l1) break;
+    c0 = c1; e0 = e1; c1 = c2; e1 = e2;
+    c2 = e1 < l1 ? e1 : c1; e2 = e1 < l1 ? slot_end<B>(c2, l1) : e1;
+    issue<B>(sa, rs, record_bytes, c2, e2, lane);
+    compute<B>(sb, c0, e0, l0, l1, xlane, meta, lane, gs, acc);
+    if (e0 >= l1) break;
+    c0 = c1; e0 = e1; c1 = c2; e1 = e2;
+    c2 = e1 < l1 ? e1 : c1; e2 = e1 < l1 ? slot_end<B>(c2, l1) : e1;
+    issue<B>(sb, rs, record_bytes, c2, e2, lane);
+    compute<B>(sc, c0, e0, l0, l1, xlane, meta, lane, gs, acc);
+    if (e0 >= l1) break;
+    c0 = c1; e0 = e1; c1 = c2; e1 = e2;
   }
 }
+
+template <int B>
+__device__ __forceinline__ void preload(__amdgpu_buffer_rsrc_t rs, int rb, int l0, int l1,
+                                        int lane, Slot& sa, Slot& sb) {
+  const int e0 = slot_end<B>(l0, l1);
+  const int c1 = e0 < l1 ? e0 : l0, e1 = e0 < l1 ? slot_end<B>(c1, l1) : e0;
+  issue<B>(sa, rs, rb, l0, e0, lane);
+  issue<B>(sb, rs, rb, c1, e1, lane);
+}
+
+// Dword `i` (compile-time) of the kernel-argument block, from the copy held one
+// dword per lane, as a scalar.
+#define KARG(T, field) kfield<T>(kv, offsetof(GemvArgs, field) / 4)
+template <class T>
+__device__ __forceinline__ T kfield(uint32_t kv, int dw) {
+  if constexpr (sizeof(T) == 8) {
+    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(kv, dw));
+    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(kv, dw + 1));
+    return __builtin_bit_cast(T, lo | (hi << 32));
+  } else {
+    return __builtin_bit_cast(T, static_cast<uint32_t>(__builtin_amdgcn_readlane(kv, dw)));
+  }
+}
+
+// Block descriptors, read from the per-lane copy of the argument block with
+// v_readlane at a uniform (possibly run-time) lane index: no dependent loads, and
+// no indexed private array for the compiler to spill to scratch memory.
+struct Blocks {
+  uint32_t kv;
+  __device__ int bits(int i) const { return kfield<int32_t>(kv, offsetof(GemvArgs, bits) / 4 + i); }
+  __device__ int cb(int i) const { return kfield<int32_t>(kv, offsetof(GemvArgs, chunk_begin) / 4 + i); }
+  __device__ int ce(int i) const { return kfield<int32_t>(kv, offsetof(GemvArgs, chunk_end) / 4 + i); }
+  __device__ int64_t off(int i) const {
+    return kfield<int64_t>(kv, offsetof(GemvArgs, block_offset) / 4 + 2 * i);
+  }
+  __device__ int64_t tb(int i) const {
+    return kfield<int64_t>(kv, offsetof(GemvArgs, tile_bytes) / 4 + 2 * i);
+  }
+  __device__ int rb(int i) const {
+    return kfield<int32_t>(kv, offsetof(GemvArgs, record_bytes) / 4 + 2 * i);
+  }
+};
 
 __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   extern __shared__ uint32_t smem[];
   const int tile = blockIdx.x, s = blockIdx.y;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  const int m = a.m;
-  const int cw0 = a.split[s * kWaves], cw1 = a.split[(s + 1) * kWaves];
+  // The argument block is read with two vector loads (one dword per lane: the
+  // first 256 bytes, and this wave's split entries) and broadcast with
+  // v_readlane; scalar loads of it would miss the scalar cache line by line.
+  const uint32_t* kargs = (const uint32_t*)(__builtin_amdgcn_kernarg_segment_ptr());
+  static_assert(offsetof(GemvArgs, split) == 256, "argument block layout");
+  const uint32_t kv = kargs[lane];
+  const uint32_t ks = kargs[64 + s * kWaves + min(lane, kWaves)];
+  const int m = KARG(int32_t, m);
+  const int cw0 = __builtin_amdgcn_readlane(ks, 0), cw1 = __builtin_amdgcn_readlane(ks, kWaves);
   const int range = (cw1 - cw0) * kChunk;  // staged channels
   const int kbase = cw0 * kChunk;
-  const int c0 = a.split[s * kWaves + wave], c1 = a.split[s * kWaves + wave + 1];
-
-  // Start streaming this wave's first weight batch before staging x'.
+  int c0 = cw0, c1 = cw0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int lo = __builtin_amdgcn_readlane(ks, w), hi = __builtin_amdgcn_readlane(ks, w + 1);
+    c0 = (w == wave) ? lo : c0;
+    c1 = (w == wave) ? hi : c1;
+  }
+  const Blocks bd{kv};
+  const int nblocks = KARG(int32_t, nblocks);
+  const uint8_t* packed = KARG(const uint8_t*, packed);
+  const int32_t* perm = KARG(const int32_t*, perm);
+  const uint16_t* xg = KARG(const uint16_t*, x);
+  const int kdim = KARG(int32_t, k);
+  // Start streaming this wave's first two slots before staging x' and metadata.
   int first = 0;
-  while (first < a.nblocks && a.chunk_end[first] <= c0) ++first;
-  Buf b0;
+#pragma unroll
+  for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) first += (i < nblocks && bd.ce(i) <= c0) ? 1 : 0;
+  Slot sa, sb;
   bool preloaded = false;
-  if (c0 < c1 && first < a.nblocks) {
-    const int l0 = c0 - a.chunk_begin[first];
-    const int l1 = min(c1, a.chunk_end[first]) - a.chunk_begin[first];
-    const uint8_t* tile_base = a.packed + a.block_offset[first] + tile * a.tile_bytes[first];
-    const int64_t rb = a.record_bytes[first];
+  if (c0 < c1 && first < nblocks) {
+    const int fb = bd.bits(first), fcb = bd.cb(first);
+    const int hi = min(c1, bd.ce(first));
+    const __amdgpu_buffer_rsrc_t rs =
+        tile_rsrc(packed + bd.off(first) + tile * bd.tb(first), bd.tb(first));
+    const int rb = bd.rb(first);
     preloaded = true;
-    switch (a.bits[first]) {
-      case 2: issue<2>(b0, tile_base, rb, l0, batch_end<2>(l0, l1), lane); break;
-      case 3: issue<3>(b0, tile_base, rb, l0, batch_end<3>(l0, l1), lane); break;
-      case 4: issue<4>(b0, tile_base, rb, l0, batch_end<4>(l0, l1), lane); break;
-      case 8: issue<8>(b0, tile_base, rb, l0, batch_end<8>(l0, l1), lane); break;
-      default: issue<16>(b0, tile_base, rb, l0, batch_end<16>(l0, l1), lane); break;
+    switch (fb) {
+      case 2: preload<2>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
+      case 3: preload<3>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
+      case 4: preload<4>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
+      case 8: preload<8>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
+      default: preload<16>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
     }
   }
 
-  // Stage x'[i][k'] = x[i][perm[k']] for this work-group's clustered channels
-  // (rows 0..m-1) and a zero row m read by the MFMA columns of absent tokens.
+  // LDS: x' rows 0..m-1, a zero row m (MFMA columns of absent tokens), then the
+  // metadata of every group the work-group touches.
   uint16_t* xs16 = reinterpret_cast<uint16_t*>(smem);
-  for (int kk = threadIdx.x; kk < range; kk += blockDim.x) {
-    const int kp = kbase + kk;
-    const int src = a.perm != nullptr ? a.perm[kp] : kp;
-    const bool ok = static_cast<unsigned>(src) < static_cast<unsigned>(a.k);
-    for (int mi = 0; mi < m; ++mi) xs16[mi * range + kk] = ok ? a.x[static_cast<int64_t>(mi) * a.k + src] : 0;
-    xs16[m * range + kk] = 0;
+  uint8_t* meta_lds = reinterpret_cast<uint8_t*>(smem) + static_cast<size_t>(m + 1) * range * 2;
+
+  // Metadata: group records of the blocks with b <= 8 that overlap [cw0, cw1),
+  // copied 16 bytes per thread and round.
+  {
+    int slot0 = 0;
+#pragma unroll
+    for (int bi = 0; bi < POLYQ_MAX_BLOCKS; ++bi) {
+      if (bi >= nblocks || bd.bits(bi) > 8) continue;
+      const int lo = max(cw0, bd.cb(bi)), hi = min(cw1, bd.ce(bi));
+      if (lo >= hi) continue;
+      const int g0 = (lo - bd.cb(bi)) >> 2, g1 = ((hi - 1 - bd.cb(bi)) >> 2) + 1;
+      const uint8_t* tile_base = packed + bd.off(bi) + tile * bd.tb(bi);
+      const int pieces = (g1 - g0) * (kMetaBytes / 16);
+      for (int i = threadIdx.x; i < pieces; i += blockDim.x) {
+        const int g = g0 + i / (kMetaBytes / 16), o = (i % (kMetaBytes / 16)) * 16;
+        *reinterpret_cast<uint4*>(meta_lds + (slot0 + g - g0) * kMetaBytes + o) =
+            *reinterpret_cast<const uint4*>(tile_base + g * bd.rb(bi) + o);
+      }
+      slot0 += g1 - g0;
+    }
+  }
+
+  // x'[i][k'] = x[i][perm[k']] for this work-group's clustered channels.  Each
+  // thread takes 8 consecutive channels per round of 2048: two 16-byte perm
+  // loads, then all of its gathers before any LDS store, so a round costs two
+  // memory latencies (one without a permutation).
+  for (int kk0 = threadIdx.x * 8; kk0 < range; kk0 += blockDim.x * 8) {
+    const int kp0 = kbase + kk0;
+    if (perm != nullptr) {
+      const int4* pp = reinterpret_cast<const int4*>(perm + kp0);
+      const int4 p0 = pp[0], p1 = pp[1];
+      const int src[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+      for (int mi = 0; mi < m; mi += 2) {
+        uint16_t v[2][8];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const bool ok = mi + u < m && static_cast<unsigned>(src[e]) < static_cast<unsigned>(kdim);
+            v[u][e] = ok ? xg[static_cast<int64_t>(mi + u) * kdim + src[e]] : 0;
+          }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          if (mi + u < m) {
+            uint4 q;
+            q.x = v[u][0] | (static_cast<uint32_t>(v[u][1]) << 16);
+            q.y = v[u][2] | (static_cast<uint32_t>(v[u][3]) << 16);
+            q.z = v[u][4] | (static_cast<uint32_t>(v[u][5]) << 16);
+            q.w = v[u][6] | (static_cast<uint32_t>(v[u][7]) << 16);
+            *reinterpret_cast<uint4*>(xs16 + (mi + u) * range + kk0) = q;
+          }
+        }
+      }
+    } else {
+      for (int mi = 0; mi < m; ++mi)
+        *reinterpret_cast<uint4*>(xs16 + mi * range + kk0) =
+            *reinterpret_cast<const uint4*>(xg + static_cast<int64_t>(mi) * kdim + kp0);
+    }
+    *reinterpret_cast<uint4*>(xs16 + m * range + kk0) = uint4{0u, 0u, 0u, 0u};
   }
   __syncthreads();
 
@@ -388,20 +510,39 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   const int tok = lane & 15;
   // this lane's activation row (token lane%16, or the zero row) and channel quarter
   const uint32_t* xrow = smem + ((tok < m ? tok : m) * range + 8 * (lane >> 4)) / 2;
-  for (int bi = first; bi < a.nblocks; ++bi) {
-    const int lo = max(c0, a.chunk_begin[bi]), hi = min(c1, a.chunk_end[bi]);
+  // LDS metadata slot of the first staged group of each block
+  int meta_slot = 0;
+#pragma unroll
+  for (int bi = 0; bi < POLYQ_MAX_BLOCKS; ++bi) {
+    if (bi >= first || bd.bits(bi) > 8) continue;
+    const int lo = max(cw0, bd.cb(bi)), hi = min(cw1, bd.ce(bi));
+    if (lo < hi) meta_slot += ((hi - 1 - bd.cb(bi)) >> 2) + 1 - ((lo - bd.cb(bi)) >> 2);
+  }
+  for (int bi = first; bi < nblocks; ++bi) {
+    const int bits = bd.bits(bi), cb = bd.cb(bi), ce = bd.ce(bi);
+    const int lo = max(c0, cb), hi = min(c1, ce);
     if (lo >= hi) break;
-    const uint8_t* tile_base = a.packed + a.block_offset[bi] + tile * a.tile_bytes[bi];
-    const int l0 = lo - a.chunk_begin[bi], l1 = hi - a.chunk_begin[bi];
-    const uint32_t* xlane = xrow + (lo - cw0) * 16;
-    const int64_t rb = a.record_bytes[bi];
+    const int64_t tb = bd.tb(bi);
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(packed + bd.off(bi) + tile * tb, tb);
+    const int rb = bd.rb(bi);
+    const int l0 = lo - cb, l1 = hi - cb;
+    // block-local chunk 0 of this block, relative to the staged range
+    const uint32_t* xlane = xrow + (cb - cw0) * 16;
+    // LDS metadata of block-local group 0 (the work-group staged this block's
+    // groups from the one holding max(cw0, block start))
+    const int wg_lo = max(cw0, cb);
+    const uint8_t* meta = meta_lds + (meta_slot - ((wg_lo - cb) >> 2)) * kMetaBytes;
     const bool pre = preloaded && bi == first;
-    switch (a.bits[bi]) {
-      case 2: run_segment<2>(tile_base, rb, l0, l1, xlane, lane, b0, pre, acc); break;
-      case 3: run_segment<3>(tile_base, rb, l0, l1, xlane, lane, b0, pre, acc); break;
-      case 4: run_segment<4>(tile_base, rb, l0, l1, xlane, lane, b0, pre, acc); break;
-      case 8: run_segment<8>(tile_base, rb, l0, l1, xlane, lane, b0, pre, acc); break;
-      default: run_segment<16>(tile_base, rb, l0, l1, xlane, lane, b0, pre, acc); break;
+    switch (bits) {
+      case 2: run_segment<2>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
+      case 3: run_segment<3>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
+      case 4: run_segment<4>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
+      case 8: run_segment<8>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
+      default: run_segment<16>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
+    }
+    if (bits <= 8) {
+      const int whi = min(cw1, ce);
+      meta_slot += ((whi - 1 - cb) >> 2) + 1 - ((wg_lo - cb) >> 2);
     }
   }
 
@@ -474,8 +615,9 @@ extern "C" polyq_status polyq_gemv(const polyq_layout* layout, const void* packe
   const polyq_layout& L = *layout;
   if (packed == nullptr || x == nullptr || y == nullptr) return POLYQ_ERR_ARG;
   if (reinterpret_cast<uintptr_t>(packed) % 256 != 0) return POLYQ_ERR_ARG;
-  if (reinterpret_cast<uintptr_t>(x) % 2 != 0 || reinterpret_cast<uintptr_t>(y) % 4 != 0)
-    return POLYQ_ERR_ARG;
+  if (reinterpret_cast<uintptr_t>(x) % 16 != 0 || reinterpret_cast<uintptr_t>(y) % 4 != 0 ||
+      reinterpret_cast<uintptr_t>(perm) % 16 != 0)
+    return POLYQ_ERR_ARG;  // activations and permutation are read as 16-byte vectors
   if (m < 1) return POLYQ_ERR_ARG;
   if (m > POLYQ_MAX_M_GEMV) return POLYQ_ERR_CAPACITY;
   GemvPlan plan;

@@ -13,7 +13,7 @@ bool bits_in_palette(int b) { return b == 2 || b == 3 || b == 4 || b == 8 || b =
 
 // GEMV work split knobs.
 constexpr int kWavesPerWG = 4;
-constexpr int kTargetWGs = 1024;          // 256 CUs x 4 resident work-groups
+constexpr int kResidentWGs = 512;        // 256 CUs x 2 co-resident 4-wave work-groups
 constexpr int kMinChunksPerWave = 4;      // below this the per-wave setup dominates
 constexpr size_t kLdsBudget = 64 * 1024;  // per work-group
 
@@ -95,9 +95,23 @@ bool layout_is_valid(const polyq_layout* L) {
 }
 
 size_t gemv_lds_bytes(const GemvPlan& p, int32_t m) {
-  const size_t xs = static_cast<size_t>(p.lds_chunks) * kChunk * (m + 1) * 2;  // + a zero row
+  // x' rows + a zero row, then the staged group metadata; reused for the reduction
+  const size_t xs = static_cast<size_t>(p.lds_chunks) * kChunk * (m + 1) * 2 +
+                    static_cast<size_t>(p.lds_groups) * kMetaBytes;
   const size_t red = static_cast<size_t>(p.W) * m * kTileRows * 4;
   return std::max(xs, red);
+}
+
+// Group records of b <= 8 blocks that overlap the chunk range [lo, hi).
+static int groups_touched(const polyq_layout& L, int lo, int hi) {
+  int n = 0;
+  for (int i = 0; i < L.nblocks; ++i) {
+    if (L.block[i].bits > 8) continue;
+    const int b0 = L.k_begin[i] / kChunk, b1 = b0 + L.block[i].len / kChunk;
+    const int a = std::max(lo, b0), b = std::min(hi, b1);
+    if (a < b) n += ((b - 1 - b0) >> 2) + 1 - ((a - b0) >> 2);
+  }
+  return n;
 }
 
 static void partition(const std::vector<int64_t>& prefix, int parts, int32_t* split) {
@@ -117,30 +131,79 @@ static void partition(const std::vector<int64_t>& prefix, int parts, int32_t* sp
   split[parts] = C;
 }
 
+// Cost of one 32-channel chunk of a 64-row tile, in units of 64 bytes (codes +
+// the chunk's share of its group's 256-byte metadata).
+static int64_t chunk_cost(int bits) { return 4 * bits + (bits <= 8 ? 1 : 0); }
+
+// `parts` waves per tile with every wave inside one block: waves are given to
+// blocks in proportion to their bytes (at least one each, at most one per
+// chunk) and each block's chunks are split evenly among its waves.  Returns
+// false when there are fewer waves than blocks.
+static bool partition_by_block(const polyq_layout& L, int parts, int32_t* split) {
+  const int nb = L.nblocks;
+  if (parts < nb) return false;
+  int64_t cost[POLYQ_MAX_BLOCKS], total = 0;
+  int nch[POLYQ_MAX_BLOCKS], n[POLYQ_MAX_BLOCKS], used = 0;
+  for (int i = 0; i < nb; ++i) {
+    nch[i] = L.block[i].len / kChunk;
+    cost[i] = nch[i] * chunk_cost(L.block[i].bits);
+    total += cost[i];
+  }
+  for (int i = 0; i < nb; ++i) {
+    n[i] = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(nch[i], parts * cost[i] / total)));
+    used += n[i];
+  }
+  while (used < parts) {  // next wave to the block with the most bytes per wave
+    int best = -1;
+    for (int i = 0; i < nb; ++i)
+      if (n[i] < nch[i] && (best < 0 || cost[i] * n[best] > cost[best] * n[i])) best = i;
+    if (best < 0) break;
+    ++n[best];
+    ++used;
+  }
+  while (used > parts) {  // take a wave from the block with the fewest bytes per wave
+    int best = -1;
+    for (int i = 0; i < nb; ++i)
+      if (n[i] > 1 && (best < 0 || cost[i] * n[best] < cost[best] * n[i])) best = i;
+    --n[best];
+    --used;
+  }
+  int u = 0;
+  split[0] = 0;
+  for (int i = 0; i < nb; ++i) {
+    const int c0 = L.k_begin[i] / kChunk;
+    for (int j = 0; j < n[i]; ++j) split[++u] = c0 + static_cast<int>(static_cast<int64_t>(nch[i]) * (j + 1) / n[i]);
+  }
+  for (; u < parts; ++u) split[u + 1] = L.n_chunks;  // waves left without work
+  return true;
+}
+
 int plan_gemv(const polyq_layout& L, int32_t m, GemvPlan* p) {
   const int C = L.n_chunks, T = L.n_tiles;
   std::vector<int64_t> prefix(C + 1, 0);
   for (int i = 0; i < L.nblocks; ++i) {
     const int b = L.block[i].bits;
     const int c0 = L.k_begin[i] / kChunk, nc = L.block[i].len / kChunk;
-    for (int c = 0; c < nc; ++c) {
-      int64_t cost = static_cast<int64_t>(kTileRows) * 4 * b;
-      if (b <= 8 && c % kChunksPerGroup == 0) cost += kMetaBytes;
-      prefix[c0 + c + 1] = prefix[c0 + c] + cost;
-    }
+    for (int c = 0; c < nc; ++c) prefix[c0 + c + 1] = prefix[c0 + c] + chunk_cost(b);
   }
   const int W = kWavesPerWG;
-  int S = (kTargetWGs + T - 1) / T;
+  // One round of co-resident work-groups: splits beyond that only add a second
+  // round of prologue and fix-up latency.
+  int S = std::max(1, kResidentWGs / T);
   S = std::min(S, std::max(1, C / (W * kMinChunksPerWave)));
   S = std::max(1, std::min(S, kMaxSplitEntries / W));
   for (;;) {
     p->S = S;
     p->W = W;
     p->nsplit = S * W;
-    partition(prefix, S * W, p->split);
-    int worst = 0;
-    for (int s = 0; s < S; ++s) worst = std::max(worst, p->split[(s + 1) * W] - p->split[s * W]);
+    if (!partition_by_block(L, S * W, p->split)) partition(prefix, S * W, p->split);
+    int worst = 0, worst_groups = 0;
+    for (int s = 0; s < S; ++s) {
+      worst = std::max(worst, p->split[(s + 1) * W] - p->split[s * W]);
+      worst_groups = std::max(worst_groups, groups_touched(L, p->split[s * W], p->split[(s + 1) * W]));
+    }
     p->lds_chunks = worst;
+    p->lds_groups = worst_groups;
     if (gemv_lds_bytes(*p, m) <= kLdsBudget) return 0;
     if (S * W >= kMaxSplitEntries || S >= C) return 1;
     ++S;
