@@ -1,17 +1,24 @@
 #!/usr/bin/env python3
-"""Benchmark of the mixed-bit decode GEMV (and, as secondary figures, the
-prefill GEMM) on one MI355X.
+"""Benchmark of the mixed-bit decode GEMV (headline) and prefill GEMM on one MI355X.
 
-Default workload: one Llama2-13B-shaped decoder layer at batch 1 (q/k/v/o
+Headline workload: one Llama2-13B-shaped decoder layer at batch 1 (q/k/v/o
 5120x5120, gate/up 13824x5120, down 5120x13824), every linear at a 3.0-bit
 average budget (2/3/4/8/16 b channel mix), fp16 activations with 1 % outlier
 channels, channel permutation gathered inside the kernel.  A step is the seven
-GEMVs of the layer.  Inputs are resident in HBM; the step cycles through enough
-distinct copies of the packed layer (>= 1.2 GB) that the 256 MB Infinity
-Cache cannot serve the weights.
+GEMVs of the layer.  Inputs are resident in HBM; consecutive steps cycle through
+enough distinct copies of the packed layer (>= 1.2 GB) that the 256 MB
+Infinity Cache cannot serve the weights.
 
-Prints one JSON line (rank 0).  `value` = effective weight GB/s = algorithmic
-weight bytes of the step (codes + fp16 scale/zero) / step time.
+`value` = effective weight GB/s = algorithmic weight bytes of the step (codes
++ fp16 scale/zero, Eq. 7 budget) / step time.  The same JSON line carries the
+roofline of the GEMV kernel (bytes per launch / average launch time from HIP
+events on the launch stream), the prefill GEMM at M=512 (4.0-bit mix, bf16) as
+a secondary figure, and the fp64 CPU oracle timed on a bounded sample.
+
+Other modes (each prints its own single JSON line):
+  --sweep        budget sweep 3/4/5/6 b x M in {1, 4, 16} on the Llama2-13B layer
+  --qwen         Qwen3-32B-shaped stack of 64 layers, variants G and P
+  --copy-probe   a plain device copy of known size (HBM counter calibration)
 """
 from __future__ import annotations
 
@@ -27,6 +34,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 ROTATE_BYTES = 1.2e9
+METRIC = "decode GEMV effective weight GB/s (% HBM peak); prefill TFLOP/s at M=512"
 
 
 def _args():
@@ -38,7 +46,12 @@ def _args():
                    help="G: permutation gathered in-kernel; P: activations pre-permuted")
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
-    p.add_argument("--no-secondary", action="store_true")
+    p.add_argument("--no-prefill", action="store_true", help="skip the prefill GEMM figure")
+    p.add_argument("--prefill-only", action="store_true", help="time only the prefill GEMM")
+    p.add_argument("--sweep", action="store_true")
+    p.add_argument("--qwen", action="store_true")
+    p.add_argument("--qwen-layers", type=int, default=64)
+    p.add_argument("--copy-probe", type=int, default=0, metavar="MIB")
     return p.parse_args()
 
 
@@ -46,57 +59,116 @@ def _log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def build_layer(torch, pq, synth, config, mix=None, target_bits=None, m=1, x_dtype=None):
+def _clone(pl):
+    import copy
+    from paper_2607_14618_amd._lib import _aligned_empty
+    c = copy.copy(pl)
+    c.packed = _aligned_empty(pl.packed.numel(), pl.packed.device)
+    c.packed.copy_(pl.packed)
+    return c
+
+
+def build_layer(torch, pq, synth, config, layer=0, mix=None, target_bits=None, m=1,
+                x_dtype=None):
+    """[(name, PackedLinear, x on device)] for one synthetic layer."""
     dev = torch.device("cuda", 0)
-    lins, groups = synth.make_layer(config, mix=mix, target_bits=target_bits, m=m,
+    lins, groups = synth.make_layer(config, layer=layer, mix=mix, target_bits=target_bits, m=m,
                                     x_dtype=x_dtype or torch.float16, device=dev)
-    packed = []
+    out = []
     for lin in lins:
         pl = pq.PackedLinear(lin.blocks, lin.codes, lin.scales, lin.zeros, lin.perm, device=dev)
-        packed.append((lin, pl, groups[lin.group].x.to(dev)))
-        lin.codes = lin.scales = lin.zeros = None     # free host/device copies
-    return packed
+        out.append((lin.name, pl, groups[lin.group].x.to(dev)))
+        lin.codes = lin.scales = lin.zeros = None
+    return out
 
 
-def time_decode(torch, pq, layers, steps, warmup, variant):
-    """Run `steps` decode steps; each step runs every linear of one layer copy."""
+def rotation(layer, step_bytes):
+    copies = max(2, int(-(-ROTATE_BYTES // step_bytes)))
+    return [layer] + [[(nm, _clone(pl), x) for nm, pl, x in layer] for _ in range(copies - 1)]
+
+
+def time_steps(torch, steps, warmup, launches):
+    """launches(i) -> list of zero-arg callables (step i).  Returns (ms/step,
+    mean ms per launch position) from HIP events on the launch stream."""
     dev = torch.device("cuda", 0)
     stream = torch.cuda.current_stream(dev)
-    nlin = len(layers[0])
-    ys = [torch.empty((x.shape[0], pl.n), dtype=torch.float32, device=dev) for _, pl, x in layers[0]]
-    xs = []
-    for _, pl, x in layers[0]:
-        xs.append(pl.permute(x) if variant == "P" else x)
-
-    def step(i, ev=None):
-        copy = layers[i % len(layers)]
-        for j, (_, pl, _) in enumerate(copy):
-            if ev is not None:
-                ev[j][0].record(stream)
-            pl.decode(xs[j], pre_permuted=(variant == "P"), y=ys[j])
-            if ev is not None:
-                ev[j][1].record(stream)
-
     for i in range(warmup):
-        step(i)
+        for f in launches(i):
+            f()
     torch.cuda.synchronize()
-    evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-            for _ in range(nlin)] for _ in range(steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
+    n = len(launches(0))
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(n)] for _ in range(steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    t_start.record(stream)
+    t0.record(stream)
     for i in range(steps):
-        step(i, evs[i])
-    t_end.record(stream)
+        for j, f in enumerate(launches(i)):
+            ev[i][j][0].record(stream)
+            f()
+            ev[i][j][1].record(stream)
+    t1.record(stream)
     torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    per_lin_ms = [sum(evs[i][j][0].elapsed_time(evs[i][j][1]) for i in range(steps)) / steps
-                  for j in range(nlin)]
-    return total_ms / steps, per_lin_ms
+    per = [sum(ev[i][j][0].elapsed_time(ev[i][j][1]) for i in range(steps)) / steps for j in range(n)]
+    return t0.elapsed_time(t1) / steps, per
 
 
-def cpu_baseline(torch, synth, seconds_budget):
+def decode_launches(torch, copies, variant):
+    dev = torch.device("cuda", 0)
+    ys = [torch.empty((x.shape[0], pl.n), dtype=torch.float32, device=dev) for _, pl, x in copies[0]]
+    xs = [pl.permute(x) if variant == "P" else x for _, pl, x in copies[0]]
+    pre = variant == "P"
+
+    def launches(i):
+        return [(lambda pl=pl, j=j: pl.decode(xs[j], pre_permuted=pre, y=ys[j]))
+                for j, (_, pl, _) in enumerate(copies[i % len(copies)])]
+    return launches
+
+
+def decode_figure(torch, pq, synth, steps, warmup, variant, config=1, mix=None, target_bits=None,
+                  m=1):
+    layer = build_layer(torch, pq, synth, config, mix=mix, target_bits=target_bits, m=m)
+    step_bytes = sum(pl.weight_bytes for _, pl, _ in layer)
+    copies = rotation(layer, step_bytes)
+    ms, per = time_steps(torch, steps, warmup, decode_launches(torch, copies, variant))
+    kern_ms = sum(per)
+    res = {"ms_step": ms, "kern_ms": kern_ms, "step_bytes": step_bytes, "copies": len(copies),
+           "gbs": step_bytes / (ms * 1e-3) / 1e9, "kernel_gbs": step_bytes / (kern_ms * 1e-3) / 1e9,
+           "per_linear": {nm: {"us": round(t * 1e3, 2), "weight_bytes": pl.weight_bytes,
+                               "gbs": round(pl.weight_bytes / (t * 1e-3) / 1e9, 1)}
+                          for (nm, pl, _), t in zip(layer, per)}}
+    del copies, layer
+    torch.cuda.empty_cache()
+    return res
+
+
+def prefill_figure(torch, pq, synth, steps, warmup, m=512):
+    """Config: Llama2-13B layer, 4.0-bit prefill mix, bf16 activations, M=512,
+    permutation applied by the library (gather kernel + GEMM)."""
+    dev = torch.device("cuda", 0)
+    layer = build_layer(torch, pq, synth, 3, m=m, x_dtype=torch.bfloat16)
+    flops = sum(2.0 * m * pl.n * pl.k for _, pl, _ in layer)
+    ys = [torch.empty((m, pl.n), dtype=torch.float32, device=dev) for _, pl, _ in layer]
+
+    def launches(i):
+        return [(lambda pl=pl, x=x, j=j: pl.prefill(x, y=ys[j])) for j, (_, pl, x) in enumerate(layer)]
+    ms, per = time_steps(torch, steps, warmup, launches)
+    kern_ms = sum(per)
+    res = {"workload": "Llama2-13B layer, 7 linears, prefill M=512, 4.0-bit mix 2/3/4/8/16 b "
+                       "(20/30/35/13/2 %), bf16 activations, permutation applied in-library",
+           "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+           "kernel_tflops": round(flops / (kern_ms * 1e-3) / 1e12, 2),
+           "peak_tflops": BF16_PEAK_TFLOPS,
+           "frac": round(flops / (kern_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+           "ms_per_step": round(ms, 4), "flop_per_step": flops,
+           "weight_bytes_per_step": sum(pl.weight_bytes for _, pl, _ in layer),
+           "per_linear_us": {nm: round(t * 1e3, 1) for (nm, _, _), t in zip(layer, per)}}
+    del layer, ys
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(synth, seconds_budget):
     """The fp64 oracle on the host: a bounded sample of the same layer's rows."""
     import numpy as np
     import oracle
@@ -133,76 +205,137 @@ def cpu_baseline(torch, synth, seconds_budget):
                       f"linears {','.join(names)} in {dt:.1f} s"}
 
 
-def main():
-    a = _args()
-    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(the sharding design is described in DESIGN.md)", file=sys.stderr)
-        sys.exit(2)
-    import torch
-    import paper_2607_14618_amd as pq
-    import synth
-
-    _log("building the synthetic Llama2-13B layer")
-    t0 = time.time()
-    first = build_layer(torch, pq, synth, 1)
-    step_bytes = sum(pl.weight_bytes for _, pl, _ in first)
-    copies = max(2, int(-(-ROTATE_BYTES // step_bytes)))
-    layers = [first]
-    for c in range(1, copies):
-        layers.append([(lin, _clone(torch, pl), x) for lin, pl, x in first])
-    _log(f"{copies} copies x {step_bytes / 1e6:.2f} MB in {time.time() - t0:.1f} s")
-
-    ms_step, per_lin = time_decode(torch, pq, layers, a.steps, a.warmup, a.variant)
-    value = step_bytes / (ms_step * 1e-3) / 1e9
-    kern_ms = sum(per_lin)
-    achieved = step_bytes / (kern_ms * 1e-3) / 1e9
-    _log(f"decode: {ms_step * 1e3:.1f} us/step, {value:.1f} GB/s; kernels {kern_ms * 1e3:.1f} us, "
-         f"{achieved:.1f} GB/s")
-    per_linear = {lin.name: {"us": round(t * 1e3, 2), "weight_bytes": pl.weight_bytes,
-                             "gbs": round(pl.weight_bytes / (t * 1e-3) / 1e9, 1)}
-                  for (lin, pl, _), t in zip(first, per_lin)}
-    out = {
-        "metric": "decode GEMV effective weight GB/s (% HBM peak); prefill TFLOP/s at M=512",
-        "value": round(value, 2),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": a.steps,
-        "warmup": a.warmup,
-        "ms_per_step": round(ms_step, 6),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f16",
-        "data": "synthetic",
-        "config": {"workload": "Llama2-13B decoder layer, decode M=1, 7 linears, 3.0-bit mix "
-                               "2/3/4/8/16 b, fp16 activations, in-kernel channel gather"
-                               if a.variant == "G" else
-                               "Llama2-13B decoder layer, decode M=1, 7 linears, 3.0-bit mix, "
-                               "pre-permuted activations",
-                   "m": 1, "avg_bits": 3.0, "variant": a.variant, "linears": len(first),
-                   "weight_bytes_per_step": step_bytes, "rotation_copies": copies,
-                   "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2)},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "gemv_kernel<1>",
-                     "per_launch_bytes": round(step_bytes / len(first)),
-                     "avg_launch_us": round(kern_ms * 1e3 / len(first), 3),
-                     "per_linear": per_linear},
-    }
-    if not a.no_cpu:
-        _log("timing the CPU oracle")
-        out["cpu_baseline"] = cpu_baseline(torch, synth, a.cpu_seconds)
+def line(value, unit, steps, warmup, ms, dtype, config, higher=True, **extra):
+    out = {"metric": METRIC, "value": round(value, 2), "unit": unit, "n_gpus": 1, "steps": steps,
+           "warmup": warmup, "ms_per_step": round(ms, 6), "higher_is_better": higher,
+           "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+           "config": config}
+    out.update(extra)
     print(json.dumps(out), flush=True)
 
 
-def _clone(torch, pl):
-    import copy
-    from paper_2607_14618_amd._lib import _aligned_empty
-    c = copy.copy(pl)
-    c.packed = _aligned_empty(pl.packed.numel(), pl.packed.device)
-    c.packed.copy_(pl.packed)
-    return c
+def main_default(a, torch, pq, synth):
+    if a.prefill_only:
+        p = prefill_figure(torch, pq, synth, max(3, a.steps // 20), max(1, a.warmup // 10))
+        _log(f"prefill: {p['tflops']} TFLOP/s ({p['kernel_tflops']} in kernels)")
+        line(p["tflops"], "TFLOP/s", max(3, a.steps // 20), max(1, a.warmup // 10),
+             p["ms_per_step"], "bf16", {"workload": p["workload"], "m": 512}, prefill=p)
+        return
+    _log("building the synthetic Llama2-13B layer")
+    t0 = time.time()
+    d = decode_figure(torch, pq, synth, a.steps, a.warmup, a.variant)
+    _log(f"{d['copies']} copies x {d['step_bytes'] / 1e6:.2f} MB ({time.time() - t0:.1f} s); "
+         f"decode: {d['ms_step'] * 1e3:.1f} us/step, {d['gbs']:.1f} GB/s; "
+         f"kernels {d['kern_ms'] * 1e3:.1f} us, {d['kernel_gbs']:.1f} GB/s")
+    nlin = len(d["per_linear"])
+    extra = {
+        "roofline": {"bound": "hbm", "achieved": round(d["kernel_gbs"], 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(d["kernel_gbs"] / HBM_PEAK_GBS, 4),
+                     "traffic": None, "kernel": "gemv_kernel",
+                     "bytes_per_launch": round(d["step_bytes"] / nlin),
+                     "avg_launch_us": round(d["kern_ms"] * 1e3 / nlin, 3),
+                     "per_linear": d["per_linear"]},
+    }
+    if not a.no_prefill:
+        _log("prefill GEMM, M=512")
+        extra["prefill"] = prefill_figure(torch, pq, synth, 10, 3)
+        _log(f"prefill: {extra['prefill']['tflops']} TFLOP/s "
+             f"({extra['prefill']['kernel_tflops']} in kernels)")
+    if not a.no_cpu:
+        _log("timing the CPU oracle")
+        extra["cpu_baseline"] = cpu_baseline(synth, a.cpu_seconds)
+    wl = ("Llama2-13B decoder layer, decode M=1, 7 linears (q/k/v/o 5120x5120, gate/up "
+          "13824x5120, down 5120x13824), 3.0-bit mix 2/3/4/8/16 b (45/35/16/3/1 %), fp16 "
+          "activations, " + ("channel permutation gathered in-kernel" if a.variant == "G"
+                             else "activations pre-permuted"))
+    line(d["gbs"], "GB/s", a.steps, a.warmup, d["ms_step"], "f16",
+         {"workload": wl, "m": 1, "avg_bits": 3.0, "variant": a.variant, "linears": nlin,
+          "weight_bytes_per_step": d["step_bytes"], "rotation_copies": d["copies"],
+          "pct_hbm_peak": round(100 * d["gbs"] / HBM_PEAK_GBS, 2)}, **extra)
+
+
+def main_sweep(a, torch, pq, synth):
+    rows = []
+    for bits in (3, 4, 5, 6):
+        for m in (1, 4, 16):
+            d = decode_figure(torch, pq, synth, a.steps, a.warmup, a.variant, config=2,
+                              mix=synth.SWEEP_MIXES[bits], target_bits=bits, m=m)
+            rows.append({"avg_bits": bits, "m": m, "weight_bytes": d["step_bytes"],
+                         "us_per_step": round(d["ms_step"] * 1e3, 2), "gbs": round(d["gbs"], 1),
+                         "kernel_us": round(d["kern_ms"] * 1e3, 2),
+                         "kernel_gbs": round(d["kernel_gbs"], 1)})
+            _log(json.dumps(rows[-1]))
+    base = [r for r in rows if r["avg_bits"] == 3 and r["m"] == 1][0]
+    for r in rows:
+        r["time_ratio_vs_3b"] = round(r["us_per_step"] / base["us_per_step"], 3)
+        r["bytes_ratio_vs_3b"] = round(r["weight_bytes"] / base["weight_bytes"], 3)
+    top = [r for r in rows if r["avg_bits"] == 3 and r["m"] == 1][0]
+    line(top["gbs"], "GB/s", a.steps, a.warmup, top["us_per_step"] / 1e3, "f16",
+         {"workload": "budget sweep on the Llama2-13B layer, 3/4/5/6 b x M in {1,4,16}",
+          "variant": a.variant}, sweep=rows)
+
+
+def main_qwen(a, torch, pq, synth):
+    dev = torch.device("cuda", 0)
+    _log(f"building {a.qwen_layers} Qwen3-32B-shaped layers")
+    t0 = time.time()
+    layers = [build_layer(torch, pq, synth, 4, layer=l) for l in range(a.qwen_layers)]
+    step_bytes = sum(pl.weight_bytes for L in layers for _, pl, _ in L)
+    _log(f"{step_bytes / 1e9:.2f} GB packed in {time.time() - t0:.1f} s")
+    flat = [t for L in layers for t in L]
+    res = {}
+    for variant in ("G", "P"):
+        launches = decode_launches(torch, [flat], variant)
+        steps, warmup = max(2, a.steps // 40), 1
+        ms, per = time_steps(torch, steps, warmup, launches)
+        res[variant] = {"ms_per_step": round(ms, 4), "gbs": round(step_bytes / (ms * 1e-3) / 1e9, 1),
+                        "kernel_gbs": round(step_bytes / (sum(per) * 1e-3) / 1e9, 1)}
+        _log(f"qwen {variant}: {res[variant]}")
+    line(res[a.variant]["gbs"], "GB/s", max(2, a.steps // 40), 1, res[a.variant]["ms_per_step"],
+         "f16", {"workload": f"Qwen3-32B-shaped stack of {a.qwen_layers} decoder layers, decode M=1, "
+                             "3.0-bit mix, variants G (in-kernel gather) and P (pre-permuted)",
+                 "layers": a.qwen_layers, "weight_bytes_per_step": step_bytes,
+                 "variant": a.variant}, variants=res)
+
+
+def main_copy_probe(a, torch):
+    """A plain device-to-device copy of known size: the reference point that
+    scales the HBM byte counters (FETCH_SIZE, WRITE_SIZE) of the other kernels."""
+    dev = torch.device("cuda", 0)
+    n = a.copy_probe << 20
+    src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    reps = 10
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    line(2 * n / (ms * 1e-3) / 1e9, "GB/s", reps, 3, ms, "f32",
+         {"workload": f"device copy of {a.copy_probe} MiB (reads {n} B, writes {n} B per launch)"})
+
+
+def main():
+    a = _args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(the sharding design is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if a.copy_probe:
+        return main_copy_probe(a, torch)
+    import paper_2607_14618_amd as pq
+    import synth
+    if a.sweep:
+        return main_sweep(a, torch, pq, synth)
+    if a.qwen:
+        return main_qwen(a, torch, pq, synth)
+    return main_default(a, torch, pq, synth)
 
 
 if __name__ == "__main__":

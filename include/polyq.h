@@ -73,19 +73,26 @@ typedef struct {
  * block_offset[i] + t * tile_bytes[i].  A tile holds the block's groups of 128
  * channels in order (the last one may hold 32, 64 or 96); group j of a tile
  * starts at j * record_bytes[i] and is
- *     [meta: 64 rows x {fp16 s, fp16 z} = 256 B, only for b <= 8]
- *     [chunk 0][chunk 1]...   up to 4 chunks of 32 channels,
- * and chunk c holds 64 rows x (4*b) bytes, row r at c*64*4b + r*4b.  So one
- * 32-channel chunk of 64 rows is one contiguous 512 B/768 B/1 KB/2 KB/4 KB run.
- * Inside a row's 4b bytes (32-bit words, little endian) code i of the chunk is:
- *   b = 2, 4, 8, 16: word i / (32/b); inside the word the even codes fill the
- *        low half and the odd codes the high half, in order: code 2p+h of the
- *        word sits at bits [16h + b*p, 16h + b*p + b).
+ *     [meta: 256 B, only for b <= 8][chunk 0][chunk 1]...  (up to 4 chunks of
+ *     32 channels, chunk c at 256 + c * 256 * b for b <= 8, c * 4096 for b = 16).
+ * Meta (fp16 bits): z of tile row R at half (R % 16) * 4 + R / 16, and s of row R
+ *     at half 64 + ((R % 16) / 4) * 16 + (R / 16) * 4 + R % 4.
+ * Chunk (64 rows x 32 channels, 256 * b bytes): 64 lane slices of 4 * b bytes,
+ *     slice l at l * 4b.  Slice l holds channels 8 * (l / 16) .. + 7 of the four
+ *     rows 16 * r + l % 16, r = 0..3 (the operand fragment a 64-lane 16x16x32
+ *     matrix instruction takes per row sub-tile); its code i = 8 * r + t is row
+ *     sub-tile r, channel 8 * (l / 16) + t.  Inside the slice's b words
+ *     (32-bit, little endian):
+ *   b = 2, 4, 8, 16: word d holds codes d*P .. d*P + P - 1, P = 32 / b; the
+ *        even codes fill the low half and the odd codes the high half, in order:
+ *        code d*P + 2p + h sits at bits [16h + b*p, 16h + b*p + b).
  *   b = 3: word d (d = 0,1,2) holds codes 10d .. 10d+9 as five pairs; pair p
  *        (codes 10d+2p, 10d+2p+1) sits at bits F..F+2 and 16+F..18+F with
  *        F = {0, 3, 6, 10, 13}[p]; codes 30 and 31 keep bit j in bit 9
  *        (code 30) and bit 25 (code 31) of word j.
  *   b = 16: the raw fp16 bits.
+ * Every field of a 64-lane load is therefore one contiguous, aligned run of
+ * 64 * 4b bytes.
  */
 typedef struct {
   int32_t n;        /* output channels (rows)                          */
