@@ -55,6 +55,31 @@ def _args():
     return p.parse_args()
 
 
+GEMV_SOURCES = ("paper_2607_14618_amd/csrc/gemv.hip", "paper_2607_14618_amd/csrc/codec.h",
+                "paper_2607_14618_amd/csrc/internal.h", "paper_2607_14618_amd/csrc/plan.cpp")
+GEMV_COUNTERS = "profiles/gemv_kernel_llama2_13b_decode_m1.md"
+
+
+def recorded_traffic():
+    """HBM bytes per GEMV launch from the committed rocprofv3 counter summary
+    (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None when the kernel sources
+    have changed since the counters were taken."""
+    import hashlib
+    import re
+    try:
+        text = open(os.path.join(ROOT, GEMV_COUNTERS)).read()
+        h = hashlib.sha256()
+        for f in GEMV_SOURCES:
+            h.update(open(os.path.join(ROOT, f), "rb").read())
+    except OSError:
+        return None
+    m_hash = re.search(r"Source hash [^`]*`([0-9a-f]+)`", text)
+    m_val = re.search(r"traffic_bytes_per_launch: (\d+)", text)
+    if not m_hash or not m_val or m_hash.group(1) != h.hexdigest()[:len(m_hash.group(1))]:
+        return None
+    return int(m_val.group(1))
+
+
 def _log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -231,7 +256,8 @@ def main_default(a, torch, pq, synth):
     extra = {
         "roofline": {"bound": "hbm", "achieved": round(d["kernel_gbs"], 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(d["kernel_gbs"] / HBM_PEAK_GBS, 4),
-                     "traffic": None, "kernel": "gemv_kernel",
+                     "traffic": recorded_traffic(), "traffic_unit": "bytes per launch",
+                     "kernel": "gemv_kernel",
                      "bytes_per_launch": round(d["step_bytes"] / nlin),
                      "avg_launch_us": round(d["kern_ms"] * 1e3 / nlin, 3),
                      "per_linear": d["per_linear"]},
