@@ -1,14 +1,14 @@
 // Decode / small-batch GEMV over the mixed-bit clustered weight (Sec. 4.1-4.2),
 // 1 <= M <= 16 tokens, on the matrix cores.
 //
-// Mapping on gfx950: a wave owns one 64-row tile and a contiguous range of
-// 32-channel chunks.  For each chunk, lane l loads its 4b-byte slice (rows
-// 16r + l%16, r = 0..3, channels 8(l/16) .. +7: one contiguous 512 B .. 4 KB
-// run per wave), unpacks the 32 codes into exact fp16 (q - z) values -- the
-// A fragments of four v_mfma_f32_16x16x32_f16, one per 16-row sub-tile -- and
-// the B fragment is the 8 activations x'[token l%16][8(l/16) .. +7] from LDS.
-// The 16 columns of the MFMA are the tokens, so M = 1 and M = 16 cost the same;
-// the matrix pipe is otherwise idle, so the VALU only unpacks.
+// Mapping on gfx950: a wave owns one 64-row tile and a contiguous,
+// group-aligned range of one bit block's 32-channel chunks.  For each chunk,
+// lane l loads its 4b-byte slice (rows 16r + l%16, r = 0..3, channels
+// 8(l/16) .. +7: one contiguous 512 B .. 4 KB run per wave), unpacks the 32
+// codes into exact fp16 integers q -- the A fragments of four
+// v_mfma_f32_16x16x32_f16, one per 16-row sub-tile -- and the B fragment is the
+// 8 activations x'[token l%16][8(l/16) .. +7] from LDS.  The 16 columns of the
+// MFMA are the tokens, so M = 1 and M = 16 cost the same.
 //
 // Unpacking: a code field placed at mantissa bits [f, f+b) of an fp16 half is
 // turned into the exact fp16 value (2^(10-f) + q) by OR-ing in the exponent
@@ -19,9 +19,9 @@
 // accumulation rounds.  16-bit channels enter the MFMA as their fp16 weights.
 //
 // A work-group (tile, split) stages its slice of the permuted activations
-// x'[k'] = x[perm[k']] (Eq. 9) into LDS once, its waves take byte-balanced
-// contiguous chunk ranges and reduce through LDS; splits of a tile across
-// work-groups are combined by the last-arriving work-group (fixed order).
+// x'[k'] = x[perm[k']] (Eq. 9) and the group metadata into LDS once, its waves
+// reduce through LDS, and splits of a tile across work-groups are combined by
+// the last-arriving work-group (fixed order).
 #include <hip/hip_runtime.h>
 
 #include "codec.h"
@@ -70,6 +70,10 @@ __host__ __device__ constexpr uint32_t magic(int e) {
 __device__ __forceinline__ h2 splat(float v) {
   const _Float16 h = static_cast<_Float16>(v);
   return h2{h, h};
+}
+__device__ __forceinline__ h8 splat8(float v) {
+  const _Float16 h = static_cast<_Float16>(v);
+  return h8{h, h, h, h, h, h, h, h};
 }
 
 // Raw pair values (2^(10-f) + q_even, 2^(10-f) + q_odd) of the 16 pairs of one
@@ -190,34 +194,32 @@ struct Slot {
   uint32_t w[16];
 };
 
-// End (exclusive) of the slot that starts at block-local chunk c.
-template <int B>
-__device__ __forceinline__ int slot_end(int c, int l1) {
-  constexpr int NS = Geo<B>::NS;
-  return min((c / NS) * NS + NS, l1);
-}
-
-// Issue the loads of the slot [c, ce) of one tile.  Register slice j holds
-// aligned position (c/NS)*NS + j; positions outside [c, ce) re-read chunk c.
+// Issue the loads of the slot of NS chunks starting at block-local chunk c of
+// one tile; positions at or past l1 re-read chunk l1 - 1, so every slot issues
+// the same number of loads.
 template <int B>
 __device__ __forceinline__ void issue(Slot& sl, __amdgpu_buffer_rsrc_t r, int record_bytes, int c,
-                                      int ce, int lane) {
+                                      int l1, int lane) {
   using G = Geo<B>;
-  const int base = (c / G::NS) * G::NS;
 #pragma unroll
   for (int j = 0; j < G::NS; ++j) {
-    const int pos = base + j;
-    const int cj = (pos >= c && pos < ce) ? pos : c;
+    const int cj = min(c + j, l1 - 1);
     load_slice<B>(r, lane * G::CB, (cj >> 2) * record_bytes + G::META + (cj & 3) * (64 * G::CB),
                   &sl.w[j * B]);
   }
 }
 
+// State of the group being accumulated: the per-pair constants subtracted
+// from the unpacked raw values, and the group's own accumulators (one f4 per
+// 16-row sub-tile).
+//   kExact (every zero point an integer of magnitude <= 1023):
+//     c[P] = -(2^(10-f) + z_row): one exact add leaves q - z.
+//   otherwise: c[P] = -2^(10-f) leaves q, and -z_row is added in fp16
+//     (q - z rounded to fp16 before the exact product).
 struct Group {
-  h2 c1[16];  // per pair: -(offset + z_row) (integer z) or -offset
-  h2 nz[4];   // per row: -z
-  bool exact;
-  f4 part[4];  // this group's accumulators, one per 16-row sub-tile
+  h2 c[16];
+  h2 nz[4];
+  f4 part[4];
 };
 
 __device__ __forceinline__ h8 frag(const uint32_t* w4) {
@@ -225,9 +227,28 @@ __device__ __forceinline__ h8 frag(const uint32_t* w4) {
   return __builtin_bit_cast(h8, u);
 }
 
-// Unpack one slice of a b <= 8 block into exact (q - z) fragments and run the
-// four MFMAs of its 16-row sub-tiles against the activation fragment.
-template <int B, bool kExactZ>
+// Group start: this lane's zero points (A-fragment rows 16r + l%16, r = 0..3,
+// one 8-byte LDS read) -> the pair constants.
+template <int B, bool kExact>
+__device__ __forceinline__ void start_group(const uint8_t* gm, int lane, Group& gs) {
+  using U = Unpack<B>;
+  const uint2 zz = *reinterpret_cast<const uint2*>(gm + (lane & 15) * 8);
+  const h2 z01 = as_h2(zz.x), z23 = as_h2(zz.y);
+  const h2 zs[4] = {h2{z01[0], z01[0]}, h2{z01[1], z01[1]}, h2{z23[0], z23[0]}, h2{z23[1], z23[1]}};
+#pragma unroll
+  for (int P = 0; P < 16; ++P) {
+    const h2 off = splat(U::offset[U::which[P]]);
+    gs.c[P] = kExact ? -(zs[P >> 2] + off) : -off;
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) gs.nz[r] = -zs[r];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) gs.part[r] = f4{0.f, 0.f, 0.f, 0.f};
+}
+
+// Unpack one lane slice of a b <= 8 block into fp16 (q - z) fragments and run
+// the four MFMAs of its 16-row sub-tiles.
+template <int B, bool kExact>
 __device__ __forceinline__ void quant_slice(const uint32_t* w, h8 xb, Group& gs) {
   using U = Unpack<B>;
   uint32_t v[16];
@@ -235,8 +256,8 @@ __device__ __forceinline__ void quant_slice(const uint32_t* w, h8 xb, Group& gs)
   uint32_t d[16];
 #pragma unroll
   for (int P = 0; P < 16; ++P) {
-    h2 t = as_h2(v[P]) + gs.c1[P];
-    if constexpr (!kExactZ) t = t + gs.nz[P >> 2];
+    h2 t = as_h2(v[P]) + gs.c[P];
+    if constexpr (!kExact) t = t + gs.nz[P >> 2];
     d[P] = as_u32(t);
   }
 #pragma unroll
@@ -244,66 +265,50 @@ __device__ __forceinline__ void quant_slice(const uint32_t* w, h8 xb, Group& gs)
     gs.part[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(frag(&d[4 * r]), xb, gs.part[r], 0, 0, 0);
 }
 
-// Unpack and accumulate the slot [c, ce) of a segment [l0, l1).  `xlane` is
-// this lane's activation fragment of block-local chunk 0 (LDS); `meta` is the
-// LDS copy of the metadata of block-local group 0.
-template <int B>
-__device__ __forceinline__ void compute(const Slot& sl, int c, int ce, int l0, int l1,
-                                        const uint32_t* xlane, const uint8_t* meta, int lane,
-                                        Group& gs, f4 (&acc)[4]) {
+// Group end: acc += s * part.  Lane l holds rows 16r + 4(l/16) + e; their
+// scales are 16 consecutive halves.
+__device__ __forceinline__ void fold_group(const uint8_t* gm, int lane, const Group& gs,
+                                           f4 (&acc)[4]) {
+  const uint4* sp = reinterpret_cast<const uint4*>(gm + 128 + (lane >> 4) * 32);
+  const uint4 s0 = sp[0], s1 = sp[1];
+  const uint32_t sw[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = 4 * r + e;
+      const float sc = static_cast<float>(
+          __builtin_bit_cast(_Float16, static_cast<uint16_t>(sw[i >> 1] >> (16 * (i & 1)))));
+      acc[r][e] = fmaf(sc, gs.part[r][e], acc[r][e]);
+    }
+}
+
+// Unpack and accumulate the slot starting at block-local chunk c (chunks
+// c .. min(c + NS, l1) - 1).  Wave ranges start on group boundaries, so for
+// b <= 4 a slot holds whole groups and slot position j starts a group when
+// j % 4 == 0; an 8-bit group spans two slots.  `xlane` is this lane's
+// activation fragment of block-local chunk 0 (LDS); `meta` is the LDS copy of
+// the metadata of block-local group 0.
+template <int B, bool kExact>
+__device__ __forceinline__ void compute(const Slot& sl, int c, int l1, const uint32_t* xlane,
+                                        const uint8_t* meta, int lane, Group& gs, f4 (&acc)[4]) {
   using G = Geo<B>;
-  const int base = (c / G::NS) * G::NS;
 #pragma unroll
   for (int j = 0; j < G::NS; ++j) {
-    const int pos = base + j;
-    if (pos < c || pos >= ce) continue;
+    const int pos = c + j;
+    if (pos >= l1) break;
     const h8 xb = __builtin_bit_cast(h8, *reinterpret_cast<const uint4*>(xlane + pos * 16));
     if constexpr (B == 16) {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(frag(&sl.w[j * B + 4 * r]), xb, acc[r], 0, 0, 0);
     } else {
-      using U = Unpack<B>;
       const uint8_t* gm = meta + (pos >> 2) * kMetaBytes;
-      if ((pos & 3) == 0 || pos == l0) {  // group start: zero points -> pair constants
-        const uint2 zz = *reinterpret_cast<const uint2*>(gm + (lane & 15) * 8);
-        float z[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          z[r] = static_cast<float>(__builtin_bit_cast(
-              _Float16, static_cast<uint16_t>((r < 2 ? zz.x : zz.y) >> (16 * (r & 1)))));
-        bool ok = true;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) ok = ok && (z[r] == truncf(z[r])) && fabsf(z[r]) <= 1023.f;
-        // integer zero points (the asymmetric quantizer's): one exact add per pair
-        gs.exact = __all(ok);
-#pragma unroll
-        for (int P = 0; P < 16; ++P)
-          gs.c1[P] = gs.exact ? splat(-(U::offset[U::which[P]] + z[P >> 2]))
-                              : splat(-U::offset[U::which[P]]);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) gs.nz[r] = splat(-z[r]);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) gs.part[r] = f4{0.f, 0.f, 0.f, 0.f};
-      }
-      if (gs.exact)
-        quant_slice<B, true>(&sl.w[j * B], xb, gs);
-      else
-        quant_slice<B, false>(&sl.w[j * B], xb, gs);
-      if ((pos & 3) == 3 || pos == l1 - 1) {  // group end: apply the row scales once
-        const uint4* sp = reinterpret_cast<const uint4*>(gm + 128 + (lane >> 4) * 32);
-        const uint4 s0 = sp[0], s1 = sp[1];
-        const uint32_t sw[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int i = 4 * r + e;
-            const float sc = static_cast<float>(
-                __builtin_bit_cast(_Float16, static_cast<uint16_t>(sw[i >> 1] >> (16 * (i & 1)))));
-            acc[r][e] = fmaf(sc, gs.part[r][e], acc[r][e]);
-          }
-      }
+      const bool start = B <= 4 ? (j & 3) == 0 : (j == 0 && (c & 3) == 0);
+      if (start) start_group<B, kExact>(gm, lane, gs);
+      quant_slice<B, kExact>(&sl.w[j * B], xb, gs);
+      const bool end = (B <= 4 && (j & 3) == 3) || (B == 8 && (pos & 3) == 3) || pos == l1 - 1;
+      if (end) fold_group(gm, lane, gs, acc);
     }
   }
 }
@@ -312,47 +317,35 @@ __device__ __forceinline__ void compute(const Slot& sl, int c, int ce, int l0, i
 // slot is unpacked the next two are in flight.  A slot is always issued (past
 // the segment end it re-reads the last chunk, an L1/L2 hit), so the number of
 // loads between a slot's issue and its use is fixed and each wait leaves the
-// two younger slots outstanding.  `sa`/`sb` already hold the first two slots
-// when `preloaded`.
-template <int B>
+// two younger slots outstanding.  `sa`/`sb` already hold the first two slots.
+template <int B, bool kExact>
 __device__ __forceinline__ void run_segment(__amdgpu_buffer_rsrc_t rs, int record_bytes, int l0,
                                             int l1, const uint32_t* xlane, const uint8_t* meta,
-                                            int lane, Slot& sa, Slot& sb, bool preloaded,
-                                            f4 (&acc)[4]) {
+                                            int lane, Slot& sa, Slot& sb, f4 (&acc)[4]) {
+  constexpr int NS = Geo<B>::NS;
   Slot sc;
   Group gs;
-  int c0 = l0, e0 = slot_end<B>(c0, l1);
-  int c1 = e0 < l1 ? e0 : c0, e1 = e0 < l1 ? slot_end<B>(c1, l1) : e0;
-  if (!preloaded) {
-    issue<B>(sa, rs, record_bytes, c0, e0, lane);
-    issue<B>(sb, rs, record_bytes, c1, e1, lane);
-  }
-  for (;;) {
-    int c2 = e1 < l1 ? e1 : c1, e2 = e1 < l1 ? slot_end<B>(c2, l1) : e1;
-    issue<B>(sc, rs, record_bytes, c2, e2, lane);
-    compute<B>(sa, c0, e0, l0, l1, xlane, meta, lane, gs, acc);
-    if (e0 >= l1) break;
-    c0 = c1; e0 = e1; c1 = c2; e1 = e2;
-    c2 = e1 < l1 ? e1 : c1; e2 = e1 < l1 ? slot_end<B>(c2, l1) : e1;
-    issue<B>(sa, rs, record_bytes, c2, e2, lane);
-    compute<B>(sb, c0, e0, l0, l1, xlane, meta, lane, gs, acc);
-    if (e0 >= l1) break;
-    c0 = c1; e0 = e1; c1 = c2; e1 = e2;
-    c2 = e1 < l1 ? e1 : c1; e2 = e1 < l1 ? slot_end<B>(c2, l1) : e1;
-    issue<B>(sb, rs, record_bytes, c2, e2, lane);
-    compute<B>(sc, c0, e0, l0, l1, xlane, meta, lane, gs, acc);
-    if (e0 >= l1) break;
-    c0 = c1; e0 = e1; c1 = c2; e1 = e2;
+  for (int c = l0;;) {
+    issue<B>(sc, rs, record_bytes, c + 2 * NS, l1, lane);
+    compute<B, kExact>(sa, c, l1, xlane, meta, lane, gs, acc);
+    c += NS;
+    if (c >= l1) break;
+    issue<B>(sa, rs, record_bytes, c + 2 * NS, l1, lane);
+    compute<B, kExact>(sb, c, l1, xlane, meta, lane, gs, acc);
+    c += NS;
+    if (c >= l1) break;
+    issue<B>(sb, rs, record_bytes, c + 2 * NS, l1, lane);
+    compute<B, kExact>(sc, c, l1, xlane, meta, lane, gs, acc);
+    c += NS;
+    if (c >= l1) break;
   }
 }
 
 template <int B>
 __device__ __forceinline__ void preload(__amdgpu_buffer_rsrc_t rs, int rb, int l0, int l1,
                                         int lane, Slot& sa, Slot& sb) {
-  const int e0 = slot_end<B>(l0, l1);
-  const int c1 = e0 < l1 ? e0 : l0, e1 = e0 < l1 ? slot_end<B>(c1, l1) : e0;
-  issue<B>(sa, rs, rb, l0, e0, lane);
-  issue<B>(sb, rs, rb, c1, e1, lane);
+  issue<B>(sa, rs, rb, l0, l1, lane);
+  issue<B>(sb, rs, rb, l0 + Geo<B>::NS, l1, lane);
 }
 
 // Dword `i` (compile-time) of the kernel-argument block, from the copy held one
@@ -387,6 +380,52 @@ struct Blocks {
     return kfield<int32_t>(kv, offsetof(GemvArgs, record_bytes) / 4 + 2 * i);
   }
 };
+
+// The wave's chunks [c0, c1), block by block (one block unless the layer is too
+// small to give every block its own waves).
+template <bool kExact>
+__device__ __forceinline__ void run_blocks(const Blocks& bd, int first, int nblocks, int c0, int c1,
+                                           int cw0, int cw1, const uint8_t* packed, int tile,
+                                           const uint32_t* xrow, const uint8_t* meta_lds,
+                                           int meta_slot, bool preloaded, int lane, Slot& sa,
+                                           Slot& sb, f4 (&acc)[4]) {
+  for (int bi = first; bi < nblocks; ++bi) {
+    const int bits = bd.bits(bi), cb = bd.cb(bi), ce = bd.ce(bi);
+    const int lo = max(c0, cb), hi = min(c1, ce);
+    if (lo >= hi) break;
+    const int64_t tb = bd.tb(bi);
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(packed + bd.off(bi) + tile * tb, tb);
+    const int rb = bd.rb(bi);
+    const int l0 = lo - cb, l1 = hi - cb;
+    // block-local chunk 0 of this block, relative to the staged range
+    const uint32_t* xlane = xrow + (cb - cw0) * 16;
+    // LDS metadata of block-local group 0 (the work-group staged this block's
+    // groups from the one holding max(cw0, block start))
+    const int wg_lo = max(cw0, cb);
+    const uint8_t* meta = meta_lds + (meta_slot - ((wg_lo - cb) >> 2)) * kMetaBytes;
+    if (!preloaded || bi != first) {  // a wave that spans blocks (small layers only)
+      switch (bits) {
+        case 2: preload<2>(rs, rb, l0, l1, lane, sa, sb); break;
+        case 3: preload<3>(rs, rb, l0, l1, lane, sa, sb); break;
+        case 4: preload<4>(rs, rb, l0, l1, lane, sa, sb); break;
+        case 8: preload<8>(rs, rb, l0, l1, lane, sa, sb); break;
+        default: preload<16>(rs, rb, l0, l1, lane, sa, sb); break;
+      }
+    }
+    switch (bits) {
+      case 2: run_segment<2, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
+      case 3: run_segment<3, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
+      case 4: run_segment<4, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
+      case 8: run_segment<8, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
+      default: run_segment<16, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
+    }
+    if (bits <= 8) {
+      const int whi = min(cw1, ce);
+      meta_slot += ((whi - 1 - cb) >> 2) + 1 - ((wg_lo - cb) >> 2);
+    }
+  }
+
+}
 
 __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   extern __shared__ uint32_t smem[];
@@ -444,7 +483,9 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   uint8_t* meta_lds = reinterpret_cast<uint8_t*>(smem) + static_cast<size_t>(m + 1) * range * 2;
 
   // Metadata: group records of the blocks with b <= 8 that overlap [cw0, cw1),
-  // copied 16 bytes per thread and round.
+  // copied 16 bytes per thread and round.  The zero points are checked on the
+  // way: the fast unpack needs every one to be an integer with |z| <= 1023.
+  bool z_ok = true;
   {
     int slot0 = 0;
 #pragma unroll
@@ -457,8 +498,17 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
       const int pieces = (g1 - g0) * (kMetaBytes / 16);
       for (int i = threadIdx.x; i < pieces; i += blockDim.x) {
         const int g = g0 + i / (kMetaBytes / 16), o = (i % (kMetaBytes / 16)) * 16;
-        *reinterpret_cast<uint4*>(meta_lds + (slot0 + g - g0) * kMetaBytes + o) =
-            *reinterpret_cast<const uint4*>(tile_base + g * bd.rb(bi) + o);
+        const uint4 v = *reinterpret_cast<const uint4*>(tile_base + g * bd.rb(bi) + o);
+        *reinterpret_cast<uint4*>(meta_lds + (slot0 + g - g0) * kMetaBytes + o) = v;
+        if (o < kMetaBytes / 2) {
+          const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+          for (int h = 0; h < 8; ++h) {
+            const float z = static_cast<float>(
+                __builtin_bit_cast(_Float16, static_cast<uint16_t>(w[h >> 1] >> (16 * (h & 1)))));
+            z_ok = z_ok && z == truncf(z) && fabsf(z) <= 1023.f;
+          }
+        }
       }
       slot0 += g1 - g0;
     }
@@ -502,7 +552,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
     }
     *reinterpret_cast<uint4*>(xs16 + m * range + kk0) = uint4{0u, 0u, 0u, 0u};
   }
-  __syncthreads();
+  const bool exact = __syncthreads_and(z_ok);
 
   f4 acc[4];
 #pragma unroll
@@ -518,33 +568,12 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
     const int lo = max(cw0, bd.cb(bi)), hi = min(cw1, bd.ce(bi));
     if (lo < hi) meta_slot += ((hi - 1 - bd.cb(bi)) >> 2) + 1 - ((lo - bd.cb(bi)) >> 2);
   }
-  for (int bi = first; bi < nblocks; ++bi) {
-    const int bits = bd.bits(bi), cb = bd.cb(bi), ce = bd.ce(bi);
-    const int lo = max(c0, cb), hi = min(c1, ce);
-    if (lo >= hi) break;
-    const int64_t tb = bd.tb(bi);
-    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(packed + bd.off(bi) + tile * tb, tb);
-    const int rb = bd.rb(bi);
-    const int l0 = lo - cb, l1 = hi - cb;
-    // block-local chunk 0 of this block, relative to the staged range
-    const uint32_t* xlane = xrow + (cb - cw0) * 16;
-    // LDS metadata of block-local group 0 (the work-group staged this block's
-    // groups from the one holding max(cw0, block start))
-    const int wg_lo = max(cw0, cb);
-    const uint8_t* meta = meta_lds + (meta_slot - ((wg_lo - cb) >> 2)) * kMetaBytes;
-    const bool pre = preloaded && bi == first;
-    switch (bits) {
-      case 2: run_segment<2>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
-      case 3: run_segment<3>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
-      case 4: run_segment<4>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
-      case 8: run_segment<8>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
-      default: run_segment<16>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, pre, acc); break;
-    }
-    if (bits <= 8) {
-      const int whi = min(cw1, ce);
-      meta_slot += ((whi - 1 - cb) >> 2) + 1 - ((wg_lo - cb) >> 2);
-    }
-  }
+  if (exact)
+    run_blocks<true>(bd, first, nblocks, c0, c1, cw0, cw1, packed, tile, xrow, meta_lds, meta_slot,
+                     preloaded, lane, sa, sb, acc);
+  else
+    run_blocks<false>(bd, first, nblocks, c0, c1, cw0, cw1, packed, tile, xrow, meta_lds,
+                      meta_slot, preloaded, lane, sa, sb, acc);
 
   // Reduce the waves' partial sums (fixed order).  MFMA result layout: lane l
   // holds rows 16r + 4(l/16) + e of token l%16.

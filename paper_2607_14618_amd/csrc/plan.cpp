@@ -114,7 +114,22 @@ static int groups_touched(const polyq_layout& L, int lo, int hi) {
   return n;
 }
 
-static void partition(const std::vector<int64_t>& prefix, int parts, int32_t* split) {
+// The group boundary (block-relative multiple of 4 chunks, or the block end)
+// nearest to chunk c.  GEMV waves start and end on these, so that every group
+// record is processed whole by one wave.
+static int snap_to_group(const polyq_layout& L, int c) {
+  for (int i = 0; i < L.nblocks; ++i) {
+    const int b0 = L.k_begin[i] / kChunk, b1 = b0 + L.block[i].len / kChunk;
+    if (c < b0 || c >= b1) continue;
+    const int down = b0 + (c - b0) / kChunksPerGroup * kChunksPerGroup;
+    const int up = std::min(b1, down + kChunksPerGroup);
+    return (c - down <= up - c) ? down : up;
+  }
+  return c;
+}
+
+static void partition(const polyq_layout& L, const std::vector<int64_t>& prefix, int parts,
+                      int32_t* split) {
   const int C = static_cast<int>(prefix.size()) - 1;
   const int64_t total = prefix[C];
   split[0] = 0;
@@ -125,7 +140,7 @@ static void partition(const std::vector<int64_t>& prefix, int parts, int32_t* sp
     // pick the nearer of c-1 and c
     int best = c;
     if (c > 0 && goal - prefix[c - 1] < prefix[c] - goal) best = c - 1;
-    best = std::max(best, static_cast<int>(split[j - 1]));
+    best = std::max(snap_to_group(L, best), static_cast<int>(split[j - 1]));
     split[j] = best;
   }
   split[parts] = C;
@@ -137,26 +152,27 @@ static int64_t chunk_cost(int bits) { return 4 * bits + (bits <= 8 ? 1 : 0); }
 
 // `parts` waves per tile with every wave inside one block: waves are given to
 // blocks in proportion to their bytes (at least one each, at most one per
-// chunk) and each block's chunks are split evenly among its waves.  Returns
+// group) and each block's groups are split evenly among its waves.  Returns
 // false when there are fewer waves than blocks.
 static bool partition_by_block(const polyq_layout& L, int parts, int32_t* split) {
   const int nb = L.nblocks;
   if (parts < nb) return false;
   int64_t cost[POLYQ_MAX_BLOCKS], total = 0;
-  int nch[POLYQ_MAX_BLOCKS], n[POLYQ_MAX_BLOCKS], used = 0;
+  int nch[POLYQ_MAX_BLOCKS], ngr[POLYQ_MAX_BLOCKS], n[POLYQ_MAX_BLOCKS], used = 0;
   for (int i = 0; i < nb; ++i) {
     nch[i] = L.block[i].len / kChunk;
+    ngr[i] = (nch[i] + kChunksPerGroup - 1) / kChunksPerGroup;
     cost[i] = nch[i] * chunk_cost(L.block[i].bits);
     total += cost[i];
   }
   for (int i = 0; i < nb; ++i) {
-    n[i] = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(nch[i], parts * cost[i] / total)));
+    n[i] = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(ngr[i], parts * cost[i] / total)));
     used += n[i];
   }
   while (used < parts) {  // next wave to the block with the most bytes per wave
     int best = -1;
     for (int i = 0; i < nb; ++i)
-      if (n[i] < nch[i] && (best < 0 || cost[i] * n[best] > cost[best] * n[i])) best = i;
+      if (n[i] < ngr[i] && (best < 0 || cost[i] * n[best] > cost[best] * n[i])) best = i;
     if (best < 0) break;
     ++n[best];
     ++used;
@@ -172,7 +188,10 @@ static bool partition_by_block(const polyq_layout& L, int parts, int32_t* split)
   split[0] = 0;
   for (int i = 0; i < nb; ++i) {
     const int c0 = L.k_begin[i] / kChunk;
-    for (int j = 0; j < n[i]; ++j) split[++u] = c0 + static_cast<int>(static_cast<int64_t>(nch[i]) * (j + 1) / n[i]);
+    for (int j = 0; j < n[i]; ++j) {
+      const int g = static_cast<int>(static_cast<int64_t>(ngr[i]) * (j + 1) / n[i]);
+      split[++u] = c0 + std::min(nch[i], g * kChunksPerGroup);
+    }
   }
   for (; u < parts; ++u) split[u + 1] = L.n_chunks;  // waves left without work
   return true;
@@ -196,7 +215,7 @@ int plan_gemv(const polyq_layout& L, int32_t m, GemvPlan* p) {
     p->S = S;
     p->W = W;
     p->nsplit = S * W;
-    if (!partition_by_block(L, S * W, p->split)) partition(prefix, S * W, p->split);
+    if (!partition_by_block(L, S * W, p->split)) partition(L, prefix, S * W, p->split);
     int worst = 0, worst_groups = 0;
     for (int s = 0; s < S; ++s) {
       worst = std::max(worst, p->split[(s + 1) * W] - p->split[s * W]);
