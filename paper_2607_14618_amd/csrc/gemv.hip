@@ -44,6 +44,7 @@ struct GemvArgs {
   float* partial;     // [S][m][rows_pad], only when S > 1
   uint32_t* counter;  // [n_tiles], only when S > 1
   int32_t n, k, m, nblocks, rows_pad, S;
+  int32_t wave_groups;  // LDS metadata slots per wave
   int32_t bits[POLYQ_MAX_BLOCKS];
   int32_t chunk_begin[POLYQ_MAX_BLOCKS];
   int32_t chunk_end[POLYQ_MAX_BLOCKS];
@@ -187,6 +188,9 @@ template <int B>
 struct Geo {
   static constexpr int NS = B == 2 ? 8 : (B <= 4 ? 4 : (B == 8 ? 2 : 1));  // chunks per slot
   static constexpr int CB = 4 * B;                                          // bytes per lane slice
+  // dwords between consecutive slices in a slot (3-bit slices start 4-aligned:
+  // a 96-bit register tuple must start on an even register)
+  static constexpr int SW = B == 3 ? 4 : B;
   static constexpr int META = B <= 8 ? kMetaBytes : 0;
 };
 
@@ -196,16 +200,16 @@ struct Slot {
 
 // Issue the loads of the slot of NS chunks starting at block-local chunk c of
 // one tile; positions at or past l1 re-read chunk l1 - 1, so every slot issues
-// the same number of loads.
+// the same number of loads.  voff = lane * 4B (the lane's slice offset).
 template <int B>
 __device__ __forceinline__ void issue(Slot& sl, __amdgpu_buffer_rsrc_t r, int record_bytes, int c,
-                                      int l1, int lane) {
+                                      int l1, int voff) {
   using G = Geo<B>;
 #pragma unroll
   for (int j = 0; j < G::NS; ++j) {
     const int cj = min(c + j, l1 - 1);
-    load_slice<B>(r, lane * G::CB, (cj >> 2) * record_bytes + G::META + (cj & 3) * (64 * G::CB),
-                  &sl.w[j * B]);
+    load_slice<B>(r, voff, (cj >> 2) * record_bytes + G::META + (cj & 3) * (64 * G::CB),
+                  &sl.w[j * G::SW]);
   }
 }
 
@@ -301,12 +305,12 @@ __device__ __forceinline__ void compute(const Slot& sl, int c, int l1, const uin
     if constexpr (B == 16) {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(frag(&sl.w[j * B + 4 * r]), xb, acc[r], 0, 0, 0);
+        acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(frag(&sl.w[j * G::SW + 4 * r]), xb, acc[r], 0, 0, 0);
     } else {
       const uint8_t* gm = meta + (pos >> 2) * kMetaBytes;
       const bool start = B <= 4 ? (j & 3) == 0 : (j == 0 && (c & 3) == 0);
       if (start) start_group<B, kExact>(gm, lane, gs);
-      quant_slice<B, kExact>(&sl.w[j * B], xb, gs);
+      quant_slice<B, kExact>(&sl.w[j * G::SW], xb, gs);
       const bool end = (B <= 4 && (j & 3) == 3) || (B == 8 && (pos & 3) == 3) || pos == l1 - 1;
       if (end) fold_group(gm, lane, gs, acc);
     }
@@ -323,18 +327,19 @@ __device__ __forceinline__ void run_segment(__amdgpu_buffer_rsrc_t rs, int recor
                                             int l1, const uint32_t* xlane, const uint8_t* meta,
                                             int lane, Slot& sa, Slot& sb, f4 (&acc)[4]) {
   constexpr int NS = Geo<B>::NS;
+  const int voff = lane * Geo<B>::CB;
   Slot sc;
   Group gs;
   for (int c = l0;;) {
-    issue<B>(sc, rs, record_bytes, c + 2 * NS, l1, lane);
+    issue<B>(sc, rs, record_bytes, c + 2 * NS, l1, voff);
     compute<B, kExact>(sa, c, l1, xlane, meta, lane, gs, acc);
     c += NS;
     if (c >= l1) break;
-    issue<B>(sa, rs, record_bytes, c + 2 * NS, l1, lane);
+    issue<B>(sa, rs, record_bytes, c + 2 * NS, l1, voff);
     compute<B, kExact>(sb, c, l1, xlane, meta, lane, gs, acc);
     c += NS;
     if (c >= l1) break;
-    issue<B>(sb, rs, record_bytes, c + 2 * NS, l1, lane);
+    issue<B>(sb, rs, record_bytes, c + 2 * NS, l1, voff);
     compute<B, kExact>(sc, c, l1, xlane, meta, lane, gs, acc);
     c += NS;
     if (c >= l1) break;
@@ -343,9 +348,24 @@ __device__ __forceinline__ void run_segment(__amdgpu_buffer_rsrc_t rs, int recor
 
 template <int B>
 __device__ __forceinline__ void preload(__amdgpu_buffer_rsrc_t rs, int rb, int l0, int l1,
-                                        int lane, Slot& sa, Slot& sb) {
-  issue<B>(sa, rs, rb, l0, l1, lane);
-  issue<B>(sb, rs, rb, l0 + Geo<B>::NS, l1, lane);
+                                        int voff, Slot& sa, Slot& sb) {
+  issue<B>(sa, rs, rb, l0, l1, voff);
+  issue<B>(sb, rs, rb, l0 + Geo<B>::NS, l1, voff);
+}
+
+__device__ __forceinline__ size_t align16(size_t v) { return (v + 15) & ~static_cast<size_t>(15); }
+
+// Global-address-space view of a device pointer.  Pointers rebuilt from the
+// argument block are generic to the compiler; generic (flat) loads also count
+// against the LDS counter and may alias LDS, which forces full waits between
+// the staging loads and the LDS stores.
+template <class T>
+__device__ __forceinline__ const __attribute__((address_space(1))) T* gl(const T* p) {
+  return (const __attribute__((address_space(1))) T*)(p);
+}
+__device__ __forceinline__ uint4 ldg16(const void* p) {
+  const u4v v = *gl(reinterpret_cast<const u4v*>(p));
+  return uint4{v.x, v.y, v.z, v.w};
 }
 
 // Dword `i` (compile-time) of the kernel-argument block, from the copy held one
@@ -382,13 +402,15 @@ struct Blocks {
 };
 
 // The wave's chunks [c0, c1), block by block (one block unless the layer is too
-// small to give every block its own waves).
+// small to give every block its own waves).  `wmeta` holds the metadata of the
+// wave's groups in order.
 template <bool kExact>
 __device__ __forceinline__ void run_blocks(const Blocks& bd, int first, int nblocks, int c0, int c1,
-                                           int cw0, int cw1, const uint8_t* packed, int tile,
-                                           const uint32_t* xrow, const uint8_t* meta_lds,
-                                           int meta_slot, bool preloaded, int lane, Slot& sa,
-                                           Slot& sb, f4 (&acc)[4]) {
+                                           int cw0, const uint8_t* packed, int tile,
+                                           const uint32_t* xrow, const uint8_t* wmeta,
+                                           bool preloaded, int lane, Slot& sa, Slot& sb,
+                                           f4 (&acc)[4]) {
+  int gslot = 0;
   for (int bi = first; bi < nblocks; ++bi) {
     const int bits = bd.bits(bi), cb = bd.cb(bi), ce = bd.ce(bi);
     const int lo = max(c0, cb), hi = min(c1, ce);
@@ -399,17 +421,15 @@ __device__ __forceinline__ void run_blocks(const Blocks& bd, int first, int nblo
     const int l0 = lo - cb, l1 = hi - cb;
     // block-local chunk 0 of this block, relative to the staged range
     const uint32_t* xlane = xrow + (cb - cw0) * 16;
-    // LDS metadata of block-local group 0 (the work-group staged this block's
-    // groups from the one holding max(cw0, block start))
-    const int wg_lo = max(cw0, cb);
-    const uint8_t* meta = meta_lds + (meta_slot - ((wg_lo - cb) >> 2)) * kMetaBytes;
+    // metadata of block-local group 0 (only groups >= l0 / 4 are read)
+    const uint8_t* meta = wmeta + (gslot - (l0 >> 2)) * kMetaBytes;
     if (!preloaded || bi != first) {  // a wave that spans blocks (small layers only)
       switch (bits) {
-        case 2: preload<2>(rs, rb, l0, l1, lane, sa, sb); break;
-        case 3: preload<3>(rs, rb, l0, l1, lane, sa, sb); break;
-        case 4: preload<4>(rs, rb, l0, l1, lane, sa, sb); break;
-        case 8: preload<8>(rs, rb, l0, l1, lane, sa, sb); break;
-        default: preload<16>(rs, rb, l0, l1, lane, sa, sb); break;
+        case 2: preload<2>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
+        case 3: preload<3>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
+        case 4: preload<4>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
+        case 8: preload<8>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
+        default: preload<16>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
       }
     }
     switch (bits) {
@@ -419,12 +439,8 @@ __device__ __forceinline__ void run_blocks(const Blocks& bd, int first, int nblo
       case 8: run_segment<8, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
       default: run_segment<16, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
     }
-    if (bits <= 8) {
-      const int whi = min(cw1, ce);
-      meta_slot += ((whi - 1 - cb) >> 2) + 1 - ((wg_lo - cb) >> 2);
-    }
+    if (bits <= 8) gslot += ((l1 - 1) >> 2) + 1 - (l0 >> 2);
   }
-
 }
 
 __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
@@ -455,104 +471,170 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   const int32_t* perm = KARG(const int32_t*, perm);
   const uint16_t* xg = KARG(const uint16_t*, x);
   const int kdim = KARG(int32_t, k);
-  // Start streaming this wave's first two slots before staging x' and metadata.
+  // ---- Prologue.  Vector loads complete in issue order, so the order of
+  // issue below is the order in which the wave can use them: permutation ->
+  // activation gathers and group metadata -> the first two weight slots.  The
+  // gathers are waited for (x' into LDS, barrier) while the weight slots are
+  // still in flight.
   int first = 0;
 #pragma unroll
   for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) first += (i < nblocks && bd.ce(i) <= c0) ? 1 : 0;
-  Slot sa, sb;
-  bool preloaded = false;
-  if (c0 < c1 && first < nblocks) {
-    const int fb = bd.bits(first), fcb = bd.cb(first);
-    const int hi = min(c1, bd.ce(first));
-    const __amdgpu_buffer_rsrc_t rs =
-        tile_rsrc(packed + bd.off(first) + tile * bd.tb(first), bd.tb(first));
-    const int rb = bd.rb(first);
-    preloaded = true;
-    switch (fb) {
-      case 2: preload<2>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
-      case 3: preload<3>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
-      case 4: preload<4>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
-      case 8: preload<8>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
-      default: preload<16>(rs, rb, c0 - fcb, hi - fcb, lane, sa, sb); break;
-    }
-  }
+  const bool has_work = c0 < c1 && first < nblocks;
+  const int fb = has_work ? bd.bits(first) : 16, fcb = has_work ? bd.cb(first) : 0;
+  const int fl0 = c0 - fcb, fl1 = has_work ? min(c1, bd.ce(first)) - fcb : 0;
+  const int frb = has_work ? bd.rb(first) : 0;
+  const uint8_t* ftile = has_work ? packed + bd.off(first) + tile * bd.tb(first) : packed;
+  // The first block's slice offset, formed before any staging load is issued
+  // (an opaque value the compiler keeps live: rematerialized later, it would
+  // land in a register with a pending load and cost a full wait).
+  int fvoff;
+  asm volatile("v_mul_u32_u24 %0, %1, %2" : "=v"(fvoff) : "v"(lane), "s"(4 * fb));
 
-  // LDS: x' rows 0..m-1, a zero row m (MFMA columns of absent tokens), then the
-  // metadata of every group the work-group touches.
+  // LDS: x' rows 0..m-1 and a zero row m (MFMA columns of absent tokens) for
+  // the work-group's channels, then each wave's own group metadata.
   uint16_t* xs16 = reinterpret_cast<uint16_t*>(smem);
-  uint8_t* meta_lds = reinterpret_cast<uint8_t*>(smem) + static_cast<size_t>(m + 1) * range * 2;
+  const int wave_groups = KARG(int32_t, wave_groups);
+  uint8_t* wmeta = reinterpret_cast<uint8_t*>(smem) + align16((m + 1) * range * 2) +
+                   static_cast<size_t>(wave) * wave_groups * kMetaBytes;
 
-  // Metadata: group records of the blocks with b <= 8 that overlap [cw0, cw1),
-  // copied 16 bytes per thread and round.  The zero points are checked on the
-  // way: the fast unpack needs every one to be an integer with |z| <= 1023.
-  bool z_ok = true;
+  // (1) Permutation of this thread's channels: 8 consecutive channels in each
+  // of kFastRounds rounds of 2048.  The code is branch-free so that every load
+  // is issued before the first use: indices are clamped, results masked, and
+  // without a permutation the (ignored) index loads read the packed buffer,
+  // which always holds more than 4k bytes.
+  constexpr int kRound = kWaves * 64 * 8;
+  constexpr int kFastRounds = 4;
+  const int fast_end = min(range, kFastRounds * kRound);
+  const bool use_perm = perm != nullptr;
+  const int32_t* pbase = use_perm ? perm : reinterpret_cast<const int32_t*>(packed);
+  int src[kFastRounds][8];
+#pragma unroll
+  for (int u = 0; u < kFastRounds; ++u) {
+    const int kk = u * kRound + static_cast<int>(threadIdx.x) * 8;
+    const bool has = kk < fast_end;
+    const int kp0 = kbase + (has ? kk : 0);
+    const uint4 p0 = ldg16(pbase + kp0), p1 = ldg16(pbase + kp0 + 4);
+    const int pv[8] = {static_cast<int>(p0.x), static_cast<int>(p0.y), static_cast<int>(p0.z),
+                       static_cast<int>(p0.w), static_cast<int>(p1.x), static_cast<int>(p1.y),
+                       static_cast<int>(p1.z), static_cast<int>(p1.w)};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int v = use_perm ? pv[e] : kp0 + e;
+      src[u][e] = has && static_cast<unsigned>(v) < static_cast<unsigned>(kdim) ? v : -1;
+    }
+  }
+  // (2) Activations of token 0 for those channels.
+  uint32_t q[kFastRounds][4];
   {
-    int slot0 = 0;
+    const auto xr = gl(xg);
 #pragma unroll
-    for (int bi = 0; bi < POLYQ_MAX_BLOCKS; ++bi) {
-      if (bi >= nblocks || bd.bits(bi) > 8) continue;
-      const int lo = max(cw0, bd.cb(bi)), hi = min(cw1, bd.ce(bi));
-      if (lo >= hi) continue;
-      const int g0 = (lo - bd.cb(bi)) >> 2, g1 = ((hi - 1 - bd.cb(bi)) >> 2) + 1;
-      const uint8_t* tile_base = packed + bd.off(bi) + tile * bd.tb(bi);
-      const int pieces = (g1 - g0) * (kMetaBytes / 16);
-      for (int i = threadIdx.x; i < pieces; i += blockDim.x) {
-        const int g = g0 + i / (kMetaBytes / 16), o = (i % (kMetaBytes / 16)) * 16;
-        const uint4 v = *reinterpret_cast<const uint4*>(tile_base + g * bd.rb(bi) + o);
-        *reinterpret_cast<uint4*>(meta_lds + (slot0 + g - g0) * kMetaBytes + o) = v;
-        if (o < kMetaBytes / 2) {
-          const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    for (int u = 0; u < kFastRounds; ++u) {
+      uint32_t h[8];
 #pragma unroll
-          for (int h = 0; h < 8; ++h) {
-            const float z = static_cast<float>(
-                __builtin_bit_cast(_Float16, static_cast<uint16_t>(w[h >> 1] >> (16 * (h & 1)))));
-            z_ok = z_ok && z == truncf(z) && fabsf(z) <= 1023.f;
-          }
-        }
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t v = xr[max(src[u][e], 0)];
+        h[e] = src[u][e] >= 0 ? v : 0u;
       }
-      slot0 += g1 - g0;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) q[u][d] = h[2 * d] | (h[2 * d + 1] << 16);
     }
   }
+  // (3) Metadata of the wave's first groups (four 16-byte pieces per lane).
+  const int fg0 = fl0 >> 2, fpieces = (fb <= 8 && fl0 < fl1) ? ((((fl1 - 1) >> 2) + 1 - fg0) * 16) : 0;
+  uint4 mv[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int j = min(u * 64 + lane, max(fpieces - 1, 0));
+    mv[u] = ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16);
+  }
+  // (4) The first two weight slots of the wave's first block.
+  Slot sa, sb;
+  if (has_work) {
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, bd.tb(first));
+    switch (fb) {
+      case 2: preload<2>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+      case 3: preload<3>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+      case 4: preload<4>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+      case 8: preload<8>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+      default: preload<16>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+    }
+  }
+  const bool preloaded = has_work;
+  // (5) x' of token 0 and the zero row into LDS.
+#pragma unroll
+  for (int u = 0; u < kFastRounds; ++u) {
+    const int kk = u * kRound + static_cast<int>(threadIdx.x) * 8;
+    if (kk < fast_end) {
+      *reinterpret_cast<uint4*>(xs16 + kk) = uint4{q[u][0], q[u][1], q[u][2], q[u][3]};
+      *reinterpret_cast<uint4*>(xs16 + m * range + kk) = uint4{0u, 0u, 0u, 0u};
+    }
+  }
+  // (6) Rare: more tokens, or channels past the fast rounds (these loads wait
+  // behind the weight slots).
+  auto stage_slow = [&](int k_lo, int k_hi, int t_lo, bool zero_row) {
+    for (int kk = k_lo + static_cast<int>(threadIdx.x) * 8; kk < k_hi; kk += kRound) {
+      int sr[8];
+      const uint4 p0 = ldg16(pbase + kbase + kk), p1 = ldg16(pbase + kbase + kk + 4);
+      const int pv[8] = {static_cast<int>(p0.x), static_cast<int>(p0.y), static_cast<int>(p0.z),
+                         static_cast<int>(p0.w), static_cast<int>(p1.x), static_cast<int>(p1.y),
+                         static_cast<int>(p1.z), static_cast<int>(p1.w)};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int v = use_perm ? pv[e] : kbase + kk + e;
+        sr[e] = static_cast<unsigned>(v) < static_cast<unsigned>(kdim) ? v : -1;
+      }
+      for (int t = t_lo; t < m; ++t) {
+        const auto xr = gl(xg + static_cast<int64_t>(t) * kdim);
+        uint32_t h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) h[e] = sr[e] >= 0 ? static_cast<uint32_t>(xr[max(sr[e], 0)]) : 0u;
+        *reinterpret_cast<uint4*>(xs16 + t * range + kk) =
+            uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+      }
+      if (zero_row) *reinterpret_cast<uint4*>(xs16 + m * range + kk) = uint4{0u, 0u, 0u, 0u};
+    }
+  };
+  if (m > 1) stage_slow(0, fast_end, 1, false);
+  if (range > fast_end) stage_slow(fast_end, range, 0, true);
+  __syncthreads();
 
-  // x'[i][k'] = x[i][perm[k']] for this work-group's clustered channels.  Each
-  // thread takes 8 consecutive channels per round of 2048: two 16-byte perm
-  // loads, then all of its gathers before any LDS store, so a round costs two
-  // memory latencies (one without a permutation).
-  for (int kk0 = threadIdx.x * 8; kk0 < range; kk0 += blockDim.x * 8) {
-    const int kp0 = kbase + kk0;
-    if (perm != nullptr) {
-      const int4* pp = reinterpret_cast<const int4*>(perm + kp0);
-      const int4 p0 = pp[0], p1 = pp[1];
-      const int src[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-      for (int mi = 0; mi < m; mi += 2) {
-        uint16_t v[2][8];
+  // (7) The wave's own metadata into LDS (the zero points are checked on the
+  // way: the fast unpack needs every one to be an integer with |z| <= 1023),
+  // then any groups beyond the first 16 and any further blocks.
+  bool z_ok = true;
+  auto meta_store = [&](uint4* dst, int j, uint4 v) {
+    dst[j] = v;
+    if ((j & 15) < kMetaBytes / 32) {  // a piece of zero points
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const bool ok = mi + u < m && static_cast<unsigned>(src[e]) < static_cast<unsigned>(kdim);
-            v[u][e] = ok ? xg[static_cast<int64_t>(mi + u) * kdim + src[e]] : 0;
-          }
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          if (mi + u < m) {
-            uint4 q;
-            q.x = v[u][0] | (static_cast<uint32_t>(v[u][1]) << 16);
-            q.y = v[u][2] | (static_cast<uint32_t>(v[u][3]) << 16);
-            q.z = v[u][4] | (static_cast<uint32_t>(v[u][5]) << 16);
-            q.w = v[u][6] | (static_cast<uint32_t>(v[u][7]) << 16);
-            *reinterpret_cast<uint4*>(xs16 + (mi + u) * range + kk0) = q;
-          }
-        }
+      for (int h = 0; h < 8; ++h) {
+        const float z = static_cast<float>(
+            __builtin_bit_cast(_Float16, static_cast<uint16_t>(w[h >> 1] >> (16 * (h & 1)))));
+        z_ok = z_ok && z == truncf(z) && fabsf(z) <= 1023.f;
       }
-    } else {
-      for (int mi = 0; mi < m; ++mi)
-        *reinterpret_cast<uint4*>(xs16 + mi * range + kk0) =
-            *reinterpret_cast<const uint4*>(xg + static_cast<int64_t>(mi) * kdim + kp0);
     }
-    *reinterpret_cast<uint4*>(xs16 + m * range + kk0) = uint4{0u, 0u, 0u, 0u};
+  };
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    if (u * 64 + lane < fpieces) meta_store(reinterpret_cast<uint4*>(wmeta), u * 64 + lane, mv[u]);
+  {
+    int gslot = 0;
+    for (int bi = first; bi < nblocks; ++bi) {
+      const int cb = bd.cb(bi), ce = bd.ce(bi);
+      const int lo = max(c0, cb), hi = min(c1, ce);
+      if (lo >= hi) break;
+      if (bd.bits(bi) > 8) continue;
+      const int g0 = (lo - cb) >> 2, g1 = ((hi - 1 - cb) >> 2) + 1;
+      const int pieces = (g1 - g0) * (kMetaBytes / 16);
+      const int rb = bd.rb(bi);
+      const uint8_t* rec0 = packed + bd.off(bi) + tile * bd.tb(bi) + static_cast<int64_t>(g0) * rb;
+      uint4* dst = reinterpret_cast<uint4*>(wmeta) + gslot * (kMetaBytes / 16);
+      for (int j = (bi == first ? 4 * 64 : 0) + lane; j < pieces; j += 64)
+        meta_store(dst, j, ldg16(rec0 + (j >> 4) * rb + (j & 15) * 16));
+      gslot += g1 - g0;
+    }
   }
-  const bool exact = __syncthreads_and(z_ok);
+  const bool exact = __all(z_ok);
 
   f4 acc[4];
 #pragma unroll
@@ -560,20 +642,12 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   const int tok = lane & 15;
   // this lane's activation row (token lane%16, or the zero row) and channel quarter
   const uint32_t* xrow = smem + ((tok < m ? tok : m) * range + 8 * (lane >> 4)) / 2;
-  // LDS metadata slot of the first staged group of each block
-  int meta_slot = 0;
-#pragma unroll
-  for (int bi = 0; bi < POLYQ_MAX_BLOCKS; ++bi) {
-    if (bi >= first || bd.bits(bi) > 8) continue;
-    const int lo = max(cw0, bd.cb(bi)), hi = min(cw1, bd.ce(bi));
-    if (lo < hi) meta_slot += ((hi - 1 - bd.cb(bi)) >> 2) + 1 - ((lo - bd.cb(bi)) >> 2);
-  }
   if (exact)
-    run_blocks<true>(bd, first, nblocks, c0, c1, cw0, cw1, packed, tile, xrow, meta_lds, meta_slot,
-                     preloaded, lane, sa, sb, acc);
+    run_blocks<true>(bd, first, nblocks, c0, c1, cw0, packed, tile, xrow, wmeta, preloaded, lane,
+                     sa, sb, acc);
   else
-    run_blocks<false>(bd, first, nblocks, c0, c1, cw0, cw1, packed, tile, xrow, meta_lds,
-                      meta_slot, preloaded, lane, sa, sb, acc);
+    run_blocks<false>(bd, first, nblocks, c0, c1, cw0, packed, tile, xrow, wmeta, preloaded, lane,
+                      sa, sb, acc);
 
   // Reduce the waves' partial sums (fixed order).  MFMA result layout: lane l
   // holds rows 16r + 4(l/16) + e of token l%16.
@@ -624,9 +698,18 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   if (ticket % static_cast<uint32_t>(a.S) != static_cast<uint32_t>(a.S - 1)) return;
   for (int mi = 0; mi < m; ++mi) {
     float v = 0.f;
-    for (int s2 = 0; s2 < a.S; ++s2)
-      v += __hip_atomic_exchange(&a.partial[(static_cast<int64_t>(s2) * m + mi) * a.rows_pad + row],
-                                 0.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int s0 = 0; s0 < a.S; s0 += 8) {  // eight reads in flight at a time
+      float t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        t[u] = s0 + u < a.S
+                   ? __hip_atomic_exchange(
+                         &a.partial[(static_cast<int64_t>(s0 + u) * m + mi) * a.rows_pad + row], 0.f,
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                   : 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v += t[u];
+    }
     if (row < a.n) a.y[static_cast<int64_t>(mi) * a.n + row] = v;
   }
   if (lane == 0) __hip_atomic_store(&a.counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -666,6 +749,7 @@ extern "C" polyq_status polyq_gemv(const polyq_layout* layout, const void* packe
   a.nblocks = L.nblocks;
   a.rows_pad = L.n_tiles * kTileRows;
   a.S = plan.S;
+  a.wave_groups = plan.lds_groups;
   if (plan.W != kWaves) return POLYQ_ERR_UNSUPPORTED;
   a.partial = nullptr;
   a.counter = nullptr;

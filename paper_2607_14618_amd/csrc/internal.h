@@ -22,7 +22,7 @@ struct GemvPlan {
   int32_t S;                    // WG splits per 64-row tile
   int32_t W;                    // waves per WG
   int32_t lds_chunks;           // largest chunk range of one WG
-  int32_t lds_groups;           // most group records one WG stages (b <= 8 blocks)
+  int32_t lds_groups;           // most group records one wave stages (b <= 8 blocks)
   int32_t nsplit;               // S * W
   int32_t split[kMaxSplitEntries + 1];
 };

@@ -95,9 +95,10 @@ bool layout_is_valid(const polyq_layout* L) {
 }
 
 size_t gemv_lds_bytes(const GemvPlan& p, int32_t m) {
-  // x' rows + a zero row, then the staged group metadata; reused for the reduction
-  const size_t xs = static_cast<size_t>(p.lds_chunks) * kChunk * (m + 1) * 2 +
-                    static_cast<size_t>(p.lds_groups) * kMetaBytes;
+  // x' rows + a zero row (16-byte aligned), then every wave's group metadata;
+  // reused for the reduction
+  const size_t xs = static_cast<size_t>(align_up(static_cast<int64_t>(p.lds_chunks) * kChunk * (m + 1) * 2, 16)) +
+                    static_cast<size_t>(p.W) * p.lds_groups * kMetaBytes;
   const size_t red = static_cast<size_t>(p.W) * m * kTileRows * 4;
   return std::max(xs, red);
 }
@@ -217,10 +218,9 @@ int plan_gemv(const polyq_layout& L, int32_t m, GemvPlan* p) {
     p->nsplit = S * W;
     if (!partition_by_block(L, S * W, p->split)) partition(L, prefix, S * W, p->split);
     int worst = 0, worst_groups = 0;
-    for (int s = 0; s < S; ++s) {
-      worst = std::max(worst, p->split[(s + 1) * W] - p->split[s * W]);
-      worst_groups = std::max(worst_groups, groups_touched(L, p->split[s * W], p->split[(s + 1) * W]));
-    }
+    for (int s = 0; s < S; ++s) worst = std::max(worst, p->split[(s + 1) * W] - p->split[s * W]);
+    for (int w = 0; w < S * W; ++w)
+      worst_groups = std::max(worst_groups, groups_touched(L, p->split[w], p->split[w + 1]));
     p->lds_chunks = worst;
     p->lds_groups = worst_groups;
     if (gemv_lds_bytes(*p, m) <= kLdsBudget) return 0;
