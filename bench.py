@@ -52,6 +52,8 @@ def _args():
     p.add_argument("--qwen", action="store_true")
     p.add_argument("--qwen-layers", type=int, default=64)
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB")
+    p.add_argument("--per-linear", action="store_true",
+                   help="one launch per linear instead of one per shared-input group")
     return p.parse_args()
 
 
@@ -138,30 +140,63 @@ def time_steps(torch, steps, warmup, launches):
     return t0.elapsed_time(t1) / steps, per
 
 
-def decode_launches(torch, copies, variant):
+# Linears of a decoder layer that share an input and run as one launch: a
+# decode step can only batch what one activation vector feeds (q/k/v, gate/up).
+SHARED_INPUT = (("q_proj", "k_proj", "v_proj"), ("o_proj",), ("gate_proj", "up_proj"),
+                ("down_proj",))
+
+
+def schedule(layer, grouped):
+    """Launches of one layer step: lists of linear indices."""
+    if not grouped:
+        return [[j] for j in range(len(layer))]
+    names = [nm for nm, _, _ in layer]
+    out, seen = [], set()
+    for grp in SHARED_INPUT:
+        idx = [names.index(n) for n in grp if n in names]
+        if idx:
+            out.append(idx)
+            seen.update(idx)
+    out += [[j] for j in range(len(layer)) if j not in seen]
+    return out
+
+
+def decode_launches(torch, pq, copies, variant, grouped=True):
     dev = torch.device("cuda", 0)
     ys = [torch.empty((x.shape[0], pl.n), dtype=torch.float32, device=dev) for _, pl, x in copies[0]]
     xs = [pl.permute(x) if variant == "P" else x for _, pl, x in copies[0]]
     pre = variant == "P"
+    sched = schedule(copies[0], grouped)
+
+    def launch(copy, idx):
+        if len(idx) == 1:
+            j = idx[0]
+            return lambda: copy[j][1].decode(xs[j], pre_permuted=pre, y=ys[j])
+        return lambda: pq.decode_batch([copy[j][1] for j in idx], [xs[j] for j in idx],
+                                       pre_permuted=pre, ys=[ys[j] for j in idx])
+
+    per_copy = [[launch(copy, idx) for idx in sched] for copy in copies]
 
     def launches(i):
-        return [(lambda pl=pl, j=j: pl.decode(xs[j], pre_permuted=pre, y=ys[j]))
-                for j, (_, pl, _) in enumerate(copies[i % len(copies)])]
-    return launches
+        return per_copy[i % len(copies)]
+    return launches, sched
 
 
 def decode_figure(torch, pq, synth, steps, warmup, variant, config=1, mix=None, target_bits=None,
-                  m=1):
+                  m=1, grouped=True):
     layer = build_layer(torch, pq, synth, config, mix=mix, target_bits=target_bits, m=m)
     step_bytes = sum(pl.weight_bytes for _, pl, _ in layer)
     copies = rotation(layer, step_bytes)
-    ms, per = time_steps(torch, steps, warmup, decode_launches(torch, copies, variant))
+    launches, sched = decode_launches(torch, pq, copies, variant, grouped)
+    ms, per = time_steps(torch, steps, warmup, launches)
     kern_ms = sum(per)
     res = {"ms_step": ms, "kern_ms": kern_ms, "step_bytes": step_bytes, "copies": len(copies),
+           "launches": len(sched),
            "gbs": step_bytes / (ms * 1e-3) / 1e9, "kernel_gbs": step_bytes / (kern_ms * 1e-3) / 1e9,
-           "per_linear": {nm: {"us": round(t * 1e3, 2), "weight_bytes": pl.weight_bytes,
-                               "gbs": round(pl.weight_bytes / (t * 1e-3) / 1e9, 1)}
-                          for (nm, pl, _), t in zip(layer, per)}}
+           "per_launch": {"+".join(layer[j][0] for j in idx): {
+               "us": round(t * 1e3, 2), "weight_bytes": sum(layer[j][1].weight_bytes for j in idx),
+               "gbs": round(sum(layer[j][1].weight_bytes for j in idx) / (t * 1e-3) / 1e9, 1)}
+               for idx, t in zip(sched, per)}}
     del copies, layer
     torch.cuda.empty_cache()
     return res
@@ -248,11 +283,11 @@ def main_default(a, torch, pq, synth):
         return
     _log("building the synthetic Llama2-13B layer")
     t0 = time.time()
-    d = decode_figure(torch, pq, synth, a.steps, a.warmup, a.variant)
+    d = decode_figure(torch, pq, synth, a.steps, a.warmup, a.variant, grouped=not a.per_linear)
     _log(f"{d['copies']} copies x {d['step_bytes'] / 1e6:.2f} MB ({time.time() - t0:.1f} s); "
          f"decode: {d['ms_step'] * 1e3:.1f} us/step, {d['gbs']:.1f} GB/s; "
          f"kernels {d['kern_ms'] * 1e3:.1f} us, {d['kernel_gbs']:.1f} GB/s")
-    nlin = len(d["per_linear"])
+    nlin = d["launches"]
     extra = {
         "roofline": {"bound": "hbm", "achieved": round(d["kernel_gbs"], 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(d["kernel_gbs"] / HBM_PEAK_GBS, 4),
@@ -260,7 +295,7 @@ def main_default(a, torch, pq, synth):
                      "kernel": "gemv_kernel",
                      "bytes_per_launch": round(d["step_bytes"] / nlin),
                      "avg_launch_us": round(d["kern_ms"] * 1e3 / nlin, 3),
-                     "per_linear": d["per_linear"]},
+                     "per_launch": d["per_launch"]},
     }
     if not a.no_prefill:
         _log("prefill GEMM, M=512")
@@ -275,7 +310,9 @@ def main_default(a, torch, pq, synth):
           "activations, " + ("channel permutation gathered in-kernel" if a.variant == "G"
                              else "activations pre-permuted"))
     line(d["gbs"], "GB/s", a.steps, a.warmup, d["ms_step"], "f16",
-         {"workload": wl, "m": 1, "avg_bits": 3.0, "variant": a.variant, "linears": nlin,
+         {"workload": wl, "m": 1, "avg_bits": 3.0, "variant": a.variant, "linears": 7,
+          "launches": ("one per linear" if a.per_linear else
+                       "one per shared-input group: q/k/v, o, gate/up, down"),
           "weight_bytes_per_step": d["step_bytes"], "rotation_copies": d["copies"],
           "pct_hbm_peak": round(100 * d["gbs"] / HBM_PEAK_GBS, 2)}, **extra)
 
@@ -308,12 +345,12 @@ def main_qwen(a, torch, pq, synth):
     layers = [build_layer(torch, pq, synth, 4, layer=l) for l in range(a.qwen_layers)]
     step_bytes = sum(pl.weight_bytes for L in layers for _, pl, _ in L)
     _log(f"{step_bytes / 1e9:.2f} GB packed in {time.time() - t0:.1f} s")
-    flat = [t for L in layers for t in L]
     res = {}
     for variant in ("G", "P"):
-        launches = decode_launches(torch, [flat], variant)
+        per_layer = [decode_launches(torch, pq, [L], variant, not a.per_linear) for L in layers]
+        flat = [f for launches, _ in per_layer for f in launches(0)]
         steps, warmup = max(2, a.steps // 40), 1
-        ms, per = time_steps(torch, steps, warmup, launches)
+        ms, per = time_steps(torch, steps, warmup, lambda i: flat)
         res[variant] = {"ms_per_step": round(ms, 4), "gbs": round(step_bytes / (ms * 1e-3) / 1e9, 1),
                         "kernel_gbs": round(step_bytes / (sum(per) * 1e-3) / 1e9, 1)}
         _log(f"qwen {variant}: {res[variant]}")

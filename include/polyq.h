@@ -45,6 +45,7 @@ extern "C" {
 #define POLYQ_GROUP 128       /* quantization group, counted from each block start   */
 #define POLYQ_TILE_ROWS 64    /* output rows per packed tile                         */
 #define POLYQ_MAX_M_GEMV 16   /* tokens per polyq_gemv call                          */
+#define POLYQ_MAX_BATCH 8     /* linears per polyq_gemv_batch call                   */
 #define POLYQ_MAX_K (1 << 20) /* input channels                                      */
 #define POLYQ_MAX_N (1 << 24) /* output channels                                     */
 
@@ -170,6 +171,31 @@ size_t polyq_gemv_workspace_bytes(const polyq_layout* layout, int32_t m);
 polyq_status polyq_gemv(const polyq_layout* layout, const void* packed, const int32_t* perm,
                         const uint16_t* x, int32_t m, float* y, void* workspace,
                         size_t workspace_bytes, void* stream);
+
+/*
+ * polyq_gemv_batch -- up to POLYQ_MAX_BATCH independent decode products in one
+ * launch (e.g. the q/k/v projections, or gate/up, which share x and perm):
+ * item i computes exactly what polyq_gemv(items[i].layout, items[i].packed,
+ * items[i].perm, items[i].x, m, items[i].y, ...) computes, with the same
+ * argument rules per item.  Items may share x and perm; no y may overlap any
+ * input or another y.  The work split of every item is sized for the whole
+ * launch, so the workspace is queried for the batch:
+ *   workspace of at least polyq_gemv_batch_workspace_bytes(items, count, m)
+ *   bytes (only the layout field of each item is read by the query; 0 on an
+ *   invalid request), zero-filled before first use and left zero-filled by
+ *   every completed call, as for polyq_gemv.
+ */
+typedef struct {
+  const polyq_layout* layout;
+  const void* packed;
+  const int32_t* perm; /* may be NULL (x already clustered) */
+  const uint16_t* x;   /* fp16 [m][k] */
+  float* y;            /* fp32 [m][n] */
+} polyq_gemv_item;
+
+size_t polyq_gemv_batch_workspace_bytes(const polyq_gemv_item* items, int32_t count, int32_t m);
+polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32_t m,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * polyq_gemm -- prefill product for any m >= 1 (bf16 activations):

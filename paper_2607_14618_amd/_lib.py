@@ -21,6 +21,7 @@ QUANTUM = 32
 GROUP = 128
 TILE_ROWS = 64
 MAX_M_GEMV = 16
+MAX_BATCH = 8
 
 STATUS = {0: "POLYQ_OK", 1: "POLYQ_ERR_ARG", 2: "POLYQ_ERR_BITS", 3: "POLYQ_ERR_QUANTUM",
           4: "POLYQ_ERR_SHAPE", 5: "POLYQ_ERR_CAPACITY", 6: "POLYQ_ERR_UNSUPPORTED",
@@ -28,7 +29,8 @@ STATUS = {0: "POLYQ_OK", 1: "POLYQ_ERR_ARG", 2: "POLYQ_ERR_BITS", 3: "POLYQ_ERR_
 
 # every symbol include/polyq.h declares
 EXPORTS = ("polyq_plan", "polyq_pack", "polyq_unpack", "polyq_permute", "polyq_gemv_workspace_bytes",
-           "polyq_gemv", "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_status_str")
+           "polyq_gemv", "polyq_gemv_batch_workspace_bytes", "polyq_gemv_batch",
+           "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_status_str")
 
 
 class Block(ctypes.Structure):
@@ -57,6 +59,11 @@ class Layout(ctypes.Structure):
     def __repr__(self):
         return (f"Layout(n={self.n}, k={self.k}, blocks={self.blocks}, n_groups={self.n_groups}, "
                 f"packed_bytes={self.packed_bytes}, weight_bytes={self.weight_bytes})")
+
+
+class GemvItem(ctypes.Structure):
+    _fields_ = [("layout", ctypes.POINTER(Layout)), ("packed", ctypes.c_void_p),
+                ("perm", ctypes.c_void_p), ("x", ctypes.c_void_p), ("y", ctypes.c_void_p)]
 
 
 class PolyQError(RuntimeError):
@@ -89,13 +96,17 @@ def lib() -> ctypes.CDLL:
             L.polyq_gemv_workspace_bytes.argtypes = [lp, i32]
             L.polyq_gemv_workspace_bytes.restype = sz
             L.polyq_gemv.argtypes = [lp, vp, vp, vp, i32, vp, vp, sz, vp]
+            ip = ctypes.POINTER(GemvItem)
+            L.polyq_gemv_batch_workspace_bytes.argtypes = [ip, i32, i32]
+            L.polyq_gemv_batch_workspace_bytes.restype = sz
+            L.polyq_gemv_batch.argtypes = [ip, i32, i32, vp, sz, vp]
             L.polyq_gemm_workspace_bytes.argtypes = [lp, i32, ctypes.c_int]
             L.polyq_gemm_workspace_bytes.restype = sz
             L.polyq_gemm.argtypes = [lp, vp, vp, vp, i32, vp, vp, sz, vp]
             L.polyq_status_str.argtypes = [ctypes.c_int]
             L.polyq_status_str.restype = ctypes.c_char_p
             for name in ("polyq_plan", "polyq_pack", "polyq_unpack", "polyq_permute",
-                         "polyq_gemv", "polyq_gemm"):
+                         "polyq_gemv", "polyq_gemv_batch", "polyq_gemm"):
                 getattr(L, name).restype = ctypes.c_int
             _lib = L
     return _lib
@@ -246,6 +257,42 @@ def gemv(layout: Layout, packed: torch.Tensor, perm: Optional[torch.Tensor], x: 
                             _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                             _stream(dev)), "polyq_gemv")
     return y
+
+
+def gemv_batch(items: Sequence[Tuple[Layout, torch.Tensor, Optional[torch.Tensor], torch.Tensor,
+                                     Optional[torch.Tensor]]],
+               workspace: Optional[torch.Tensor] = None):
+    """One launch of several GEMVs: items are (layout, packed, perm, x, y or None)
+    with the same token count m.  Returns the list of outputs."""
+    if not 1 <= len(items) <= MAX_BATCH:
+        raise ValueError(f"1..{MAX_BATCH} items per batch")
+    arr = (GemvItem * len(items))()
+    keep, ys, m, dev = [], [], None, None
+    for i, (layout, packed, perm, x, y) in enumerate(items):
+        x2 = x if x.dim() == 2 else x.reshape(1, -1)
+        d = _need_cuda(packed, perm, x2, y, workspace)
+        dev = d if dev is None else dev
+        if d != dev:
+            raise ValueError("all tensors must be on the same device")
+        if x2.dtype != torch.float16 or x2.shape[1] != layout.k:
+            raise ValueError("x must be fp16 [m][k]")
+        if m is None:
+            m = x2.shape[0]
+        elif x2.shape[0] != m:
+            raise ValueError("every item of a batch has the same m")
+        if perm is not None and (perm.dtype != torch.int32 or perm.numel() != layout.k):
+            raise ValueError("perm must be int32 [k]")
+        if y is None:
+            y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
+        arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y))
+        keep.append(x2)
+        ys.append(y)
+    need = int(lib().polyq_gemv_batch_workspace_bytes(arr, len(items), m)) if 1 <= m <= MAX_M_GEMV else 0
+    ws = workspace if workspace is not None else _workspace("gemv", need, dev, zero=True)
+    _check(lib().polyq_gemv_batch(arr, len(items), m, _ptr(ws),
+                                  0 if ws is None else ws.numel() * ws.element_size(), _stream(dev)),
+           "polyq_gemv_batch")
+    return ys
 
 
 def gemm(layout: Layout, packed: torch.Tensor, perm: Optional[torch.Tensor], x: torch.Tensor,

@@ -23,6 +23,9 @@
 // reduce through LDS, and splits of a tile across work-groups are combined by
 // the last-arriving work-group (fixed order).
 #include <hip/hip_runtime.h>
+#include <string.h>
+
+#include <algorithm>
 
 #include "codec.h"
 #include "internal.h"
@@ -36,22 +39,35 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 4;  // waves per work-group (the host plan uses the same)
 
-struct GemvArgs {
+constexpr int kMaxItems = POLYQ_MAX_BATCH;
+
+// One linear of a launch: exactly 64 dwords, so that one vector load (a dword
+// per lane) fetches it.
+struct GemvItem {
   const uint8_t* packed;
   const int32_t* perm;
   const uint16_t* x;
   float* y;
   float* partial;     // [S][m][rows_pad], only when S > 1
   uint32_t* counter;  // [n_tiles], only when S > 1
-  int32_t n, k, m, nblocks, rows_pad, S;
-  int32_t wave_groups;  // LDS metadata slots per wave
+  int32_t n, k, nblocks, rows_pad, S, wave_groups, n_tiles, n_chunks;
   int32_t bits[POLYQ_MAX_BLOCKS];
   int32_t chunk_begin[POLYQ_MAX_BLOCKS];
-  int32_t chunk_end[POLYQ_MAX_BLOCKS];
+  int32_t wave_begin[POLYQ_MAX_BLOCKS];  // first wave (per tile) of each block
+  int32_t waves[POLYQ_MAX_BLOCKS];       // waves per tile given to each block
+  uint32_t magic[POLYQ_MAX_BLOCKS];      // div_magic(waves)
+  int32_t tile_bytes[POLYQ_MAX_BLOCKS];
   int64_t block_offset[POLYQ_MAX_BLOCKS];
-  int64_t tile_bytes[POLYQ_MAX_BLOCKS];
-  int64_t record_bytes[POLYQ_MAX_BLOCKS];
-  int32_t split[kMaxSplitEntries + 1];
+  int32_t pad[4];
+};
+
+// The launch: a 64-dword header (work-groups [wg_begin[i], wg_begin[i+1]) run
+// linear i), then the linears.
+struct GemvBatchArgs {
+  int32_t count, m;
+  int32_t wg_begin[kMaxItems + 1];
+  int32_t pad[64 - 2 - (kMaxItems + 1)];
+  GemvItem item[kMaxItems];
 };
 
 __device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
@@ -353,6 +369,52 @@ __device__ __forceinline__ void preload(__amdgpu_buffer_rsrc_t rs, int rb, int l
   issue<B>(sb, rs, rb, l0 + Geo<B>::NS, l1, voff);
 }
 
+// Dword `dw` of a 64-dword argument record held one dword per lane, as a
+// scalar (v_readlane; dw must be wave-uniform).
+template <class T>
+__device__ __forceinline__ T kfield(uint32_t kv, int dw) {
+  if constexpr (sizeof(T) == 8) {
+    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(kv, dw));
+    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(kv, dw + 1));
+    return __builtin_bit_cast(T, lo | (hi << 32));
+  } else {
+    return __builtin_bit_cast(T, static_cast<uint32_t>(__builtin_amdgcn_readlane(kv, dw)));
+  }
+}
+#define ITEM(T, field) kfield<T>(kv, offsetof(GemvItem, field) / 4)
+
+// Block descriptors of the work-group's linear, read from the per-lane copy of
+// its argument record with v_readlane at a uniform (possibly run-time) index:
+// no dependent loads, and no indexed private array for the compiler to spill
+// to scratch memory.
+struct Blocks {
+  uint32_t kv;
+  int nblocks, n_chunks;
+  __device__ int bits(int i) const { return kfield<int32_t>(kv, offsetof(GemvItem, bits) / 4 + i); }
+  __device__ int cb(int i) const { return kfield<int32_t>(kv, offsetof(GemvItem, chunk_begin) / 4 + i); }
+  // a block ends where the next one begins (i + 1 must be a compile-time index
+  // or uniform; reads past the last block fall back to the layer end)
+  __device__ int ce(int i) const {
+    return i + 1 < nblocks ? kfield<int32_t>(kv, offsetof(GemvItem, chunk_begin) / 4 + i + 1) : n_chunks;
+  }
+  __device__ int64_t off(int i) const {
+    return kfield<int64_t>(kv, offsetof(GemvItem, block_offset) / 4 + 2 * i);
+  }
+  __device__ int tb(int i) const { return kfield<int32_t>(kv, offsetof(GemvItem, tile_bytes) / 4 + i); }
+  // record of a group: 256 bytes of metadata (b <= 8) + 4 chunk slices of 256 b bytes
+  __device__ int rb(int i) const {
+    const int b = bits(i);
+    return (b <= 8 ? kMetaBytes : 0) + kChunksPerGroup * 64 * 4 * b;
+  }
+  __device__ void operator()(int i, int* c0, int* c1, int* w0, int* nw, uint32_t* mg) const {
+    *c0 = cb(i);
+    *c1 = ce(i);
+    *w0 = kfield<int32_t>(kv, offsetof(GemvItem, wave_begin) / 4 + i);
+    *nw = kfield<int32_t>(kv, offsetof(GemvItem, waves) / 4 + i);
+    *mg = kfield<uint32_t>(kv, offsetof(GemvItem, magic) / 4 + i);
+  }
+};
+
 __device__ __forceinline__ size_t align16(size_t v) { return (v + 15) & ~static_cast<size_t>(15); }
 
 // Global-address-space view of a device pointer.  Pointers rebuilt from the
@@ -368,109 +430,52 @@ __device__ __forceinline__ uint4 ldg16(const void* p) {
   return uint4{v.x, v.y, v.z, v.w};
 }
 
-// Dword `i` (compile-time) of the kernel-argument block, from the copy held one
-// dword per lane, as a scalar.
-#define KARG(T, field) kfield<T>(kv, offsetof(GemvArgs, field) / 4)
-template <class T>
-__device__ __forceinline__ T kfield(uint32_t kv, int dw) {
-  if constexpr (sizeof(T) == 8) {
-    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(kv, dw));
-    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(kv, dw + 1));
-    return __builtin_bit_cast(T, lo | (hi << 32));
-  } else {
-    return __builtin_bit_cast(T, static_cast<uint32_t>(__builtin_amdgcn_readlane(kv, dw)));
-  }
-}
-
-// Block descriptors, read from the per-lane copy of the argument block with
-// v_readlane at a uniform (possibly run-time) lane index: no dependent loads, and
-// no indexed private array for the compiler to spill to scratch memory.
-struct Blocks {
-  uint32_t kv;
-  __device__ int bits(int i) const { return kfield<int32_t>(kv, offsetof(GemvArgs, bits) / 4 + i); }
-  __device__ int cb(int i) const { return kfield<int32_t>(kv, offsetof(GemvArgs, chunk_begin) / 4 + i); }
-  __device__ int ce(int i) const { return kfield<int32_t>(kv, offsetof(GemvArgs, chunk_end) / 4 + i); }
-  __device__ int64_t off(int i) const {
-    return kfield<int64_t>(kv, offsetof(GemvArgs, block_offset) / 4 + 2 * i);
-  }
-  __device__ int64_t tb(int i) const {
-    return kfield<int64_t>(kv, offsetof(GemvArgs, tile_bytes) / 4 + 2 * i);
-  }
-  __device__ int rb(int i) const {
-    return kfield<int32_t>(kv, offsetof(GemvArgs, record_bytes) / 4 + 2 * i);
-  }
-};
-
-// The wave's chunks [c0, c1), block by block (one block unless the layer is too
-// small to give every block its own waves).  `wmeta` holds the metadata of the
-// wave's groups in order.
-template <bool kExact>
-__device__ __forceinline__ void run_blocks(const Blocks& bd, int first, int nblocks, int c0, int c1,
-                                           int cw0, const uint8_t* packed, int tile,
-                                           const uint32_t* xrow, const uint8_t* wmeta,
-                                           bool preloaded, int lane, Slot& sa, Slot& sb,
-                                           f4 (&acc)[4]) {
-  int gslot = 0;
-  for (int bi = first; bi < nblocks; ++bi) {
-    const int bits = bd.bits(bi), cb = bd.cb(bi), ce = bd.ce(bi);
-    const int lo = max(c0, cb), hi = min(c1, ce);
-    if (lo >= hi) break;
-    const int64_t tb = bd.tb(bi);
-    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(packed + bd.off(bi) + tile * tb, tb);
-    const int rb = bd.rb(bi);
-    const int l0 = lo - cb, l1 = hi - cb;
-    // block-local chunk 0 of this block, relative to the staged range
-    const uint32_t* xlane = xrow + (cb - cw0) * 16;
-    // metadata of block-local group 0 (only groups >= l0 / 4 are read)
-    const uint8_t* meta = wmeta + (gslot - (l0 >> 2)) * kMetaBytes;
-    if (!preloaded || bi != first) {  // a wave that spans blocks (small layers only)
-      switch (bits) {
-        case 2: preload<2>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
-        case 3: preload<3>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
-        case 4: preload<4>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
-        case 8: preload<8>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
-        default: preload<16>(rs, rb, l0, l1, lane * 4 * bits, sa, sb); break;
-      }
-    }
-    switch (bits) {
-      case 2: run_segment<2, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
-      case 3: run_segment<3, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
-      case 4: run_segment<4, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
-      case 8: run_segment<8, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
-      default: run_segment<16, kExact>(rs, rb, l0, l1, xlane, meta, lane, sa, sb, acc); break;
-    }
-    if (bits <= 8) gslot += ((l1 - 1) >> 2) + 1 - (l0 >> 2);
-  }
-}
-
-__global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
+// One work-group = (linear, 64-row tile, split); its four waves each take one
+// block's range of the split (wave_range) and share the split's staged x'.
+__global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a) {
   extern __shared__ uint32_t smem[];
-  const int tile = blockIdx.x, s = blockIdx.y;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  // The argument block is read with two vector loads (one dword per lane: the
-  // first 256 bytes, and this wave's split entries) and broadcast with
+  // The argument block is read with vector loads (one dword per lane: the
+  // batch header, then this work-group's linear) and broadcast with
   // v_readlane; scalar loads of it would miss the scalar cache line by line.
   const uint32_t* kargs = (const uint32_t*)(__builtin_amdgcn_kernarg_segment_ptr());
-  static_assert(offsetof(GemvArgs, split) == 256, "argument block layout");
-  const uint32_t kv = kargs[lane];
-  const uint32_t ks = kargs[64 + s * kWaves + min(lane, kWaves)];
-  const int m = KARG(int32_t, m);
-  const int cw0 = __builtin_amdgcn_readlane(ks, 0), cw1 = __builtin_amdgcn_readlane(ks, kWaves);
-  const int range = (cw1 - cw0) * kChunk;  // staged channels
-  const int kbase = cw0 * kChunk;
-  int c0 = cw0, c1 = cw0;
+  static_assert(sizeof(GemvItem) == 256 && offsetof(GemvBatchArgs, item) == 256, "argument layout");
+  const uint32_t hv = kargs[lane];
+  const int count = kfield<int32_t>(hv, offsetof(GemvBatchArgs, count) / 4);
+  const int m = kfield<int32_t>(hv, offsetof(GemvBatchArgs, m) / 4);
+  const int bid = blockIdx.x;
+  int it = 0;
+#pragma unroll
+  for (int i = 1; i < kMaxItems; ++i)
+    it += (i < count && bid >= kfield<int32_t>(hv, offsetof(GemvBatchArgs, wg_begin) / 4 + i)) ? 1 : 0;
+  const int local = bid - kfield<int32_t>(hv, offsetof(GemvBatchArgs, wg_begin) / 4 + it);
+  const uint32_t kv = kargs[(offsetof(GemvBatchArgs, item) / 4) + it * 64 + lane];
+  const int n_tiles = ITEM(int32_t, n_tiles), S = ITEM(int32_t, S);
+  const int tile = local % n_tiles, s = local / n_tiles;
+  const int nblocks = ITEM(int32_t, nblocks), n_chunks = ITEM(int32_t, n_chunks);
+  const Blocks bd{kv, nblocks, n_chunks};
+  // this wave's chunks [c0, c1) and the work-group's [cw0, cw1)
+  int c0 = n_chunks, c1 = n_chunks, cw0 = n_chunks, cw1 = 0;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
-    const int lo = __builtin_amdgcn_readlane(ks, w), hi = __builtin_amdgcn_readlane(ks, w + 1);
-    c0 = (w == wave) ? lo : c0;
-    c1 = (w == wave) ? hi : c1;
+    int lo, hi;
+    wave_range(s * kWaves + w, nblocks, n_chunks, bd, &lo, &hi);
+    if (w == wave) {
+      c0 = lo;
+      c1 = hi;
+    }
+    if (lo < hi) {
+      cw0 = min(cw0, lo);
+      cw1 = max(cw1, hi);
+    }
   }
-  const Blocks bd{kv};
-  const int nblocks = KARG(int32_t, nblocks);
-  const uint8_t* packed = KARG(const uint8_t*, packed);
-  const int32_t* perm = KARG(const int32_t*, perm);
-  const uint16_t* xg = KARG(const uint16_t*, x);
-  const int kdim = KARG(int32_t, k);
+  if (cw1 <= cw0) cw0 = cw1 = 0;
+  const int range = (cw1 - cw0) * kChunk;  // staged channels
+  const int kbase = cw0 * kChunk;
+  const uint8_t* packed = ITEM(const uint8_t*, packed);
+  const int32_t* perm = ITEM(const int32_t*, perm);
+  const uint16_t* xg = ITEM(const uint16_t*, x);
+  const int kdim = ITEM(int32_t, k);
   // ---- Prologue.  Vector loads complete in issue order, so the order of
   // issue below is the order in which the wave can use them: permutation ->
   // activation gathers and group metadata -> the first two weight slots.  The
@@ -481,19 +486,20 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) first += (i < nblocks && bd.ce(i) <= c0) ? 1 : 0;
   const bool has_work = c0 < c1 && first < nblocks;
   const int fb = has_work ? bd.bits(first) : 16, fcb = has_work ? bd.cb(first) : 0;
-  const int fl0 = c0 - fcb, fl1 = has_work ? min(c1, bd.ce(first)) - fcb : 0;
+  const int fl0 = c0 - fcb, fl1 = has_work ? c1 - fcb : 0;
   const int frb = has_work ? bd.rb(first) : 0;
-  const uint8_t* ftile = has_work ? packed + bd.off(first) + tile * bd.tb(first) : packed;
-  // The first block's slice offset, formed before any staging load is issued
-  // (an opaque value the compiler keeps live: rematerialized later, it would
-  // land in a register with a pending load and cost a full wait).
+  const int ftb = has_work ? bd.tb(first) : 0;
+  const uint8_t* ftile = has_work ? packed + bd.off(first) + static_cast<int64_t>(tile) * ftb : packed;
+  // The block's slice offset, formed before any staging load is issued (an
+  // opaque value the compiler keeps live: rematerialized later, it would land
+  // in a register with a pending load and cost a full wait).
   int fvoff;
   asm volatile("v_mul_u32_u24 %0, %1, %2" : "=v"(fvoff) : "v"(lane), "s"(4 * fb));
 
   // LDS: x' rows 0..m-1 and a zero row m (MFMA columns of absent tokens) for
   // the work-group's channels, then each wave's own group metadata.
   uint16_t* xs16 = reinterpret_cast<uint16_t*>(smem);
-  const int wave_groups = KARG(int32_t, wave_groups);
+  const int wave_groups = ITEM(int32_t, wave_groups);
   uint8_t* wmeta = reinterpret_cast<uint8_t*>(smem) + align16((m + 1) * range * 2) +
                    static_cast<size_t>(wave) * wave_groups * kMetaBytes;
 
@@ -547,10 +553,10 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
     const int j = min(u * 64 + lane, max(fpieces - 1, 0));
     mv[u] = ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16);
   }
-  // (4) The first two weight slots of the wave's first block.
+  // (4) The first two weight slots.
   Slot sa, sb;
   if (has_work) {
-    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, bd.tb(first));
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, ftb);
     switch (fb) {
       case 2: preload<2>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
       case 3: preload<3>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
@@ -559,7 +565,6 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
       default: preload<16>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
     }
   }
-  const bool preloaded = has_work;
   // (5) x' of token 0 and the zero row into LDS.
 #pragma unroll
   for (int u = 0; u < kFastRounds; ++u) {
@@ -600,10 +605,10 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
 
   // (7) The wave's own metadata into LDS (the zero points are checked on the
   // way: the fast unpack needs every one to be an integer with |z| <= 1023),
-  // then any groups beyond the first 16 and any further blocks.
+  // then any groups beyond the first 16.
   bool z_ok = true;
-  auto meta_store = [&](uint4* dst, int j, uint4 v) {
-    dst[j] = v;
+  auto meta_store = [&](int j, uint4 v) {
+    reinterpret_cast<uint4*>(wmeta)[j] = v;
     if ((j & 15) < kMetaBytes / 32) {  // a piece of zero points
       const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -616,38 +621,42 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   };
 #pragma unroll
   for (int u = 0; u < 4; ++u)
-    if (u * 64 + lane < fpieces) meta_store(reinterpret_cast<uint4*>(wmeta), u * 64 + lane, mv[u]);
-  {
-    int gslot = 0;
-    for (int bi = first; bi < nblocks; ++bi) {
-      const int cb = bd.cb(bi), ce = bd.ce(bi);
-      const int lo = max(c0, cb), hi = min(c1, ce);
-      if (lo >= hi) break;
-      if (bd.bits(bi) > 8) continue;
-      const int g0 = (lo - cb) >> 2, g1 = ((hi - 1 - cb) >> 2) + 1;
-      const int pieces = (g1 - g0) * (kMetaBytes / 16);
-      const int rb = bd.rb(bi);
-      const uint8_t* rec0 = packed + bd.off(bi) + tile * bd.tb(bi) + static_cast<int64_t>(g0) * rb;
-      uint4* dst = reinterpret_cast<uint4*>(wmeta) + gslot * (kMetaBytes / 16);
-      for (int j = (bi == first ? 4 * 64 : 0) + lane; j < pieces; j += 64)
-        meta_store(dst, j, ldg16(rec0 + (j >> 4) * rb + (j & 15) * 16));
-      gslot += g1 - g0;
-    }
-  }
+    if (u * 64 + lane < fpieces) meta_store(u * 64 + lane, mv[u]);
+  for (int j = 4 * 64 + lane; j < fpieces; j += 64)
+    meta_store(j, ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16));
   const bool exact = __all(z_ok);
 
+  // ---- Main loop over the wave's block range.
   f4 acc[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) acc[r] = f4{0.f, 0.f, 0.f, 0.f};
   const int tok = lane & 15;
-  // this lane's activation row (token lane%16, or the zero row) and channel quarter
-  const uint32_t* xrow = smem + ((tok < m ? tok : m) * range + 8 * (lane >> 4)) / 2;
-  if (exact)
-    run_blocks<true>(bd, first, nblocks, c0, c1, cw0, packed, tile, xrow, wmeta, preloaded, lane,
-                     sa, sb, acc);
-  else
-    run_blocks<false>(bd, first, nblocks, c0, c1, cw0, packed, tile, xrow, wmeta, preloaded, lane,
-                      sa, sb, acc);
+  if (has_work) {
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, ftb);
+    // this lane's activation fragment of block-local chunk 0 (token lane%16,
+    // or the zero row; channel quarter lane/16), relative to the staged range
+    const uint32_t* xlane =
+        smem + ((tok < m ? tok : m) * range + 8 * (lane >> 4)) / 2 + (fcb - cw0) * 16;
+    // metadata of block-local group 0 (only groups >= fl0 / 4 are read)
+    const uint8_t* meta = wmeta - fg0 * kMetaBytes;
+    if (exact) {
+      switch (fb) {
+        case 2: run_segment<2, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        case 3: run_segment<3, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        case 4: run_segment<4, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        case 8: run_segment<8, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        default: run_segment<16, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+      }
+    } else {
+      switch (fb) {
+        case 2: run_segment<2, false>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        case 3: run_segment<3, false>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        case 4: run_segment<4, false>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        case 8: run_segment<8, false>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        default: break;  // 16-bit blocks have no zero points
+      }
+    }
+  }
 
   // Reduce the waves' partial sums (fixed order).  MFMA result layout: lane l
   // holds rows 16r + 4(l/16) + e of token l%16.
@@ -661,13 +670,15 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   }
   __syncthreads();
   if (wave != 0) return;
+  const int n = ITEM(int32_t, n);
+  float* y = ITEM(float*, y);
   const int row = tile * 64 + lane;
-  if (a.S == 1) {
+  if (S == 1) {
     for (int mi = 0; mi < m; ++mi) {
       float v = 0.f;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) v += red[(w * m + mi) * 64 + lane];
-      if (row < a.n) a.y[static_cast<int64_t>(mi) * a.n + row] = v;
+      if (row < n) y[static_cast<int64_t>(mi) * n + row] = v;
     }
     return;
   }
@@ -680,11 +691,14 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   // split order (deterministic), leaves them zero and resets the counter.  (A
   // release/acquire-fence version is both slower -- every fence writes back or
   // invalidates the XCD's whole L2 -- and was measured to read stale partials.)
+  float* partial = ITEM(float*, partial);
+  uint32_t* counter = ITEM(uint32_t*, counter);
+  const int rows_pad = ITEM(int32_t, rows_pad);
   for (int mi = 0; mi < m; ++mi) {
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) v += red[(w * m + mi) * 64 + lane];
-    float* p = &a.partial[(static_cast<int64_t>(s) * m + mi) * a.rows_pad + row];
+    float* p = &partial[(static_cast<int64_t>(s) * m + mi) * rows_pad + row];
     const float old = __hip_atomic_exchange(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     asm volatile("" ::"v"(old));  // keep the returning form of the swap
   }
@@ -693,26 +707,26 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   uint32_t ticket = 0;
   if (lane == 0)
-    ticket = __hip_atomic_fetch_add(&a.counter[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    ticket = __hip_atomic_fetch_add(&counter[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   ticket = __shfl(ticket, 0);
-  if (ticket % static_cast<uint32_t>(a.S) != static_cast<uint32_t>(a.S - 1)) return;
+  if (ticket % static_cast<uint32_t>(S) != static_cast<uint32_t>(S - 1)) return;
   for (int mi = 0; mi < m; ++mi) {
     float v = 0.f;
-    for (int s0 = 0; s0 < a.S; s0 += 8) {  // eight reads in flight at a time
+    for (int s0 = 0; s0 < S; s0 += 8) {  // eight reads in flight at a time
       float t[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        t[u] = s0 + u < a.S
+        t[u] = s0 + u < S
                    ? __hip_atomic_exchange(
-                         &a.partial[(static_cast<int64_t>(s0 + u) * m + mi) * a.rows_pad + row], 0.f,
+                         &partial[(static_cast<int64_t>(s0 + u) * m + mi) * rows_pad + row], 0.f,
                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
                    : 0.f;
 #pragma unroll
       for (int u = 0; u < 8; ++u) v += t[u];
     }
-    if (row < a.n) a.y[static_cast<int64_t>(mi) * a.n + row] = v;
+    if (row < n) y[static_cast<int64_t>(mi) * n + row] = v;
   }
-  if (lane == 0) __hip_atomic_store(&a.counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (lane == 0) __hip_atomic_store(&counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 }  // namespace
@@ -720,58 +734,111 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvArgs a) {
 
 using namespace polyq;
 
+namespace {
+
+// Plans of a batch: every linear's splits are sized for the whole launch.
+polyq_status plan_batch(const polyq_gemv_item* items, int32_t count, int32_t m, GemvPlan* plans,
+                        size_t* ws_offset, size_t* ws_total, size_t* lds) {
+  if (items == nullptr || count < 1) return POLYQ_ERR_ARG;
+  if (count > POLYQ_MAX_BATCH) return POLYQ_ERR_CAPACITY;
+  if (m < 1) return POLYQ_ERR_ARG;
+  if (m > POLYQ_MAX_M_GEMV) return POLYQ_ERR_CAPACITY;
+  int tiles = 0;
+  for (int i = 0; i < count; ++i) {
+    if (!layout_is_valid(items[i].layout)) return POLYQ_ERR_ARG;
+    tiles += items[i].layout->n_tiles;
+  }
+  size_t off = 0, l = 0;
+  for (int i = 0; i < count; ++i) {
+    const polyq_layout& L = *items[i].layout;
+    if (plan_gemv(L, m, tiles, &plans[i]) != 0 || plans[i].W != kWaves) return POLYQ_ERR_CAPACITY;
+    ws_offset[i] = off;
+    off += static_cast<size_t>(align_up(static_cast<int64_t>(gemv_workspace_for(L, m, plans[i])), 256));
+    l = std::max(l, gemv_lds_bytes(plans[i], m));
+  }
+  *ws_total = off;
+  *lds = l;
+  return POLYQ_OK;
+}
+
+}  // namespace
+
+extern "C" size_t polyq_gemv_batch_workspace_bytes(const polyq_gemv_item* items, int32_t count,
+                                                   int32_t m) {
+  GemvPlan plans[POLYQ_MAX_BATCH];
+  size_t offs[POLYQ_MAX_BATCH], total = 0, lds = 0;
+  if (plan_batch(items, count, m, plans, offs, &total, &lds) != POLYQ_OK) return 0;
+  return total;
+}
+
+extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32_t m,
+                                         void* workspace, size_t workspace_bytes, void* stream) {
+  GemvPlan plans[POLYQ_MAX_BATCH];
+  size_t offs[POLYQ_MAX_BATCH], total = 0, lds = 0;
+  const polyq_status st = plan_batch(items, count, m, plans, offs, &total, &lds);
+  if (st != POLYQ_OK) return st;
+  if (total > 0 && (workspace == nullptr || workspace_bytes < total)) return POLYQ_ERR_CAPACITY;
+  if (total > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return POLYQ_ERR_ARG;
+
+  GemvBatchArgs a;
+  memset(&a, 0, sizeof(a));
+  a.count = count;
+  a.m = m;
+  int wgs = 0;
+  for (int i = 0; i < count; ++i) {
+    const polyq_gemv_item& t = items[i];
+    const polyq_layout& L = *t.layout;
+    if (t.packed == nullptr || t.x == nullptr || t.y == nullptr) return POLYQ_ERR_ARG;
+    if (reinterpret_cast<uintptr_t>(t.packed) % 256 != 0) return POLYQ_ERR_ARG;
+    if (reinterpret_cast<uintptr_t>(t.x) % 16 != 0 || reinterpret_cast<uintptr_t>(t.y) % 4 != 0 ||
+        reinterpret_cast<uintptr_t>(t.perm) % 16 != 0)
+      return POLYQ_ERR_ARG;  // activations and permutation are read as 16-byte vectors
+    const GemvPlan& p = plans[i];
+    GemvItem& g = a.item[i];
+    g.packed = static_cast<const uint8_t*>(t.packed);
+    g.perm = t.perm;
+    g.x = t.x;
+    g.y = t.y;
+    g.partial = nullptr;
+    g.counter = nullptr;
+    if (p.S > 1) {  // [counters: n_tiles x u32, 256-aligned][partials: S x m x rows_pad fp32]
+      uint8_t* ws = static_cast<uint8_t*>(workspace) + offs[i];
+      g.counter = reinterpret_cast<uint32_t*>(ws);
+      g.partial = reinterpret_cast<float*>(ws + align_up(static_cast<int64_t>(L.n_tiles) * 4, 256));
+    }
+    g.n = L.n;
+    g.k = L.k;
+    g.nblocks = L.nblocks;
+    g.rows_pad = L.n_tiles * kTileRows;
+    g.S = p.S;
+    g.wave_groups = p.lds_groups;
+    g.n_tiles = L.n_tiles;
+    g.n_chunks = L.n_chunks;
+    int w0 = 0;
+    for (int b = 0; b < POLYQ_MAX_BLOCKS; ++b) {
+      const bool used = b < L.nblocks;
+      g.bits[b] = used ? L.block[b].bits : 0;
+      g.chunk_begin[b] = used ? L.k_begin[b] / kChunk : L.n_chunks;
+      g.wave_begin[b] = w0;
+      g.waves[b] = used ? p.waves[b] : 0;
+      g.magic[b] = div_magic(static_cast<uint32_t>(g.waves[b]));
+      w0 += g.waves[b];
+      g.block_offset[b] = used ? L.block_offset[b] : 0;
+      if (used && L.tile_bytes[b] > INT32_MAX) return POLYQ_ERR_UNSUPPORTED;
+      g.tile_bytes[b] = used ? static_cast<int32_t>(L.tile_bytes[b]) : 0;
+    }
+    a.wg_begin[i] = wgs;
+    wgs += L.n_tiles * p.S;
+  }
+  a.wg_begin[count] = wgs;
+
+  hipLaunchKernelGGL(gemv_kernel, dim3(wgs), dim3(kWaves * 64), lds, static_cast<hipStream_t>(stream), a);
+  return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
+}
+
 extern "C" polyq_status polyq_gemv(const polyq_layout* layout, const void* packed,
                                    const int32_t* perm, const uint16_t* x, int32_t m, float* y,
                                    void* workspace, size_t workspace_bytes, void* stream) {
-  if (!layout_is_valid(layout)) return POLYQ_ERR_ARG;
-  const polyq_layout& L = *layout;
-  if (packed == nullptr || x == nullptr || y == nullptr) return POLYQ_ERR_ARG;
-  if (reinterpret_cast<uintptr_t>(packed) % 256 != 0) return POLYQ_ERR_ARG;
-  if (reinterpret_cast<uintptr_t>(x) % 16 != 0 || reinterpret_cast<uintptr_t>(y) % 4 != 0 ||
-      reinterpret_cast<uintptr_t>(perm) % 16 != 0)
-    return POLYQ_ERR_ARG;  // activations and permutation are read as 16-byte vectors
-  if (m < 1) return POLYQ_ERR_ARG;
-  if (m > POLYQ_MAX_M_GEMV) return POLYQ_ERR_CAPACITY;
-  GemvPlan plan;
-  if (plan_gemv(L, m, &plan) != 0) return POLYQ_ERR_CAPACITY;
-  const size_t need = gemv_workspace_for(L, m, plan);
-  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return POLYQ_ERR_CAPACITY;
-  if (need > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return POLYQ_ERR_ARG;
-
-  GemvArgs a;
-  a.packed = static_cast<const uint8_t*>(packed);
-  a.perm = perm;
-  a.x = x;
-  a.y = y;
-  a.n = L.n;
-  a.k = L.k;
-  a.m = m;
-  a.nblocks = L.nblocks;
-  a.rows_pad = L.n_tiles * kTileRows;
-  a.S = plan.S;
-  a.wave_groups = plan.lds_groups;
-  if (plan.W != kWaves) return POLYQ_ERR_UNSUPPORTED;
-  a.partial = nullptr;
-  a.counter = nullptr;
-  if (need > 0) {  // [counters: n_tiles x u32, 256-aligned][partials: S x m x rows_pad fp32]
-    a.counter = static_cast<uint32_t*>(workspace);
-    a.partial = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
-                                         align_up(static_cast<int64_t>(L.n_tiles) * 4, 256));
-  }
-  for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) {
-    const bool used = i < L.nblocks;
-    a.bits[i] = used ? L.block[i].bits : 0;
-    a.chunk_begin[i] = used ? L.k_begin[i] / kChunk : 0;
-    a.chunk_end[i] = used ? (L.k_begin[i] + L.block[i].len) / kChunk : 0;
-    a.block_offset[i] = used ? L.block_offset[i] : 0;
-    a.tile_bytes[i] = used ? L.tile_bytes[i] : 0;
-    a.record_bytes[i] = used ? L.record_bytes[i] : 0;
-  }
-  for (int i = 0; i <= plan.nsplit; ++i) a.split[i] = plan.split[i];
-  for (int i = plan.nsplit + 1; i <= kMaxSplitEntries; ++i) a.split[i] = plan.split[plan.nsplit];
-
-  const dim3 grid(L.n_tiles, plan.S), block(kWaves * 64);
-  const size_t lds = gemv_lds_bytes(plan, m);
-  hipLaunchKernelGGL(gemv_kernel, grid, block, lds, static_cast<hipStream_t>(stream), a);
-  return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
+  const polyq_gemv_item item{layout, packed, perm, x, y};
+  return polyq_gemv_batch(&item, 1, m, workspace, workspace_bytes, stream);
 }

@@ -2,6 +2,7 @@
 // mixed-bit linear-layer library.  Not part of the public ABI (include/polyq.h).
 #pragma once
 
+#include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "polyq.h"
@@ -14,22 +15,63 @@ constexpr int kGroup = POLYQ_GROUP;         // channels per quantization group
 constexpr int kChunksPerGroup = kGroup / kChunk;
 constexpr int kMetaBytes = kTileRows * 4;   // {fp16 s, fp16 z} per row of a tile
 
-// Decode GEMV launch plan: WGs = n_tiles x S, each of W waves; wave w of split
-// s processes the global chunk range [split[s*W + w], split[s*W + w + 1]).
+// Decode GEMV launch plan: the work-groups of one linear are n_tiles x S, each
+// of W waves; wave w (0 <= w < S * W, across the tile's splits) covers the
+// chunk range wave_range(w).  Every wave stays inside one block: block i gets
+// waves[i] waves per tile.
 constexpr int kMaxSplitEntries = 256;  // S * W <= this
 
 struct GemvPlan {
-  int32_t S;                    // WG splits per 64-row tile
-  int32_t W;                    // waves per WG
-  int32_t lds_chunks;           // largest chunk range of one WG
-  int32_t lds_groups;           // most group records one wave stages (b <= 8 blocks)
-  int32_t nsplit;               // S * W
-  int32_t split[kMaxSplitEntries + 1];
+  int32_t S;                        // WG splits per 64-row tile
+  int32_t W;                        // waves per WG
+  int32_t waves[POLYQ_MAX_BLOCKS];  // waves per tile given to each block
+  int32_t lds_chunks;               // largest chunk range of one WG
+  int32_t lds_groups;               // most group records one wave stages (b <= 8 blocks)
 };
 
-// Returns 0 on success.  Chooses S and W for `m` tokens and partitions the
-// layer's chunks by bytes.
-int plan_gemv(const polyq_layout& L, int32_t m, GemvPlan* p);
+// ceil(2^32 / d) for 2 <= d, or 0 for d == 1: floor(a / d) == mul_hi(a, M) for
+// every a < 2^24 (the rounding error a * (M d - 2^32) / (d 2^32) < 1/d never
+// crosses an integer).
+__host__ __device__ inline uint32_t div_magic(uint32_t d) {
+  return d <= 1 ? 0u : static_cast<uint32_t>((0x100000000ull + d - 1) / d);
+}
+__host__ __device__ inline uint32_t div_by_magic(uint32_t a, uint32_t magic) {
+  return magic == 0 ? a : static_cast<uint32_t>((static_cast<uint64_t>(a) * magic) >> 32);
+}
+
+// Chunk range [lo, hi) of wave w of every tile: waves are handed to the blocks
+// in order (waves[i] to block i, starting at wave w0[i]) and a block's groups
+// are split evenly among its waves, so that every wave starts and ends on a
+// group boundary of one block.  Waves past the last block get an empty range
+// at the end of the layer.  blk(i, &cb, &ce, &w0, &nw, &magic) gives block i's
+// chunk range, first wave, wave count and div_magic(wave count); the loop is
+// unrolled so that i is a compile-time constant.  Shared by the host planner
+// and the kernel, which must agree exactly.
+template <class Blk>
+__host__ __device__ inline void wave_range(int w, int nblocks, int n_chunks, const Blk& blk,
+                                           int* lo, int* hi) {
+  int l = n_chunks, h = n_chunks;
+#pragma unroll
+  for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) {
+    int cb = 0, ce = 0, w0 = 0, nw = 0;
+    uint32_t magic = 0;
+    blk(i, &cb, &ce, &w0, &nw, &magic);
+    if (i < nblocks && w >= w0 && w < w0 + nw) {
+      const int nch = ce - cb, ngr = (nch + kChunksPerGroup - 1) / kChunksPerGroup, j = w - w0;
+      const int a = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * j), magic));
+      const int b = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * (j + 1)), magic));
+      l = cb + (a < nch ? a : nch);
+      h = cb + (b < nch ? b : nch);
+    }
+  }
+  *lo = l;
+  *hi = h;
+}
+
+// Returns 0 on success.  Chooses S, W and the waves per block for `m` tokens;
+// `launch_tiles` is the number of 64-row tiles of every linear that shares the
+// launch (the splits are sized so that the launch fills the GPU about once).
+int plan_gemv(const polyq_layout& L, int32_t m, int32_t launch_tiles, GemvPlan* p);
 
 // Bytes of GEMV workspace needed for plan p (0 when S == 1): one uint32 counter
 // per tile (padded to 256 B) followed by the partials [S][m][n_tiles*64] fp32.
@@ -40,6 +82,22 @@ bool layout_is_valid(const polyq_layout* L);
 
 // LDS bytes of a GEMV work-group for plan p and m tokens.
 size_t gemv_lds_bytes(const GemvPlan& p, int32_t m);
+
+// Block accessor of a layout for wave_range (host side).
+struct LayoutBlocks {
+  const polyq_layout* L;
+  const int32_t* waves;
+  void operator()(int i, int* cb, int* ce, int* w0, int* nw, uint32_t* magic) const {
+    if (i >= L->nblocks) return;
+    *cb = L->k_begin[i] / kChunk;
+    *ce = (L->k_begin[i] + L->block[i].len) / kChunk;
+    int first = 0;
+    for (int j = 0; j < i; ++j) first += waves[j];
+    *w0 = first;
+    *nw = waves[i];
+    *magic = div_magic(static_cast<uint32_t>(waves[i]));
+  }
+};
 
 inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 

@@ -115,55 +115,22 @@ static int groups_touched(const polyq_layout& L, int lo, int hi) {
   return n;
 }
 
-// The group boundary (block-relative multiple of 4 chunks, or the block end)
-// nearest to chunk c.  GEMV waves start and end on these, so that every group
-// record is processed whole by one wave.
-static int snap_to_group(const polyq_layout& L, int c) {
-  for (int i = 0; i < L.nblocks; ++i) {
-    const int b0 = L.k_begin[i] / kChunk, b1 = b0 + L.block[i].len / kChunk;
-    if (c < b0 || c >= b1) continue;
-    const int down = b0 + (c - b0) / kChunksPerGroup * kChunksPerGroup;
-    const int up = std::min(b1, down + kChunksPerGroup);
-    return (c - down <= up - c) ? down : up;
-  }
-  return c;
-}
-
-static void partition(const polyq_layout& L, const std::vector<int64_t>& prefix, int parts,
-                      int32_t* split) {
-  const int C = static_cast<int>(prefix.size()) - 1;
-  const int64_t total = prefix[C];
-  split[0] = 0;
-  int c = 0;
-  for (int j = 1; j < parts; ++j) {
-    const int64_t goal = (total * j + parts / 2) / parts;
-    while (c < C && prefix[c] < goal) ++c;
-    // pick the nearer of c-1 and c
-    int best = c;
-    if (c > 0 && goal - prefix[c - 1] < prefix[c] - goal) best = c - 1;
-    best = std::max(snap_to_group(L, best), static_cast<int>(split[j - 1]));
-    split[j] = best;
-  }
-  split[parts] = C;
-}
-
 // Cost of one 32-channel chunk of a 64-row tile, in units of 64 bytes (codes +
 // the chunk's share of its group's 256-byte metadata).
 static int64_t chunk_cost(int bits) { return 4 * bits + (bits <= 8 ? 1 : 0); }
 
-// `parts` waves per tile with every wave inside one block: waves are given to
-// blocks in proportion to their bytes (at least one each, at most one per
-// group) and each block's groups are split evenly among its waves.  Returns
-// false when there are fewer waves than blocks.
-static bool partition_by_block(const polyq_layout& L, int parts, int32_t* split) {
+// `parts` (>= nblocks) waves per tile, every wave inside one block: waves are
+// given to blocks in proportion to their bytes (at least one each, at most one
+// per group); wave_range then splits each block's groups evenly among its
+// waves.  Waves left over when every block has one wave per group stay idle.
+static void waves_per_block(const polyq_layout& L, int parts, int32_t* n) {
   const int nb = L.nblocks;
-  if (parts < nb) return false;
   int64_t cost[POLYQ_MAX_BLOCKS], total = 0;
-  int nch[POLYQ_MAX_BLOCKS], ngr[POLYQ_MAX_BLOCKS], n[POLYQ_MAX_BLOCKS], used = 0;
+  int ngr[POLYQ_MAX_BLOCKS], used = 0;
   for (int i = 0; i < nb; ++i) {
-    nch[i] = L.block[i].len / kChunk;
-    ngr[i] = (nch[i] + kChunksPerGroup - 1) / kChunksPerGroup;
-    cost[i] = nch[i] * chunk_cost(L.block[i].bits);
+    const int nch = L.block[i].len / kChunk;
+    ngr[i] = (nch + kChunksPerGroup - 1) / kChunksPerGroup;
+    cost[i] = nch * chunk_cost(L.block[i].bits);
     total += cost[i];
   }
   for (int i = 0; i < nb; ++i) {
@@ -185,42 +152,36 @@ static bool partition_by_block(const polyq_layout& L, int parts, int32_t* split)
     --n[best];
     --used;
   }
-  int u = 0;
-  split[0] = 0;
-  for (int i = 0; i < nb; ++i) {
-    const int c0 = L.k_begin[i] / kChunk;
-    for (int j = 0; j < n[i]; ++j) {
-      const int g = static_cast<int>(static_cast<int64_t>(ngr[i]) * (j + 1) / n[i]);
-      split[++u] = c0 + std::min(nch[i], g * kChunksPerGroup);
-    }
-  }
-  for (; u < parts; ++u) split[u + 1] = L.n_chunks;  // waves left without work
-  return true;
+  for (int i = nb; i < POLYQ_MAX_BLOCKS; ++i) n[i] = 0;
 }
 
-int plan_gemv(const polyq_layout& L, int32_t m, GemvPlan* p) {
-  const int C = L.n_chunks, T = L.n_tiles;
-  std::vector<int64_t> prefix(C + 1, 0);
-  for (int i = 0; i < L.nblocks; ++i) {
-    const int b = L.block[i].bits;
-    const int c0 = L.k_begin[i] / kChunk, nc = L.block[i].len / kChunk;
-    for (int c = 0; c < nc; ++c) prefix[c0 + c + 1] = prefix[c0 + c] + chunk_cost(b);
-  }
-  const int W = kWavesPerWG;
-  // One round of co-resident work-groups: splits beyond that only add a second
-  // round of prologue and fix-up latency.
-  int S = std::max(1, kResidentWGs / T);
+int plan_gemv(const polyq_layout& L, int32_t m, int32_t launch_tiles, GemvPlan* p) {
+  const int C = L.n_chunks, W = kWavesPerWG;
+  // One round of co-resident work-groups per launch: splits beyond that only
+  // add prologue and fix-up latency.  Every block needs a wave of its own.
+  int S = std::max(1, kResidentWGs / std::max(1, launch_tiles));
   S = std::min(S, std::max(1, C / (W * kMinChunksPerWave)));
+  S = std::max(S, (L.nblocks + W - 1) / W);
   S = std::max(1, std::min(S, kMaxSplitEntries / W));
   for (;;) {
     p->S = S;
     p->W = W;
-    p->nsplit = S * W;
-    if (!partition_by_block(L, S * W, p->split)) partition(L, prefix, S * W, p->split);
+    waves_per_block(L, S * W, p->waves);
+    const LayoutBlocks blk{&L, p->waves};
     int worst = 0, worst_groups = 0;
-    for (int s = 0; s < S; ++s) worst = std::max(worst, p->split[(s + 1) * W] - p->split[s * W]);
-    for (int w = 0; w < S * W; ++w)
-      worst_groups = std::max(worst_groups, groups_touched(L, p->split[w], p->split[w + 1]));
+    for (int s = 0; s < S; ++s) {
+      int lo = C, hi = 0;
+      for (int w = 0; w < W; ++w) {
+        int a, b;
+        wave_range(s * W + w, L.nblocks, C, blk, &a, &b);
+        if (a < b) {
+          lo = std::min(lo, a);
+          hi = std::max(hi, b);
+          worst_groups = std::max(worst_groups, groups_touched(L, a, b));
+        }
+      }
+      if (lo < hi) worst = std::max(worst, hi - lo);
+    }
     p->lds_chunks = worst;
     p->lds_groups = worst_groups;
     if (gemv_lds_bytes(*p, m) <= kLdsBudget) return 0;
@@ -240,6 +201,6 @@ size_t gemv_workspace_for(const polyq_layout& L, int32_t m, const GemvPlan& p) {
 extern "C" size_t polyq_gemv_workspace_bytes(const polyq_layout* layout, int32_t m) {
   if (!polyq::layout_is_valid(layout) || m < 1 || m > POLYQ_MAX_M_GEMV) return 0;
   polyq::GemvPlan p;
-  if (polyq::plan_gemv(*layout, m, &p) != 0) return 0;
+  if (polyq::plan_gemv(*layout, m, layout->n_tiles, &p) != 0) return 0;
   return polyq::gemv_workspace_for(*layout, m, p);
 }

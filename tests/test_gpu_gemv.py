@@ -195,3 +195,70 @@ def test_gemv_capacity_errors():
     pl = packed_linear(lin)
     with pytest.raises(pq.PolyQError):
         pl.decode(torch.zeros((17, 64), dtype=torch.float16, device=dev()))
+
+
+# ----------------------------------------------------------------------- batches
+def test_gemv_batch_llama_qkv_and_gate_up():
+    """One launch per shared-input group of the Llama2-13B layer (q/k/v, gate/up):
+    every output against the oracle on sampled rows, and the batch is
+    deterministic."""
+    lins, groups = make_layer(1, device=dev(), only=("q_proj", "k_proj", "v_proj", "gate_proj",
+                                                     "up_proj"))
+    rows = np.random.default_rng(11).choice(5120, 192, replace=False)
+    for names in (("q_proj", "k_proj", "v_proj"), ("gate_proj", "up_proj")):
+        sel = [l for l in lins if l.name in names]
+        pls = [packed_linear(l) for l in sel]
+        x = groups[sel[0].group].x.to(dev())
+        ys = pq.decode_batch(pls, [x] * len(pls))
+        ys2 = pq.decode_batch(pls, [x] * len(pls))
+        torch.cuda.synchronize()
+        for lin, y, y2 in zip(sel, ys, ys2):
+            assert torch.equal(y, y2), lin.name
+            y_ref, bound = oracle_ref(lin, groups[lin.group].x, rows=rows)
+            assert_parity(y[:, rows], y_ref, bound, f"batch {lin.name}")
+
+
+@pytest.mark.parametrize("m", [1, 4])
+def test_gemv_batch_mixed_items(m):
+    """Items of different shapes and block lists, one pre-permuted, two sharing
+    x; each output equals the oracle, and a batch of one equals polyq_gemv."""
+    specs = [(100, [(2, 160), (3, 96), (4, 128), (8, 96), (16, 32)]),
+             (640, [(2, 2400), (3, 1728), (4, 768), (8, 160), (16, 64)]),
+             (37, [(4, 480), (16, 96)]),
+             (257, [(2, 2400), (3, 1728), (4, 768), (8, 160), (16, 64)])]
+    lins = [random_quant_linear(n, sum(l for _, l in b), b, seed=70 + i, mode="codes")
+            for i, (n, b) in enumerate(specs)]
+    lins[3].perm = lins[1].perm  # items 1 and 3 share x and the permutation
+    pls = [packed_linear(l) for l in lins]
+    xs = [_x(m, l.k, seed=80 + i) for i, l in enumerate(lins)]
+    xs[3] = xs[1]
+    xd = [x.to(dev()) for x in xs]
+    xd[3] = xd[1]
+    xd[2] = pls[2].permute(xd[2])  # item 2 pre-permuted
+    items = [(pl.layout, pl.packed, None if i == 2 else pl.perm, x, None)
+             for i, (pl, x) in enumerate(zip(pls, xd))]
+    ys = pq.gemv_batch(items)
+    torch.cuda.synchronize()
+    for i, (lin, x, y) in enumerate(zip(lins, xs, ys)):
+        y_ref, bound = oracle_ref(lin, x)
+        assert_parity(y, y_ref, bound, f"mixed batch item {i}")
+    y1 = pq.gemv_batch(items[:1])[0]
+    assert torch.equal(y1, pls[0].decode(xd[0]))
+
+
+def test_gemv_batch_rejects_bad_requests():
+    lin = random_quant_linear(64, 256, [(2, 128), (4, 128)], seed=3)
+    pl = packed_linear(lin)
+    x = _x(1, 256, 1).to(dev())
+    item = (pl.layout, pl.packed, pl.perm, x, None)
+    with pytest.raises(ValueError):
+        pq.gemv_batch([])
+    with pytest.raises(ValueError):
+        pq.gemv_batch([item] * 9)
+    with pytest.raises(ValueError):
+        pq.gemv_batch([item, (pl.layout, pl.packed, pl.perm, _x(2, 256, 2).to(dev()), None)])
+    lib = pq.lib()
+    arr = (pq._lib.GemvItem * 9)()
+    assert lib.polyq_gemv_batch(arr, 9, 1, None, 0, None) == 5   # POLYQ_ERR_CAPACITY
+    assert lib.polyq_gemv_batch(arr, 0, 1, None, 0, None) == 1   # POLYQ_ERR_ARG
+    assert lib.polyq_gemv_batch_workspace_bytes(arr, 0, 1) == 0
