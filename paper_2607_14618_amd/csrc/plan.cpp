@@ -13,7 +13,7 @@ bool bits_in_palette(int b) { return b == 2 || b == 3 || b == 4 || b == 8 || b =
 
 // GEMV work split knobs.
 constexpr int kWavesPerWG = 4;
-constexpr int kResidentWGs = 512;        // 256 CUs x 2 co-resident 4-wave work-groups
+constexpr int kResidentWGs = 768;        // 256 CUs x 3 co-resident 4-wave work-groups (<= 168 VGPRs)
 constexpr int kMinChunksPerWave = 4;      // below this the per-wave setup dominates
 constexpr size_t kLdsBudget = 64 * 1024;  // per work-group
 
