@@ -50,23 +50,23 @@ struct GemvItem {
   float* y;
   float* partial;     // [S][m][rows_pad], only when S > 1
   uint32_t* counter;  // [n_tiles], only when S > 1
-  int32_t n, k, nblocks, rows_pad, S, wave_groups, n_tiles, n_chunks;
+  int32_t n, k, m, nblocks, rows_pad, S;
+  int32_t wave_lds;       // LDS bytes of one wave's staging region
+  int32_t n_tiles, n_chunks;
+  uint32_t tiles_magic;   // div_magic(n_tiles)
+  int32_t pad0;
   int32_t bits[POLYQ_MAX_BLOCKS];
   int32_t chunk_begin[POLYQ_MAX_BLOCKS];
   int32_t wave_begin[POLYQ_MAX_BLOCKS];  // first wave (per tile) of each block
   int32_t waves[POLYQ_MAX_BLOCKS];       // waves per tile given to each block
   uint32_t magic[POLYQ_MAX_BLOCKS];      // div_magic(waves)
   int32_t tile_bytes[POLYQ_MAX_BLOCKS];
+  int32_t pad1;
   int64_t block_offset[POLYQ_MAX_BLOCKS];
-  int32_t pad[4];
 };
 
-// The launch: a 64-dword header (work-groups [wg_begin[i], wg_begin[i+1]) run
-// linear i), then the linears.
+// The launch: work-group (x, y) runs linear y; x = s * n_tiles + tile.
 struct GemvBatchArgs {
-  int32_t count, m;
-  int32_t wg_begin[kMaxItems + 1];
-  int32_t pad[64 - 2 - (kMaxItems + 1)];
   GemvItem item[kMaxItems];
 };
 
@@ -406,13 +406,9 @@ struct Blocks {
     const int b = bits(i);
     return (b <= 8 ? kMetaBytes : 0) + kChunksPerGroup * 64 * 4 * b;
   }
-  __device__ void operator()(int i, int* c0, int* c1, int* w0, int* nw, uint32_t* mg) const {
-    *c0 = cb(i);
-    *c1 = ce(i);
-    *w0 = kfield<int32_t>(kv, offsetof(GemvItem, wave_begin) / 4 + i);
-    *nw = kfield<int32_t>(kv, offsetof(GemvItem, waves) / 4 + i);
-    *mg = kfield<uint32_t>(kv, offsetof(GemvItem, magic) / 4 + i);
-  }
+  __device__ int w0(int i) const { return kfield<int32_t>(kv, offsetof(GemvItem, wave_begin) / 4 + i); }
+  __device__ int nw(int i) const { return kfield<int32_t>(kv, offsetof(GemvItem, waves) / 4 + i); }
+  __device__ uint32_t magic(int i) const { return kfield<uint32_t>(kv, offsetof(GemvItem, magic) / 4 + i); }
 };
 
 __device__ __forceinline__ size_t align16(size_t v) { return (v + 15) & ~static_cast<size_t>(15); }
@@ -435,43 +431,22 @@ __device__ __forceinline__ uint4 ldg16(const void* p) {
 __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a) {
   extern __shared__ uint32_t smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-  // The argument block is read with vector loads (one dword per lane: the
-  // batch header, then this work-group's linear) and broadcast with
-  // v_readlane; scalar loads of it would miss the scalar cache line by line.
+  // The work-group's linear (blockIdx.y) is read with one vector load (a dword
+  // per lane) and broadcast with v_readlane; scalar loads of it would miss the
+  // scalar cache line by line.
   const uint32_t* kargs = (const uint32_t*)(__builtin_amdgcn_kernarg_segment_ptr());
-  static_assert(sizeof(GemvItem) == 256 && offsetof(GemvBatchArgs, item) == 256, "argument layout");
-  const uint32_t hv = kargs[lane];
-  const int count = kfield<int32_t>(hv, offsetof(GemvBatchArgs, count) / 4);
-  const int m = kfield<int32_t>(hv, offsetof(GemvBatchArgs, m) / 4);
-  const int bid = blockIdx.x;
-  int it = 0;
-#pragma unroll
-  for (int i = 1; i < kMaxItems; ++i)
-    it += (i < count && bid >= kfield<int32_t>(hv, offsetof(GemvBatchArgs, wg_begin) / 4 + i)) ? 1 : 0;
-  const int local = bid - kfield<int32_t>(hv, offsetof(GemvBatchArgs, wg_begin) / 4 + it);
-  const uint32_t kv = kargs[(offsetof(GemvBatchArgs, item) / 4) + it * 64 + lane];
+  static_assert(sizeof(GemvItem) == 256 && offsetof(GemvBatchArgs, item) == 0, "argument layout");
+  const uint32_t kv = kargs[blockIdx.y * 64 + lane];
   const int n_tiles = ITEM(int32_t, n_tiles), S = ITEM(int32_t, S);
-  const int tile = local % n_tiles, s = local / n_tiles;
-  const int nblocks = ITEM(int32_t, nblocks), n_chunks = ITEM(int32_t, n_chunks);
+  const int local = blockIdx.x;
+  const int s = static_cast<int>(div_by_magic(static_cast<uint32_t>(local), ITEM(uint32_t, tiles_magic)));
+  if (s >= S) return;  // this linear has fewer work-groups than the launch's widest
+  const int tile = local - s * n_tiles;
+  const int m = ITEM(int32_t, m), nblocks = ITEM(int32_t, nblocks), n_chunks = ITEM(int32_t, n_chunks);
   const Blocks bd{kv, nblocks, n_chunks};
-  // this wave's chunks [c0, c1) and the work-group's [cw0, cw1)
-  int c0 = n_chunks, c1 = n_chunks, cw0 = n_chunks, cw1 = 0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    int lo, hi;
-    wave_range(s * kWaves + w, nblocks, n_chunks, bd, &lo, &hi);
-    if (w == wave) {
-      c0 = lo;
-      c1 = hi;
-    }
-    if (lo < hi) {
-      cw0 = min(cw0, lo);
-      cw1 = max(cw1, hi);
-    }
-  }
-  if (cw1 <= cw0) cw0 = cw1 = 0;
-  const int range = (cw1 - cw0) * kChunk;  // staged channels
-  const int kbase = cw0 * kChunk;
+  // this wave's chunks [c0, c1): one block's share (wave_range)
+  int c0, c1;
+  wave_range(s * kWaves + wave, nblocks, n_chunks, bd, &c0, &c1);
   const uint8_t* packed = ITEM(const uint8_t*, packed);
   const int32_t* perm = ITEM(const int32_t*, perm);
   const uint16_t* xg = ITEM(const uint16_t*, x);
@@ -479,8 +454,10 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   // ---- Prologue.  Vector loads complete in issue order, so the order of
   // issue below is the order in which the wave can use them: permutation ->
   // activation gathers and group metadata -> the first two weight slots.  The
-  // gathers are waited for (x' into LDS, barrier) while the weight slots are
-  // still in flight.
+  // gathers are waited for (x' into LDS) while the weight slots are still in
+  // flight.  Each wave stages only its own channels: the waves of a
+  // work-group share no x', so no work-group barrier is needed before the
+  // main loop.
   int first = 0;
 #pragma unroll
   for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) first += (i < nblocks && bd.ce(i) <= c0) ? 1 : 0;
@@ -496,19 +473,20 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   int fvoff;
   asm volatile("v_mul_u32_u24 %0, %1, %2" : "=v"(fvoff) : "v"(lane), "s"(4 * fb));
 
-  // LDS: x' rows 0..m-1 and a zero row m (MFMA columns of absent tokens) for
-  // the work-group's channels, then each wave's own group metadata.
-  uint16_t* xs16 = reinterpret_cast<uint16_t*>(smem);
-  const int wave_groups = ITEM(int32_t, wave_groups);
-  uint8_t* wmeta = reinterpret_cast<uint8_t*>(smem) + align16((m + 1) * range * 2) +
-                   static_cast<size_t>(wave) * wave_groups * kMetaBytes;
+  // LDS of this wave: x' rows 0..m-1 and a zero row m (MFMA columns of absent
+  // tokens) for its channels, then its group metadata.
+  const int range = has_work ? (c1 - c0) * kChunk : 0;
+  const int kbase = c0 * kChunk;
+  uint16_t* xs16 = reinterpret_cast<uint16_t*>(reinterpret_cast<uint8_t*>(smem) +
+                                               static_cast<size_t>(wave) * ITEM(int32_t, wave_lds));
+  uint8_t* wmeta = reinterpret_cast<uint8_t*>(xs16) + align16((m + 1) * range * 2);
 
-  // (1) Permutation of this thread's channels: 8 consecutive channels in each
-  // of kFastRounds rounds of 2048.  The code is branch-free so that every load
-  // is issued before the first use: indices are clamped, results masked, and
-  // without a permutation the (ignored) index loads read the packed buffer,
-  // which always holds more than 4k bytes.
-  constexpr int kRound = kWaves * 64 * 8;
+  // (1) Permutation of this wave's channels: 8 consecutive channels per lane
+  // in each of kFastRounds rounds of 512.  The code is branch-free so that every
+  // load is issued before the first use: indices are clamped, results masked,
+  // and without a permutation the (ignored) index loads read the packed
+  // buffer, which always holds more than 4k bytes.
+  constexpr int kRound = 64 * 8;
   constexpr int kFastRounds = 4;
   const int fast_end = min(range, kFastRounds * kRound);
   const bool use_perm = perm != nullptr;
@@ -516,7 +494,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   int src[kFastRounds][8];
 #pragma unroll
   for (int u = 0; u < kFastRounds; ++u) {
-    const int kk = u * kRound + static_cast<int>(threadIdx.x) * 8;
+    const int kk = u * kRound + lane * 8;
     const bool has = kk < fast_end;
     const int kp0 = kbase + (has ? kk : 0);
     const uint4 p0 = ldg16(pbase + kp0), p1 = ldg16(pbase + kp0 + 4);
@@ -568,7 +546,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   // (5) x' of token 0 and the zero row into LDS.
 #pragma unroll
   for (int u = 0; u < kFastRounds; ++u) {
-    const int kk = u * kRound + static_cast<int>(threadIdx.x) * 8;
+    const int kk = u * kRound + lane * 8;
     if (kk < fast_end) {
       *reinterpret_cast<uint4*>(xs16 + kk) = uint4{q[u][0], q[u][1], q[u][2], q[u][3]};
       *reinterpret_cast<uint4*>(xs16 + m * range + kk) = uint4{0u, 0u, 0u, 0u};
@@ -577,7 +555,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   // (6) Rare: more tokens, or channels past the fast rounds (these loads wait
   // behind the weight slots).
   auto stage_slow = [&](int k_lo, int k_hi, int t_lo, bool zero_row) {
-    for (int kk = k_lo + static_cast<int>(threadIdx.x) * 8; kk < k_hi; kk += kRound) {
+    for (int kk = k_lo + lane * 8; kk < k_hi; kk += kRound) {
       int sr[8];
       const uint4 p0 = ldg16(pbase + kbase + kk), p1 = ldg16(pbase + kbase + kk + 4);
       const int pv[8] = {static_cast<int>(p0.x), static_cast<int>(p0.y), static_cast<int>(p0.z),
@@ -601,11 +579,10 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   };
   if (m > 1) stage_slow(0, fast_end, 1, false);
   if (range > fast_end) stage_slow(fast_end, range, 0, true);
-  __syncthreads();
 
-  // (7) The wave's own metadata into LDS (the zero points are checked on the
-  // way: the fast unpack needs every one to be an integer with |z| <= 1023),
-  // then any groups beyond the first 16.
+  // (7) The wave's metadata into LDS (the zero points are checked on the way:
+  // the fast unpack needs every one to be an integer with |z| <= 1023), then
+  // any groups beyond the first 16.
   bool z_ok = true;
   auto meta_store = [&](int j, uint4 v) {
     reinterpret_cast<uint4*>(wmeta)[j] = v;
@@ -635,8 +612,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, ftb);
     // this lane's activation fragment of block-local chunk 0 (token lane%16,
     // or the zero row; channel quarter lane/16), relative to the staged range
-    const uint32_t* xlane =
-        smem + ((tok < m ? tok : m) * range + 8 * (lane >> 4)) / 2 + (fcb - cw0) * 16;
+    const uint32_t* xlane = reinterpret_cast<const uint32_t*>(xs16) +
+                            ((tok < m ? tok : m) * range + 8 * (lane >> 4)) / 2 + (fcb - c0) * 16;
     // metadata of block-local group 0 (only groups >= fl0 / 4 are read)
     const uint8_t* meta = wmeta - fg0 * kMetaBytes;
     if (exact) {
@@ -782,8 +759,6 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
 
   GemvBatchArgs a;
   memset(&a, 0, sizeof(a));
-  a.count = count;
-  a.m = m;
   int wgs = 0;
   for (int i = 0; i < count; ++i) {
     const polyq_gemv_item& t = items[i];
@@ -808,12 +783,14 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
     }
     g.n = L.n;
     g.k = L.k;
+    g.m = m;
     g.nblocks = L.nblocks;
     g.rows_pad = L.n_tiles * kTileRows;
     g.S = p.S;
-    g.wave_groups = p.lds_groups;
+    g.wave_lds = static_cast<int32_t>(gemv_wave_lds_bytes(p, m));
     g.n_tiles = L.n_tiles;
     g.n_chunks = L.n_chunks;
+    g.tiles_magic = div_magic(static_cast<uint32_t>(L.n_tiles));
     int w0 = 0;
     for (int b = 0; b < POLYQ_MAX_BLOCKS; ++b) {
       const bool used = b < L.nblocks;
@@ -827,12 +804,11 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
       if (used && L.tile_bytes[b] > INT32_MAX) return POLYQ_ERR_UNSUPPORTED;
       g.tile_bytes[b] = used ? static_cast<int32_t>(L.tile_bytes[b]) : 0;
     }
-    a.wg_begin[i] = wgs;
-    wgs += L.n_tiles * p.S;
+    wgs = std::max(wgs, L.n_tiles * p.S);
   }
-  a.wg_begin[count] = wgs;
 
-  hipLaunchKernelGGL(gemv_kernel, dim3(wgs), dim3(kWaves * 64), lds, static_cast<hipStream_t>(stream), a);
+  hipLaunchKernelGGL(gemv_kernel, dim3(wgs, count), dim3(kWaves * 64), lds,
+                     static_cast<hipStream_t>(stream), a);
   return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
 }
 

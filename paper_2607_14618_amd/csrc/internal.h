@@ -25,7 +25,7 @@ struct GemvPlan {
   int32_t S;                        // WG splits per 64-row tile
   int32_t W;                        // waves per WG
   int32_t waves[POLYQ_MAX_BLOCKS];  // waves per tile given to each block
-  int32_t lds_chunks;               // largest chunk range of one WG
+  int32_t lds_chunks;               // largest chunk range of one wave
   int32_t lds_groups;               // most group records one wave stages (b <= 8 blocks)
 };
 
@@ -43,29 +43,29 @@ __host__ __device__ inline uint32_t div_by_magic(uint32_t a, uint32_t magic) {
 // in order (waves[i] to block i, starting at wave w0[i]) and a block's groups
 // are split evenly among its waves, so that every wave starts and ends on a
 // group boundary of one block.  Waves past the last block get an empty range
-// at the end of the layer.  blk(i, &cb, &ce, &w0, &nw, &magic) gives block i's
-// chunk range, first wave, wave count and div_magic(wave count); the loop is
-// unrolled so that i is a compile-time constant.  Shared by the host planner
-// and the kernel, which must agree exactly.
+// at the end of the layer.  `blk` gives, for block i (a uniform run-time
+// index), cb(i) / ce(i) (chunk range), w0(i), nw(i) and magic(i) =
+// div_magic(nw(i)).  Shared by the host planner and the kernel, which must
+// agree exactly; the kernel evaluates it in scalar registers, so the block is
+// found with a handful of compares and read once.
 template <class Blk>
 __host__ __device__ inline void wave_range(int w, int nblocks, int n_chunks, const Blk& blk,
                                            int* lo, int* hi) {
-  int l = n_chunks, h = n_chunks;
+  int i = -1;
 #pragma unroll
-  for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) {
-    int cb = 0, ce = 0, w0 = 0, nw = 0;
-    uint32_t magic = 0;
-    blk(i, &cb, &ce, &w0, &nw, &magic);
-    if (i < nblocks && w >= w0 && w < w0 + nw) {
-      const int nch = ce - cb, ngr = (nch + kChunksPerGroup - 1) / kChunksPerGroup, j = w - w0;
-      const int a = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * j), magic));
-      const int b = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * (j + 1)), magic));
-      l = cb + (a < nch ? a : nch);
-      h = cb + (b < nch ? b : nch);
-    }
-  }
-  *lo = l;
-  *hi = h;
+  for (int b = 0; b < POLYQ_MAX_BLOCKS; ++b)
+    if (b < nblocks && blk.w0(b) <= w) i = b;
+  *lo = *hi = n_chunks;
+  if (i < 0) return;
+  const int w0 = blk.w0(i), nw = blk.nw(i);
+  if (w >= w0 + nw) return;
+  const int cb = blk.cb(i), nch = blk.ce(i) - cb;
+  const int ngr = (nch + kChunksPerGroup - 1) / kChunksPerGroup, j = w - w0;
+  const uint32_t magic = blk.magic(i);
+  const int a = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * j), magic));
+  const int b = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * (j + 1)), magic));
+  *lo = cb + (a < nch ? a : nch);
+  *hi = cb + (b < nch ? b : nch);
 }
 
 // Returns 0 on success.  Chooses S, W and the waves per block for `m` tokens;
@@ -80,23 +80,24 @@ size_t gemv_workspace_for(const polyq_layout& L, int32_t m, const GemvPlan& p);
 // True when `L` is exactly what polyq_plan produces for its own n, k, blocks.
 bool layout_is_valid(const polyq_layout* L);
 
-// LDS bytes of a GEMV work-group for plan p and m tokens.
+// LDS bytes of one GEMV wave's staging region, and of a work-group, for plan p
+// and m tokens.
+size_t gemv_wave_lds_bytes(const GemvPlan& p, int32_t m);
 size_t gemv_lds_bytes(const GemvPlan& p, int32_t m);
 
 // Block accessor of a layout for wave_range (host side).
 struct LayoutBlocks {
   const polyq_layout* L;
   const int32_t* waves;
-  void operator()(int i, int* cb, int* ce, int* w0, int* nw, uint32_t* magic) const {
-    if (i >= L->nblocks) return;
-    *cb = L->k_begin[i] / kChunk;
-    *ce = (L->k_begin[i] + L->block[i].len) / kChunk;
+  int cb(int i) const { return L->k_begin[i] / kChunk; }
+  int ce(int i) const { return (L->k_begin[i] + L->block[i].len) / kChunk; }
+  int w0(int i) const {
     int first = 0;
     for (int j = 0; j < i; ++j) first += waves[j];
-    *w0 = first;
-    *nw = waves[i];
-    *magic = div_magic(static_cast<uint32_t>(waves[i]));
+    return first;
   }
+  int nw(int i) const { return waves[i]; }
+  uint32_t magic(int i) const { return div_magic(static_cast<uint32_t>(waves[i])); }
 };
 
 inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }

@@ -94,13 +94,17 @@ bool layout_is_valid(const polyq_layout* L) {
   return memcmp(&ref, L, sizeof(ref)) == 0;
 }
 
+size_t gemv_wave_lds_bytes(const GemvPlan& p, int32_t m) {
+  // x' rows + a zero row of the wave's channels (16-byte aligned), then its
+  // group metadata
+  return static_cast<size_t>(align_up(static_cast<int64_t>(p.lds_chunks) * kChunk * (m + 1) * 2, 16)) +
+         static_cast<size_t>(p.lds_groups) * kMetaBytes;
+}
+
 size_t gemv_lds_bytes(const GemvPlan& p, int32_t m) {
-  // x' rows + a zero row (16-byte aligned), then every wave's group metadata;
-  // reused for the reduction
-  const size_t xs = static_cast<size_t>(align_up(static_cast<int64_t>(p.lds_chunks) * kChunk * (m + 1) * 2, 16)) +
-                    static_cast<size_t>(p.W) * p.lds_groups * kMetaBytes;
+  // every wave's staging region; reused for the reduction
   const size_t red = static_cast<size_t>(p.W) * m * kTileRows * 4;
-  return std::max(xs, red);
+  return std::max(static_cast<size_t>(p.W) * gemv_wave_lds_bytes(p, m), red);
 }
 
 // Group records of b <= 8 blocks that overlap the chunk range [lo, hi).
@@ -169,18 +173,13 @@ int plan_gemv(const polyq_layout& L, int32_t m, int32_t launch_tiles, GemvPlan* 
     waves_per_block(L, S * W, p->waves);
     const LayoutBlocks blk{&L, p->waves};
     int worst = 0, worst_groups = 0;
-    for (int s = 0; s < S; ++s) {
-      int lo = C, hi = 0;
-      for (int w = 0; w < W; ++w) {
-        int a, b;
-        wave_range(s * W + w, L.nblocks, C, blk, &a, &b);
-        if (a < b) {
-          lo = std::min(lo, a);
-          hi = std::max(hi, b);
-          worst_groups = std::max(worst_groups, groups_touched(L, a, b));
-        }
+    for (int w = 0; w < S * W; ++w) {
+      int a, b;
+      wave_range(w, L.nblocks, C, blk, &a, &b);
+      if (a < b) {
+        worst = std::max(worst, b - a);
+        worst_groups = std::max(worst_groups, groups_touched(L, a, b));
       }
-      if (lo < hi) worst = std::max(worst, hi - lo);
     }
     p->lds_chunks = worst;
     p->lds_groups = worst_groups;
