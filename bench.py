@@ -355,7 +355,11 @@ def main_qwen(a, torch, pq, synth):
     dev = torch.device("cuda", 0)
     _log(f"building {a.qwen_layers} Qwen3-32B-shaped layers")
     t0 = time.time()
-    layers = [build_layer(torch, pq, synth, 4, layer=l) for l in range(a.qwen_layers)]
+    layers = []
+    for l in range(a.qwen_layers):
+        layers.append(build_layer(torch, pq, synth, 4, layer=l))
+        if (l + 1) % 8 == 0:
+            _log(f"{l + 1} layers built ({time.time() - t0:.1f} s)")
     step_bytes = sum(pl.weight_bytes for L in layers for _, pl, _ in L)
     _log(f"{step_bytes / 1e9:.2f} GB packed in {time.time() - t0:.1f} s")
     res = {}
