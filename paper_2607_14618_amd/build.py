@@ -23,7 +23,11 @@ CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", f"-I{INCLUDE}"
           "-Wno-unused-function"]
 # Per-source additions.  The decode GEMV keeps its small MFMA accumulators in
 # VGPRs (they feed VALU folds every group; the AGPR form costs a copy each way).
-EXTRA = {"gemv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# The prefill GEMM keeps its accumulators in VGPRs too (the group fold reads
+# them every 128 channels) and its private arrays out of LDS (with one
+# work-group per CU the compiler would otherwise move one there).
+EXTRA = {"gemv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+         "gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-disable-promote-alloca-to-lds"]}
 
 
 def _compile(src: str) -> str:

@@ -2,16 +2,31 @@
 //   y[m][n] = sum_k' w_hat[n][k'] x'[m][k'],  x' = x[:, perm] (Eq. 9)
 //
 // Prefill is a dense contraction, so it runs on the bf16 matrix cores
-// (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  Each work-group owns a
-// 128-token x 64-row output tile (one packed tile); per 32-channel chunk the
-// work-group dequantizes the chunk of its 64 rows into LDS and its four waves
-// multiply it with their 32 tokens each.  Group-fold numerics: the dequantized
-// operand is (q - z), an integer of magnitude <= 255 that bf16 holds exactly;
-// each 128-channel group accumulates into its own fp32 tile, which is then
-// scaled by the row's fp16 scale s and added to the output accumulator.  A
-// 16-bit channel enters as the exact pair hi + lo of bf16 values of its fp16
-// weight (two MFMAs), so every product is exact before fp32 accumulation.
+// (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  A work-group owns 256 tokens
+// x 64*TN weight rows (TN packed tiles) and walks K one 32-channel chunk at a
+// time through a two-stage LDS ring:
+//   * every thread prefetches, two chunks ahead, 32 or 64 bytes of activations
+//     and its share of the packed chunk (one row sub-tile of one lane slice,
+//     4*b/4 .. 4*b bytes) plus that row's zero point;
+//   * the packed share is dequantized once per work-group into a bf16 tile in
+//     LDS that all waves of the work-group multiply (weights are the MFMA A
+//     operand, activations the B operand);
+//   * wave (tq, rt) multiplies rows 64*rt.. by tokens 64*tq..: 16 MFMAs per
+//     chunk; one barrier per chunk.
+// Group-fold numerics: the dequantized operand is (q - z), an integer of
+// magnitude <= 255 that bf16 holds exactly when z is an integer; each
+// 128-channel group accumulates into its own fp32 tile, which is then scaled
+// by the row's fp16 scale s (fp32 FMA) into the output accumulator.  A 16-bit
+// channel, or a group whose zero point is not an integer, enters as the pair
+// hi + lo of bf16 values (two MFMAs); for 16-bit weights the pair is exact.
+//
+// Dequantization uses the fp16 exponent field: (1024 + q) is the fp16 with
+// exponent 10 and mantissa q, so one AND-OR forms two codes of a pair as fp16,
+// and one mixed-precision FMA per code gives q - z in fp32 exactly; the bf16
+// value is then the fp32 value's upper half (exact when its lower half is 0).
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "codec.h"
 #include "internal.h"
@@ -20,179 +35,395 @@ namespace polyq {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 
-constexpr int kBM = 128;          // tokens per work-group
-constexpr int kBN = kTileRows;    // rows per work-group (one packed tile)
-constexpr int kWaves = 4;         // each wave: 32 tokens x 64 rows
-constexpr int kLdsRow = 40;       // bf16 per LDS row (32 + 8 pad against bank conflicts)
+constexpr int kTokWG = 256;   // tokens per work-group: 4 waves of 64 along M
+constexpr int kLdsRow = 40;   // bf16 per LDS row: 32 channels + 8 pad against bank conflicts
+constexpr uint32_t kMagic2 = 0x64006400u;  // two fp16 1024.0
 
 struct GemmArgs {
   const uint8_t* packed;
   const uint16_t* x;  // bf16 [m][k], clustered order
   float* y;           // fp32 [m][n]
-  int32_t n, k, m, nblocks;
+  int32_t n, k, m, nblocks, n_tiles, n_chunks, m_tiles;
+  int32_t y_vec;  // rows of y can take 16-byte stores (n % 4 == 0, y 16-byte aligned)
   int32_t bits[POLYQ_MAX_BLOCKS];
-  int32_t chunk_begin[POLYQ_MAX_BLOCKS];
-  int32_t chunk_end[POLYQ_MAX_BLOCKS];
-  int64_t block_offset[POLYQ_MAX_BLOCKS];
-  int64_t tile_bytes[POLYQ_MAX_BLOCKS];
-  int64_t record_bytes[POLYQ_MAX_BLOCKS];
+  int32_t cb[POLYQ_MAX_BLOCKS];  // first chunk of each block
+  int32_t ce[POLYQ_MAX_BLOCKS];  // end chunk of each block
+  int64_t off[POLYQ_MAX_BLOCKS];
+  int64_t tb[POLYQ_MAX_BLOCKS];  // bytes of one packed tile of the block
+  int64_t rb[POLYQ_MAX_BLOCKS];  // bytes of one group record (meta + 4 chunks)
 };
 
-// fp32 -> bf16 bits, round to nearest even (inputs here are finite).
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
+// Per-chunk facts the MFMA and dequantization stages need (32-bit, from the
+// block table in wave-uniform registers: a short chain of scalar selects).
+struct ChunkInfo {
+  int bits, cl, last;  // bit-width, chunk index in its block, ends its group
+};
+
+struct BlockTable {
+  int nblocks, bits[POLYQ_MAX_BLOCKS], cb[POLYQ_MAX_BLOCKS], ce[POLYQ_MAX_BLOCKS];
+};
+
+__device__ __forceinline__ ChunkInfo chunk_info(const BlockTable& t, int c) {
+  int bits = t.bits[0], cb = t.cb[0], ce = t.ce[0];
+#pragma unroll
+  for (int j = 1; j < POLYQ_MAX_BLOCKS; ++j) {
+    const bool in = j < t.nblocks && c >= t.ce[j - 1];
+    bits = in ? t.bits[j] : bits;
+    cb = in ? t.cb[j] : cb;
+    ce = in ? t.ce[j] : ce;
+  }
+  ChunkInfo p;
+  p.bits = bits;
+  p.cl = c - cb;
+  p.last = ((p.cl & 3) == 3 || c + 1 == ce) ? 1 : 0;
+  return p;
+}
+
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(bytes), 0x00020000);
+}
+
+// Prefetched data of one chunk for one thread.
+template <int TN>
+struct Pre {
+  u4v av[4 / TN];  // activation pieces (16 bytes each)
+  u4v w;           // 16 bytes from this thread's packed sub-tile (the first 4*b/4 .. 16 used)
+  uint32_t z, s;   // its row's fp16 zero point and scale (bits), b <= 8
+};
+
+// Two codes of a pair as fp16 (1024 + q): the fields sit at bit offsets o and
+// 16 + o of w.
+__device__ __forceinline__ uint32_t pair_magic(uint32_t w, int o, uint32_t mask2) {
+  return ((w >> o) & mask2) | kMagic2;
+}
+
+// The 4 code pairs (channels 2j, 2j+1) of row sub-tile r of a lane slice, in
+// the slice arrangement of codec.h, as fp16 pairs (1024 + q).
+template <int B>
+__device__ __forceinline__ void sub_tile_pairs(const u4v w, int r, uint32_t* hp) {
+  if constexpr (B == 2) {  // word r/2 (loaded as w.x) holds sub-tiles r & ~1 and r | 1
+    const int sh = 8 * (r & 1);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) hp[j] = pair_magic(w.x, sh + 2 * j, 0x00030003u);
+  } else if constexpr (B == 4) {  // word r
+#pragma unroll
+    for (int j = 0; j < 4; ++j) hp[j] = pair_magic(w.x, 4 * j, 0x000F000Fu);
+  } else if constexpr (B == 8) {  // words 2r, 2r+1
+#pragma unroll
+    for (int j = 0; j < 4; ++j) hp[j] = pair_magic((j >> 1) ? w.y : w.x, 8 * (j & 1), 0x00FF00FFu);
+  } else {  // B == 3: all three words; pair P = 4r + j sits in word P/5 at f3(P%5)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int P = 4 * r + j;
+      if (P < 15) {
+        const int d = P / 5, p = P - 5 * d;
+        const uint32_t wd = d == 0 ? w.x : (d == 1 ? w.y : w.z);
+        hp[j] = pair_magic(wd, 3 * p + (p >= 3 ? 1 : 0), 0x00070007u);
+      } else {  // codes 30, 31: bit d of each in bits 9 and 25 of word d
+        const uint32_t t = ((w.x >> 9) & 0x00010001u) | ((w.y >> 8) & 0x00020002u) |
+                           ((w.z >> 7) & 0x00040004u);
+        hp[j] = t | kMagic2;
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t hi_half_pair(float lo, float hi) {
+  return __builtin_amdgcn_perm(__builtin_bit_cast(uint32_t, hi), __builtin_bit_cast(uint32_t, lo),
+                               0x07060302u);
+}
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
   const uint32_t u = __builtin_bit_cast(uint32_t, f);
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
-__device__ __forceinline__ float bf16_value(uint32_t b) { return __builtin_bit_cast(float, b << 16); }
-__device__ __forceinline__ uint32_t pack2(uint32_t lo, uint32_t hi) { return lo | (hi << 16); }
 
-// Thread (row R, quarter j) dequantizes channels 8j .. 8j+7 of tile row R of one
-// chunk into bf16 (q - z) in LDS row R, columns 8j .. 8j+7.  They sit in lane
-// slice 16j + R%16, row sub-tile R/16 (slice codes 8(R/16) .. +7).
-template <int B>
-__device__ __forceinline__ void dequant_chunk(const uint8_t* chunk, int R, int j, float z,
-                                              uint16_t* lds_b) {
-  uint32_t w[B];
-  const uint32_t* src = reinterpret_cast<const uint32_t*>(chunk + (16 * j + (R & 15)) * 4 * B);
+// Eight values of one row, each exact in bf16, into the hi tile.
+__device__ __forceinline__ void store_exact(const float* v, uint16_t* hi_dst) {
+  uint4 o;
+  o.x = hi_half_pair(v[0], v[1]);
+  o.y = hi_half_pair(v[2], v[3]);
+  o.z = hi_half_pair(v[4], v[5]);
+  o.w = hi_half_pair(v[6], v[7]);
+  *reinterpret_cast<uint4*>(hi_dst) = o;
+}
+
+// Eight values of one row as the bf16 pair hi (nearest) + lo (nearest to the
+// remainder).
+__device__ __forceinline__ void store_pair(const float* v, uint16_t* hi_dst, uint16_t* lo_dst) {
+  uint32_t hb[8], lb[8];
 #pragma unroll
-  for (int d = 0; d < B; ++d) w[d] = src[d];
-  const int r = R >> 4;
-  uint32_t out[4];
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const float a = static_cast<float>(slice_code<B>(w, slice_index(r, 2 * p))) - z;
-    const float b = static_cast<float>(slice_code<B>(w, slice_index(r, 2 * p + 1))) - z;
-    out[p] = pack2(bf16_bits(a), bf16_bits(b));
+  for (int i = 0; i < 8; ++i) {
+    hb[i] = bf16_rne(v[i]);
+    lb[i] = bf16_rne(v[i] - __builtin_bit_cast(float, hb[i] << 16));
   }
-  *reinterpret_cast<uint4*>(lds_b + R * kLdsRow + 8 * j) = uint4{out[0], out[1], out[2], out[3]};
+  *reinterpret_cast<uint4*>(hi_dst) =
+      uint4{hb[0] | (hb[1] << 16), hb[2] | (hb[3] << 16), hb[4] | (hb[5] << 16), hb[6] | (hb[7] << 16)};
+  *reinterpret_cast<uint4*>(lo_dst) =
+      uint4{lb[0] | (lb[1] << 16), lb[2] | (lb[3] << 16), lb[4] | (lb[5] << 16), lb[6] | (lb[7] << 16)};
 }
 
-// 16-bit chunk: hi = bf16(w), lo = bf16(w - hi) (exact), into two LDS tiles.
-__device__ __forceinline__ void split_fp16_chunk(const uint8_t* chunk, int R, int j,
-                                                 uint16_t* lds_hi, uint16_t* lds_lo) {
-  const uint4 u = *reinterpret_cast<const uint4*>(chunk + (16 * j + (R & 15)) * 64 + 16 * (R >> 4));
-  const uint32_t wd[4] = {u.x, u.y, u.z, u.w};
-  uint32_t hi[4], lo[4];
+// Byte offset of row sub-tile r inside a lane slice of a b-bit chunk (the
+// word(s) holding its codes; 3-bit slices are read whole).
+__device__ __forceinline__ int sub_offset(int b, int r) {
+  return b == 2 ? (r >> 1) * 4 : b == 4 ? r * 4 : b == 8 ? r * 8 : b == 16 ? r * 16 : 0;
+}
+
+template <int TN>
+__global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
+  constexpr int kThreads = 256 * TN, kRows = 64 * TN;
+  constexpr int kAPieces = 4 / TN;  // 16-byte activation pieces per thread per chunk
+  __shared__ __attribute__((aligned(16))) uint16_t lds_a[2][kTokWG * kLdsRow];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_b[2][2][kRows * kLdsRow];  // [stage][hi, lo]
+  __shared__ __attribute__((aligned(16))) float lds_s[2][kRows];                 // row scales of the stage's group
+  __shared__ int lds_tag[2];  // chunk index + 1 when the stage holds a nonzero lo tile
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tq = wv & 3, rt = wv >> 2;  // MFMA role: token quarter, packed tile
+  // Token tile fastest: neighbouring work-groups (on different XCDs) share the
+  // weight rows, and each XCD's work-groups keep to a subset of token tiles.
+  const int mt = static_cast<int>(blockIdx.x) % a.m_tiles, rp = static_cast<int>(blockIdx.x) / a.m_tiles;
+  const int m0 = mt * kTokWG;
+  const int C = a.n_chunks;
+  BlockTable bt;
+  bt.nblocks = a.nblocks;
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    uint32_t h2[2], l2[2];
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const uint16_t bits = static_cast<uint16_t>(e == 0 ? (wd[p] & 0xFFFFu) : (wd[p] >> 16));
-      const float v = static_cast<float>(__builtin_bit_cast(_Float16, bits));
-      h2[e] = bf16_bits(v);
-      l2[e] = bf16_bits(v - bf16_value(h2[e]));
-    }
-    hi[p] = pack2(h2[0], h2[1]);
-    lo[p] = pack2(l2[0], l2[1]);
+  for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) {
+    bt.bits[i] = a.bits[i];
+    bt.cb[i] = a.cb[i];
+    bt.ce[i] = a.ce[i];
   }
-  *reinterpret_cast<uint4*>(lds_hi + R * kLdsRow + 8 * j) = uint4{hi[0], hi[1], hi[2], hi[3]};
-  *reinterpret_cast<uint4*>(lds_lo + R * kLdsRow + 8 * j) = uint4{lo[0], lo[1], lo[2], lo[3]};
-}
 
-__device__ __forceinline__ bf16x8 load_frag(const uint16_t* p) {
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
-}
+  // Dequantization role: packed tile dt, row sub-tile dr (wave-uniform), lane
+  // slice lane; row drow of the tile.
+  const int dp = wv >> 2, dr = wv & 3;
+  const int dt = rp * TN + dp;
+  const bool dtile_ok = dt < a.n_tiles;
+  const int drow = 16 * dr + (lane & 15);
+  const int bofs = (dp * 64 + drow) * kLdsRow + 8 * (lane >> 4);
+  const bool s_writer = lane < 16;  // one thread per row writes the row's scale
+  constexpr int kHalfB = kRows * kLdsRow;
 
-__global__ __launch_bounds__(kWaves * 64) void gemm_kernel(const GemmArgs a) {
-  __shared__ uint16_t lds_b[2][kBN * kLdsRow];  // [0]: (q - z) or hi, [1]: lo
-  __shared__ float lds_s[kBN];
+  // Activations: buffer over rows m0 .. m0 + 255 of x' (reads past row m - 1
+  // return zero); piece j of this thread is token piece/4, 16-byte segment piece%4.
+  const __amdgpu_buffer_rsrc_t xrs =
+      make_rsrc(a.x + static_cast<int64_t>(m0) * a.k, static_cast<uint32_t>(min(a.m - m0, kTokWG)) * a.k * 2u);
+  uint32_t avoff[kAPieces];
+#pragma unroll
+  for (int j = 0; j < kAPieces; ++j) {
+    const int piece = tid + j * kThreads;
+    avoff[j] = (static_cast<uint32_t>(piece >> 2) * a.k + (piece & 3) * 8) * 2u;
+  }
 
-  const int mt = blockIdx.x, tile = blockIdx.y;
-  const int tid = threadIdx.x;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int dq_row = tid & 63, dq_q = wave;  // dequant assignment: row, quarter of the chunk
-  const int m_wave = mt * kBM + wave * 32;   // first token of this wave
+  // Load cursor: the next chunk to fetch, its block and a buffer over this
+  // thread's packed tile of that block (no records for a tile past the end,
+  // so its reads return zero).
+  int lc = 0, lb = 0, lcl = 0, lbits = 0, lce = 0, lrb = 0;
+  uint32_t lvoff = 0;
+  __amdgpu_buffer_rsrc_t wrs;
+  auto set_block = [&](int b) {
+    lb = b;
+    lbits = a.bits[b];
+    lce = a.ce[b];
+    lrb = static_cast<int>(a.rb[b]);
+    const int64_t tb = a.tb[b];
+    wrs = make_rsrc(a.packed + a.off[b] + static_cast<int64_t>(dtile_ok ? dt : 0) * tb,
+                    dtile_ok ? static_cast<uint32_t>(tb) : 0u);
+    lvoff = static_cast<uint32_t>(lane * 4 * lbits + sub_offset(lbits, dr));
+    lcl = 0;
+  };
+  const uint32_t zvoff = 2 * meta_z_half(drow), svoff = 2 * meta_s_half(drow);
+  auto load = [&](Pre<TN>& pr) {
+#pragma unroll
+    for (int j = 0; j < kAPieces; ++j)
+      pr.av[j] = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, avoff[j], lc * 64, 0));
+    const int rec = (lcl >> 2) * lrb;
+    const int soff = rec + (lbits <= 8 ? kMetaBytes : 0) + (lcl & 3) * 256 * lbits;
+    pr.w = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(wrs, lvoff, soff, 0));
+    pr.z = __builtin_amdgcn_raw_buffer_load_b16(wrs, zvoff, rec, 0);
+    pr.s = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff, rec, 0);
+    ++lc;
+    ++lcl;
+    if (lc == lce && lc < C) set_block(lb + 1);
+  };
 
-  floatx4 total[2][4], part[2][4];
+  auto store = [&](int c, const Pre<TN>& pr, int st) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < kAPieces; ++j) {
+      const int piece = tid + j * kThreads;
+      *reinterpret_cast<u4v*>(&lds_a[st][(piece >> 2) * kLdsRow + (piece & 3) * 8]) = pr.av[j];
+    }
+    const ChunkInfo ci = chunk_info(bt, c);
+    uint16_t* hi = &lds_b[st][0][bofs];
+    uint16_t* lo = hi + kHalfB;
+    float v[8];
+    if (ci.bits == 16) {
+      const uint32_t ww[4] = {pr.w.x, pr.w.y, pr.w.z, pr.w.w};
 #pragma unroll
-    for (int jn = 0; jn < 4; ++jn) total[i][jn] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  // A fragment source rows (tokens) of this lane; rows >= m read as zero
-  const int arow0 = m_wave + (lane & 15), arow1 = arow0 + 16;
-  const int acol = 8 * (lane >> 4);
-
-  for (int bi = 0; bi < a.nblocks; ++bi) {
-    const int B = a.bits[bi];
-    const int cb0 = a.chunk_begin[bi], nch = a.chunk_end[bi] - cb0;
-    const uint8_t* tile_base = a.packed + a.block_offset[bi] + tile * a.tile_bytes[bi];
-    const int meta = B <= 8 ? kMetaBytes : 0;
-    for (int g = 0; g * 4 < nch; ++g) {
-      const uint8_t* rec = tile_base + g * a.record_bytes[bi];
-      float z = 0.f;
-      if (B <= 8)
-        z = static_cast<float>(reinterpret_cast<const _Float16*>(rec)[meta_z_half(dq_row)]);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int jn = 0; jn < 4; ++jn) part[i][jn] = floatx4{0.f, 0.f, 0.f, 0.f};
-      const int cend = min(nch, 4 * g + 4);
-      for (int c = 4 * g; c < cend; ++c) {
-        __syncthreads();  // the previous chunk's LDS tile is consumed
-        const uint8_t* chunk_rows = rec + meta + (c & 3) * (64 * 4 * B);
-        switch (B) {
-          case 2: dequant_chunk<2>(chunk_rows, dq_row, dq_q, z, lds_b[0]); break;
-          case 3: dequant_chunk<3>(chunk_rows, dq_row, dq_q, z, lds_b[0]); break;
-          case 4: dequant_chunk<4>(chunk_rows, dq_row, dq_q, z, lds_b[0]); break;
-          case 8: dequant_chunk<8>(chunk_rows, dq_row, dq_q, z, lds_b[0]); break;
-          default: split_fp16_chunk(chunk_rows, dq_row, dq_q, lds_b[0], lds_b[1]); break;
-        }
-        if (B <= 8 && c == 4 * g && tid < kBN)
-          lds_s[tid] = static_cast<float>(reinterpret_cast<const _Float16*>(rec)[meta_s_half(tid)]);
-        __syncthreads();
-        const int kc = (cb0 + c) * kChunk + acol;
-        bf16x8 afr[2];
-        afr[0] = arow0 < a.m ? load_frag(a.x + static_cast<int64_t>(arow0) * a.k + kc)
-                             : __builtin_bit_cast(bf16x8, uint4{0, 0, 0, 0});
-        afr[1] = arow1 < a.m ? load_frag(a.x + static_cast<int64_t>(arow1) * a.k + kc)
-                             : __builtin_bit_cast(bf16x8, uint4{0, 0, 0, 0});
-#pragma unroll
-        for (int jn = 0; jn < 4; ++jn) {
-          const bf16x8 bfr = load_frag(lds_b[0] + (jn * 16 + (lane & 15)) * kLdsRow + acol);
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-            part[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr[i], bfr, part[i][jn], 0, 0, 0);
-        }
-        if (B == 16) {
-#pragma unroll
-          for (int jn = 0; jn < 4; ++jn) {
-            const bf16x8 bfr = load_frag(lds_b[1] + (jn * 16 + (lane & 15)) * kLdsRow + acol);
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-              part[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afr[i], bfr, part[i][jn], 0, 0, 0);
-          }
-        }
+      for (int i = 0; i < 4; ++i) {
+        const h2 h = __builtin_bit_cast(h2, ww[i]);
+        v[2 * i] = static_cast<float>(h.x);
+        v[2 * i + 1] = static_cast<float>(h.y);
       }
-      // group fold: total += s[n] * part (16-bit channels: scale 1)
+      if (s_writer) lds_s[st][dp * 64 + drow] = 1.f;
+      store_pair(v, hi, lo);
+      return;
+    }
+    const float zf = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.z)));
+    if (s_writer) lds_s[st][dp * 64 + drow] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s)));
+    uint32_t hp[4];
+    switch (ci.bits) {
+      case 2: sub_tile_pairs<2>(pr.w, dr, hp); break;
+      case 3: sub_tile_pairs<3>(pr.w, dr, hp); break;
+      case 4: sub_tile_pairs<4>(pr.w, dr, hp); break;
+      default: sub_tile_pairs<8>(pr.w, dr, hp); break;
+    }
+    // (1024 + q) - (1024 + z) = q - z, exact in fp32; exact in bf16 too when z
+    // is an integer in [0, 255] (then |q - z| <= 255)
+    const float zoff = 1024.f + zf;
 #pragma unroll
-      for (int jn = 0; jn < 4; ++jn) {
-        const float s = B <= 8 ? lds_s[jn * 16 + (lane & 15)] : 1.f;
+    for (int j = 0; j < 4; ++j) {
+      const h2 h = __builtin_bit_cast(h2, hp[j]);
+      v[2 * j] = static_cast<float>(h.x) - zoff;
+      v[2 * j + 1] = static_cast<float>(h.y) - zoff;
+    }
+    if (zf == truncf(zf) && zf >= 0.f && zf <= 255.f) {
+      store_exact(v, hi);
+      *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
+    } else {
+      store_pair(v, hi, lo);
+      lds_tag[st] = c + 1;  // any thread; every writer stores the same value
+    }
+  };
+
+  f4 total[4][4], part[4][4];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) total[i][jn][e] = fmaf(s, part[i][jn][e], total[i][jn][e]);
+    for (int j = 0; j < 4; ++j) total[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  const int aofs = (tq * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
+  const int bofs_m = (rt * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
+  // Chunk c: multiply stage c&1, dequantize chunk c+1 from `slot` into the
+  // other stage, fetch chunk c+3 into `slot`, fold a finished group.
+  auto step = [&](int c, Pre<TN>& slot) {
+    const int st = c & 1;
+    const ChunkInfo ci = chunk_info(bt, c);
+    const bool two = ci.bits == 16 || lds_tag[st] == c + 1;
+    bf16x8 af[4], bfr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      af[i] = *reinterpret_cast<const bf16x8*>(&lds_b[st][0][bofs_m + i * 16 * kLdsRow]);
+      bfr[i] = *reinterpret_cast<const bf16x8*>(&lds_a[st][aofs + i * 16 * kLdsRow]);
+    }
+    if ((ci.cl & 3) == 0) {  // first chunk of a group: fresh partial sums
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          part[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) part[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], part[i][j], 0, 0, 0);
+    }
+    if (two) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(&lds_b[st][1][bofs_m + i * 16 * kLdsRow]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) part[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], part[i][j], 0, 0, 0);
+    }
+    if (c + 1 < C) store(c + 1, slot, st ^ 1);
+    if (c + 3 < C) load(slot);
+    if (ci.last) {  // group fold: total += s * part, s of rows 16 i + 4 (lane/16) + e
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f4 sv = *reinterpret_cast<const f4*>(&lds_s[st][rt * 64 + 16 * i + 4 * (lane >> 4)]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) total[i][j][e] = fmaf(sv[e], part[i][j][e], total[i][j][e]);
+      }
+    }
+    __syncthreads();
+  };
+
+  Pre<TN> s0, s1;
+  if (tid < 2) lds_tag[tid] = 0;
+  set_block(0);
+  load(s0);
+  if (C > 1) load(s1);
+  __syncthreads();
+  store(0, s0, 0);
+  if (C > 2) load(s0);
+  __syncthreads();
+  int c = 0;
+  for (; c + 1 < C; c += 2) {
+    step(c, s1);
+    step(c + 1, s0);
+  }
+  if (c < C) step(c, s1);
+
+  // D layout: lane holds weight rows 16 i + 4 (lane/16) + e of token 16 j + lane%16.
+  const int row0 = (rp * TN + rt) * kTileRows + 4 * (lane >> 4);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int tok = m0 + tq * 64 + 16 * j + (lane & 15);
+    if (tok >= a.m) continue;
+    float* yr = a.y + static_cast<int64_t>(tok) * a.n;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = row0 + 16 * i;
+      if (a.y_vec && row + 3 < a.n) {
+        *reinterpret_cast<f4*>(yr + row) = total[i][j];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (row + e < a.n) yr[row + e] = total[i][j][e];
       }
     }
   }
-  // D layout: lane holds rows 4*(lane/16)+e of the 16x16 tile, column lane%16
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int jn = 0; jn < 4; ++jn) {
-      const int col = tile * kBN + jn * 16 + (lane & 15);
-      if (col >= a.n) continue;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int row = m_wave + i * 16 + 4 * (lane >> 4) + e;
-        if (row < a.m) a.y[static_cast<int64_t>(row) * a.n + col] = total[i][jn][e];
-      }
-    }
 }
 
+// x'[i][j] = x[i][perm[j]] for one token row per work-group: the row is staged
+// in LDS with 16-byte loads, then gathered there and written with 16-byte
+// stores (k <= kPermLdsK, rows 16-byte aligned).
+constexpr int kPermLdsK = 32768;
+
+__global__ __launch_bounds__(256) void permute_rows_lds_kernel(const int32_t* __restrict__ perm,
+                                                               const uint16_t* __restrict__ x,
+                                                               uint16_t* __restrict__ out, int k) {
+  extern __shared__ uint4 row4[];
+  const uint16_t* row = reinterpret_cast<const uint16_t*>(row4);
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * k;
+  const uint4* src = reinterpret_cast<const uint4*>(x + base);
+  for (int j = threadIdx.x; j < k / 8; j += 256) row4[j] = src[j];
+  __syncthreads();
+  uint4* dst = reinterpret_cast<uint4*>(out + base);
+  const int4* p4 = reinterpret_cast<const int4*>(perm);
+  for (int j = threadIdx.x; j < k / 8; j += 256) {
+    const int4 p0 = p4[2 * j], p1 = p4[2 * j + 1];
+    const int p[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+    uint32_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = static_cast<unsigned>(p[e]) < static_cast<unsigned>(k) ? row[p[e]] : 0u;
+    dst[j] = uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+  }
+}
+
+// Fallback gather, one element per thread (any k, any alignment).
 __global__ __launch_bounds__(256) void permute_rows_kernel(const int32_t* __restrict__ perm,
                                                            const uint16_t* __restrict__ x,
                                                            uint16_t* __restrict__ out, int m, int k) {
@@ -201,6 +432,11 @@ __global__ __launch_bounds__(256) void permute_rows_kernel(const int32_t* __rest
   const int i = static_cast<int>(idx / k), kp = static_cast<int>(idx % k);
   const int p = perm[kp];
   out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
+}
+
+// Work-groups of a launch with TN packed tiles per work-group.
+int64_t gemm_groups(const polyq_layout& L, int32_t m, int tn) {
+  return static_cast<int64_t>((L.n_tiles + tn - 1) / tn) * ((m + kTokWG - 1) / kTokWG);
 }
 
 }  // namespace
@@ -229,12 +465,19 @@ extern "C" polyq_status polyq_gemm(const polyq_layout* layout, const void* packe
     const size_t need = polyq_gemm_workspace_bytes(layout, m, 1);
     if (workspace == nullptr || workspace_bytes < need) return POLYQ_ERR_CAPACITY;
     if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0) return POLYQ_ERR_ARG;
-    const int64_t items = static_cast<int64_t>(m) * L.k;
-    hipLaunchKernelGGL(permute_rows_kernel, dim3(static_cast<unsigned>((items + 255) / 256)),
-                       dim3(256), 0, st, perm, x, static_cast<uint16_t*>(workspace), m, L.k);
-    xp = static_cast<const uint16_t*>(workspace);
+    uint16_t* out = static_cast<uint16_t*>(workspace);
+    if (L.k <= kPermLdsK && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+        reinterpret_cast<uintptr_t>(perm) % 16 == 0) {
+      hipLaunchKernelGGL(permute_rows_lds_kernel, dim3(static_cast<unsigned>(m)), dim3(256),
+                         static_cast<size_t>(L.k) * 2, st, perm, x, out, L.k);
+    } else {
+      const int64_t items = static_cast<int64_t>(m) * L.k;
+      hipLaunchKernelGGL(permute_rows_kernel, dim3(static_cast<unsigned>((items + 255) / 256)),
+                         dim3(256), 0, st, perm, x, out, m, L.k);
+    }
+    xp = out;
   } else if (reinterpret_cast<uintptr_t>(x) % 16 != 0) {
-    return POLYQ_ERR_ARG;  // fragments are read as 16-byte vectors
+    return POLYQ_ERR_ARG;  // activations are read as 16-byte vectors
   }
   GemmArgs a;
   a.packed = static_cast<const uint8_t*>(packed);
@@ -244,16 +487,27 @@ extern "C" polyq_status polyq_gemm(const polyq_layout* layout, const void* packe
   a.k = L.k;
   a.m = m;
   a.nblocks = L.nblocks;
+  a.n_tiles = L.n_tiles;
+  a.n_chunks = L.n_chunks;
+  a.m_tiles = (m + kTokWG - 1) / kTokWG;
+  a.y_vec = (L.n % 4 == 0 && reinterpret_cast<uintptr_t>(y) % 16 == 0) ? 1 : 0;
   for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) {
     const bool used = i < L.nblocks;
-    a.bits[i] = used ? L.block[i].bits : 0;
-    a.chunk_begin[i] = used ? L.k_begin[i] / kChunk : 0;
-    a.chunk_end[i] = used ? (L.k_begin[i] + L.block[i].len) / kChunk : 0;
-    a.block_offset[i] = used ? L.block_offset[i] : 0;
-    a.tile_bytes[i] = used ? L.tile_bytes[i] : 0;
-    a.record_bytes[i] = used ? L.record_bytes[i] : 0;
+    a.bits[i] = used ? L.block[i].bits : 16;
+    a.cb[i] = used ? L.k_begin[i] / kChunk : L.n_chunks;
+    a.ce[i] = used ? (L.k_begin[i] + L.block[i].len) / kChunk : L.n_chunks;
+    a.off[i] = used ? L.block_offset[i] : 0;
+    a.tb[i] = used ? L.tile_bytes[i] : 0;
+    a.rb[i] = used ? L.record_bytes[i] : 0;
   }
-  const dim3 grid((m + kBM - 1) / kBM, L.n_tiles);
-  hipLaunchKernelGGL(gemm_kernel, grid, dim3(kWaves * 64), 0, st, a);
+  // Two packed tiles per work-group when that still gives a full round of
+  // work-groups, else one (twice as many work-groups, each half as wide).
+  const bool wide = gemm_groups(L, m, 2) >= 240;
+  const int64_t groups = gemm_groups(L, m, wide ? 2 : 1);
+  if (groups > 0x7FFFFFFF) return POLYQ_ERR_CAPACITY;
+  if (wide)
+    hipLaunchKernelGGL(gemm_kernel<2>, dim3(static_cast<unsigned>(groups)), dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL(gemm_kernel<1>, dim3(static_cast<unsigned>(groups)), dim3(256), 0, st, a);
   return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
 }

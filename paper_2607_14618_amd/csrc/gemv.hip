@@ -26,6 +26,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "codec.h"
 #include "internal.h"
@@ -566,13 +567,26 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
         const int v = use_perm ? pv[e] : kbase + kk + e;
         sr[e] = static_cast<unsigned>(v) < static_cast<unsigned>(kdim) ? v : -1;
       }
-      for (int t = t_lo; t < m; ++t) {
-        const auto xr = gl(xg + static_cast<int64_t>(t) * kdim);
-        uint32_t h[8];
+      // Tokens in batches of kTokBatch: every gather of a batch is issued
+      // before the first of them is used (one memory round trip per batch).
+      constexpr int kTokBatch = 8;
+      for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
+        uint32_t h[kTokBatch][8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) h[e] = sr[e] >= 0 ? static_cast<uint32_t>(xr[max(sr[e], 0)]) : 0u;
-        *reinterpret_cast<uint4*>(xs16 + t * range + kk) =
-            uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+        for (int j = 0; j < kTokBatch; ++j) {
+          const auto xr = gl(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) h[j][e] = xr[max(sr[e], 0)];
+        }
+#pragma unroll
+        for (int j = 0; j < kTokBatch; ++j) {
+          uint32_t v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = sr[e] >= 0 ? h[j][e] : 0u;
+          if (t0 + j < m)
+            *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) =
+                uint4{v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16)};
+        }
       }
       if (zero_row) *reinterpret_cast<uint4*>(xs16 + m * range + kk) = uint4{0u, 0u, 0u, 0u};
     }
@@ -671,14 +685,61 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   float* partial = ITEM(float*, partial);
   uint32_t* counter = ITEM(uint32_t*, counter);
   const int rows_pad = ITEM(int32_t, rows_pad);
-  for (int mi = 0; mi < m; ++mi) {
+  auto wg_sum = [&](int mi) {
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) v += red[(w * m + mi) * 64 + lane];
-    float* p = &partial[(static_cast<int64_t>(s) * m + mi) * rows_pad + row];
-    const float old = __hip_atomic_exchange(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    asm volatile("" ::"v"(old));  // keep the returning form of the swap
-  }
+    return v;
+  };
+  // Tokens go in batches of TB, all swaps of a batch in flight at once.
+  // Indices past the last token are clamped to it: a repeated swap writes the
+  // same value again, and in the finisher a repeated read-and-zero (issued
+  // after the real one, from the same lane) returns 0.
+  auto write_partials = [&](auto tb_tag) {
+    constexpr int TB = decltype(tb_tag)::value;
+    for (int t0 = 0; t0 < m; t0 += TB) {
+      float old[TB];
+#pragma unroll
+      for (int j = 0; j < TB; ++j) {
+        const int mi = min(t0 + j, m - 1);
+        old[j] = __hip_atomic_exchange(&partial[(static_cast<int64_t>(s) * m + mi) * rows_pad + row],
+                                       wg_sum(mi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+#pragma unroll
+      for (int j = 0; j < TB; ++j) asm volatile("" ::"v"(old[j]));  // keep the returning form
+    }
+  };
+  auto finish = [&](auto tb_tag) {
+    constexpr int TB = decltype(tb_tag)::value;
+    for (int t0 = 0; t0 < m; t0 += TB) {
+      float v[TB];
+#pragma unroll
+      for (int j = 0; j < TB; ++j) v[j] = 0.f;
+      for (int s0 = 0; s0 < S; s0 += 8) {  // eight splits of TB tokens in flight at a time
+        float t[TB][8];
+#pragma unroll
+        for (int j = 0; j < TB; ++j)
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            t[j][u] = __hip_atomic_exchange(
+                &partial[(static_cast<int64_t>(min(s0 + u, S - 1)) * m + min(t0 + j, m - 1)) * rows_pad + row],
+                0.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int j = 0; j < TB; ++j)
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v[j] += t[j][u];
+      }
+#pragma unroll
+      for (int j = 0; j < TB; ++j)
+        if (t0 + j < m && row < n) y[static_cast<int64_t>(t0 + j) * n + row] = v[j];
+    }
+  };
+  using One = std::integral_constant<int, 1>;
+  using Four = std::integral_constant<int, 4>;
+  if (m == 1)
+    write_partials(One{});
+  else
+    write_partials(Four{});
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __builtin_amdgcn_s_waitcnt(0);  // the swaps have returned
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -687,22 +748,10 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     ticket = __hip_atomic_fetch_add(&counter[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   ticket = __shfl(ticket, 0);
   if (ticket % static_cast<uint32_t>(S) != static_cast<uint32_t>(S - 1)) return;
-  for (int mi = 0; mi < m; ++mi) {
-    float v = 0.f;
-    for (int s0 = 0; s0 < S; s0 += 8) {  // eight reads in flight at a time
-      float t[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        t[u] = s0 + u < S
-                   ? __hip_atomic_exchange(
-                         &partial[(static_cast<int64_t>(s0 + u) * m + mi) * rows_pad + row], 0.f,
-                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                   : 0.f;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) v += t[u];
-    }
-    if (row < n) y[static_cast<int64_t>(mi) * n + row] = v;
-  }
+  if (m == 1)
+    finish(One{});
+  else
+    finish(Four{});
   if (lane == 0) __hip_atomic_store(&counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
