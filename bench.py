@@ -212,27 +212,37 @@ def decode_figure(torch, pq, synth, steps, warmup, variant, config=1, mix=None, 
     return res
 
 
-def prefill_figure(torch, pq, synth, steps, warmup, m=512):
+def prefill_figure(torch, pq, synth, steps, warmup, m=512, grouped=True):
     """Config: Llama2-13B layer, 4.0-bit prefill mix, bf16 activations, M=512,
-    permutation applied by the library (gather kernel + GEMM)."""
+    permutation applied by the library (gather kernel + GEMM); one launch per
+    group of linears that share an input (one permuted copy per group)."""
     dev = torch.device("cuda", 0)
     layer = build_layer(torch, pq, synth, 3, m=m, x_dtype=torch.bfloat16)
     flops = sum(2.0 * m * pl.n * pl.k for _, pl, _ in layer)
     ys = [torch.empty((m, pl.n), dtype=torch.float32, device=dev) for _, pl, _ in layer]
+    sched = schedule(layer, grouped)
 
-    def launches(i):
-        return [(lambda pl=pl, x=x, j=j: pl.prefill(x, y=ys[j])) for j, (_, pl, x) in enumerate(layer)]
-    ms, per = time_steps(torch, steps, warmup, launches, detail_steps=3)
+    def launch(idx):
+        if len(idx) == 1:
+            j = idx[0]
+            return lambda: layer[j][1].prefill(layer[j][2], y=ys[j])
+        return lambda: pq.prefill_batch([layer[j][1] for j in idx], [layer[j][2] for j in idx],
+                                        ys=[ys[j] for j in idx])
+    calls = [launch(idx) for idx in sched]
+    ms, per = time_steps(torch, steps, warmup, lambda i: calls, detail_steps=3)
     kern_ms = sum(per)
     res = {"workload": "Llama2-13B layer, 7 linears, prefill M=512, 4.0-bit mix 2/3/4/8/16 b "
                        "(20/30/35/13/2 %), bf16 activations, permutation applied in-library",
+           "launches": ("one per shared-input group: q/k/v, o, gate/up, down" if grouped
+                        else "one per linear"),
            "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
            "kernel_tflops": round(flops / (kern_ms * 1e-3) / 1e12, 2),
            "peak_tflops": BF16_PEAK_TFLOPS,
            "frac": round(flops / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
            "ms_per_step": round(ms, 4), "flop_per_step": flops,
            "weight_bytes_per_step": sum(pl.weight_bytes for _, pl, _ in layer),
-           "per_linear_us": {nm: round(t * 1e3, 1) for (nm, _, _), t in zip(layer, per)}}
+           "per_launch_us": {"+".join(layer[j][0] for j in idx): round(t * 1e3, 1)
+                             for idx, t in zip(sched, per)}}
     del layer, ys
     torch.cuda.empty_cache()
     return res
@@ -286,7 +296,8 @@ def line(value, unit, steps, warmup, ms, dtype, config, higher=True, **extra):
 
 def main_default(a, torch, pq, synth):
     if a.prefill_only:
-        p = prefill_figure(torch, pq, synth, max(3, a.steps // 20), max(1, a.warmup // 10))
+        p = prefill_figure(torch, pq, synth, max(3, a.steps // 20), max(1, a.warmup // 10),
+                           grouped=not a.per_linear)
         _log(f"prefill: {p['tflops']} TFLOP/s ({p['kernel_tflops']} in kernels)")
         line(p["tflops"], "TFLOP/s", max(3, a.steps // 20), max(1, a.warmup // 10),
              p["ms_per_step"], "bf16", {"workload": p["workload"], "m": 512}, prefill=p)
@@ -313,7 +324,7 @@ def main_default(a, torch, pq, synth):
     }
     if not a.no_prefill:
         _log("prefill GEMM, M=512")
-        extra["prefill"] = prefill_figure(torch, pq, synth, 10, 3)
+        extra["prefill"] = prefill_figure(torch, pq, synth, 10, 3, grouped=not a.per_linear)
         _log(f"prefill: {extra['prefill']['tflops']} TFLOP/s "
              f"({extra['prefill']['kernel_tflops']} in kernels)")
     if not a.no_cpu:

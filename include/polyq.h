@@ -200,19 +200,38 @@ polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32
 /*
  * polyq_gemm -- prefill product for any m >= 1 (bf16 activations):
  *   y[i][n] = sum_k' w_hat[n][k'] * x[i][perm[k']]
- *   x bf16 [m][k] bits, original channel order if perm != NULL, else clustered.
+ *   x bf16 [m][k] bits, original channel order if perm != NULL, else clustered
+ *   (then 16-byte aligned); m * k * 2 < 2^31.
  *   y fp32 [m][n], fully overwritten.
  *   workspace: at least polyq_gemm_workspace_bytes(layout, m) bytes of device
  *   scratch (holds the permuted activations when perm != NULL); contents on
  *   entry are ignored.
- * Computed with bf16 MFMA and fp32 accumulation: (q - z) is exact in bf16 and
- * the group scale is applied in fp32; a 16-bit channel enters as the exact
- * bf16 pair hi + lo of its fp16 weight.
+ * Computed with bf16 MFMA and fp32 accumulation: (q - z) enters as one exact
+ * bf16 value when z is an integer in [0, 255], else as the bf16 pair hi + lo
+ * (relative error below 2^-16); the group scale is applied in fp32; a 16-bit
+ * channel enters as the exact bf16 pair hi + lo of its fp16 weight.
  */
 size_t polyq_gemm_workspace_bytes(const polyq_layout* layout, int32_t m, int perm_given);
 polyq_status polyq_gemm(const polyq_layout* layout, const void* packed, const int32_t* perm,
                         const uint16_t* x, int32_t m, float* y, void* workspace,
                         size_t workspace_bytes, void* stream);
+
+/*
+ * polyq_gemm_batch -- up to POLYQ_MAX_BATCH independent prefill products in
+ * one launch (e.g. q/k/v, or gate/up, which share x and perm): item i computes
+ * what polyq_gemm(items[i].layout, items[i].packed, items[i].perm, items[i].x,
+ * m, items[i].y, ...) computes, with the same argument rules per item (x holds
+ * bf16 bits here).  Items with the same x and perm share one permuted copy.
+ *   workspace: at least polyq_gemm_batch_workspace_bytes(items, count, m)
+ *   bytes of device scratch (the permuted copies); contents on entry are
+ *   ignored.  The query reads the layout, x and perm fields; 0 on an invalid
+ *   request or when no item has a permutation.
+ */
+typedef polyq_gemv_item polyq_gemm_item;
+
+size_t polyq_gemm_batch_workspace_bytes(const polyq_gemm_item* items, int32_t count, int32_t m);
+polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t count, int32_t m,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static description of a status code (never NULL). */
 const char* polyq_status_str(polyq_status status);

@@ -30,7 +30,8 @@ STATUS = {0: "POLYQ_OK", 1: "POLYQ_ERR_ARG", 2: "POLYQ_ERR_BITS", 3: "POLYQ_ERR_
 # every symbol include/polyq.h declares
 EXPORTS = ("polyq_plan", "polyq_pack", "polyq_unpack", "polyq_permute", "polyq_gemv_workspace_bytes",
            "polyq_gemv", "polyq_gemv_batch_workspace_bytes", "polyq_gemv_batch",
-           "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_status_str")
+           "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_gemm_batch_workspace_bytes",
+           "polyq_gemm_batch", "polyq_status_str")
 
 
 class Block(ctypes.Structure):
@@ -103,10 +104,13 @@ def lib() -> ctypes.CDLL:
             L.polyq_gemm_workspace_bytes.argtypes = [lp, i32, ctypes.c_int]
             L.polyq_gemm_workspace_bytes.restype = sz
             L.polyq_gemm.argtypes = [lp, vp, vp, vp, i32, vp, vp, sz, vp]
+            L.polyq_gemm_batch_workspace_bytes.argtypes = [ip, i32, i32]
+            L.polyq_gemm_batch_workspace_bytes.restype = sz
+            L.polyq_gemm_batch.argtypes = [ip, i32, i32, vp, sz, vp]
             L.polyq_status_str.argtypes = [ctypes.c_int]
             L.polyq_status_str.restype = ctypes.c_char_p
             for name in ("polyq_plan", "polyq_pack", "polyq_unpack", "polyq_permute",
-                         "polyq_gemv", "polyq_gemv_batch", "polyq_gemm"):
+                         "polyq_gemv", "polyq_gemv_batch", "polyq_gemm", "polyq_gemm_batch"):
                 getattr(L, name).restype = ctypes.c_int
             _lib = L
     return _lib
@@ -311,3 +315,39 @@ def gemm(layout: Layout, packed: torch.Tensor, perm: Optional[torch.Tensor], x: 
                             _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                             _stream(dev)), "polyq_gemm")
     return y
+
+
+def gemm_batch(items: Sequence[Tuple[Layout, torch.Tensor, Optional[torch.Tensor], torch.Tensor,
+                                     Optional[torch.Tensor]]],
+               workspace: Optional[torch.Tensor] = None):
+    """One launch of several prefill GEMMs: items are (layout, packed, perm, x,
+    y or None) with bf16 x and the same token count m.  Returns the outputs."""
+    if not 1 <= len(items) <= MAX_BATCH:
+        raise ValueError(f"1..{MAX_BATCH} items per batch")
+    arr = (GemvItem * len(items))()
+    keep, ys, m, dev = [], [], None, None
+    for i, (layout, packed, perm, x, y) in enumerate(items):
+        x2 = x if x.dim() == 2 else x.reshape(1, -1)
+        d = _need_cuda(packed, perm, x2, y, workspace)
+        dev = d if dev is None else dev
+        if d != dev:
+            raise ValueError("all tensors must be on the same device")
+        if x2.dtype != torch.bfloat16 or x2.shape[1] != layout.k:
+            raise ValueError("x must be bf16 [m][k]")
+        if m is None:
+            m = x2.shape[0]
+        elif x2.shape[0] != m:
+            raise ValueError("every item of a batch has the same m")
+        if perm is not None and (perm.dtype != torch.int32 or perm.numel() != layout.k):
+            raise ValueError("perm must be int32 [k]")
+        if y is None:
+            y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
+        arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y))
+        keep.append(x2)
+        ys.append(y)
+    need = int(lib().polyq_gemm_batch_workspace_bytes(arr, len(items), m))
+    ws = workspace if workspace is not None else _workspace("gemm", need, dev, zero=False)
+    _check(lib().polyq_gemm_batch(arr, len(items), m, _ptr(ws),
+                                  0 if ws is None else ws.numel() * ws.element_size(), _stream(dev)),
+           "polyq_gemm_batch")
+    return ys

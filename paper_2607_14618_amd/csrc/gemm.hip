@@ -26,6 +26,8 @@
 // value is then the fp32 value's upper half (exact when its lower half is 0).
 #include <hip/hip_runtime.h>
 
+#include <string.h>
+
 #include <algorithm>
 
 #include "codec.h"
@@ -42,45 +44,39 @@ constexpr int kTokWG = 256;   // tokens per work-group: 4 waves of 64 along M
 constexpr int kLdsRow = 40;   // bf16 per LDS row: 32 channels + 8 pad against bank conflicts
 constexpr uint32_t kMagic2 = 0x64006400u;  // two fp16 1024.0
 
-struct GemmArgs {
+// One linear of a launch.
+struct GemmItem {
   const uint8_t* packed;
   const uint16_t* x;  // bf16 [m][k], clustered order
   float* y;           // fp32 [m][n]
-  int32_t n, k, m, nblocks, n_tiles, n_chunks, m_tiles;
+  int32_t n, k, nblocks, n_tiles, n_chunks;
   int32_t y_vec;  // rows of y can take 16-byte stores (n % 4 == 0, y 16-byte aligned)
   int32_t bits[POLYQ_MAX_BLOCKS];
   int32_t cb[POLYQ_MAX_BLOCKS];  // first chunk of each block
   int32_t ce[POLYQ_MAX_BLOCKS];  // end chunk of each block
+  int32_t pad;
   int64_t off[POLYQ_MAX_BLOCKS];
   int64_t tb[POLYQ_MAX_BLOCKS];  // bytes of one packed tile of the block
   int64_t rb[POLYQ_MAX_BLOCKS];  // bytes of one group record (meta + 4 chunks)
 };
 
-// Per-chunk facts the MFMA and dequantization stages need (32-bit, from the
-// block table in wave-uniform registers: a short chain of scalar selects).
-struct ChunkInfo {
-  int bits, cl, last;  // bit-width, chunk index in its block, ends its group
+// A launch: the linears' work-groups one after another (item i owns
+// work-groups wg_begin[i] .. wg_begin[i + 1] - 1), all with the same m.
+struct GemmBatchArgs {
+  GemmItem item[POLYQ_MAX_BATCH];
+  int32_t count, m, m_tiles, pad;
+  int32_t wg_begin[POLYQ_MAX_BATCH + 1];
 };
 
-struct BlockTable {
-  int nblocks, bits[POLYQ_MAX_BLOCKS], cb[POLYQ_MAX_BLOCKS], ce[POLYQ_MAX_BLOCKS];
+// Position of a pipeline stage in the chunk sequence: chunk c, chunk cl of
+// block bi (bit-width bits, ending at chunk ce).  Advanced one chunk at a
+// time; the block table is read (from the kernel arguments) only when a block
+// ends.
+struct ChunkCursor {
+  int c, bi, bits, cl, ce;
+  __device__ __forceinline__ bool first() const { return (cl & 3) == 0; }
+  __device__ __forceinline__ bool last() const { return (cl & 3) == 3 || c + 1 == ce; }
 };
-
-__device__ __forceinline__ ChunkInfo chunk_info(const BlockTable& t, int c) {
-  int bits = t.bits[0], cb = t.cb[0], ce = t.ce[0];
-#pragma unroll
-  for (int j = 1; j < POLYQ_MAX_BLOCKS; ++j) {
-    const bool in = j < t.nblocks && c >= t.ce[j - 1];
-    bits = in ? t.bits[j] : bits;
-    cb = in ? t.cb[j] : cb;
-    ce = in ? t.ce[j] : ce;
-  }
-  ChunkInfo p;
-  p.bits = bits;
-  p.cl = c - cb;
-  p.last = ((p.cl & 3) == 3 || c + 1 == ce) ? 1 : 0;
-  return p;
-}
 
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
@@ -177,7 +173,7 @@ __device__ __forceinline__ int sub_offset(int b, int r) {
 }
 
 template <int TN>
-__global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
+__global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
   constexpr int kThreads = 256 * TN, kRows = 64 * TN;
   constexpr int kAPieces = 4 / TN;  // 16-byte activation pieces per thread per chunk
   __shared__ __attribute__((aligned(16))) uint16_t lds_a[2][kTokWG * kLdsRow];
@@ -190,37 +186,44 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
   const int tq = wv & 3, rt = wv >> 2;  // MFMA role: token quarter, packed tile
   // Token tile fastest: neighbouring work-groups (on different XCDs) share the
   // weight rows, and each XCD's work-groups keep to a subset of token tiles.
-  const int mt = static_cast<int>(blockIdx.x) % a.m_tiles, rp = static_cast<int>(blockIdx.x) / a.m_tiles;
-  const int m0 = mt * kTokWG;
-  const int C = a.n_chunks;
-  BlockTable bt;
-  bt.nblocks = a.nblocks;
+  int idx = 0;
 #pragma unroll
-  for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) {
-    bt.bits[i] = a.bits[i];
-    bt.cb[i] = a.cb[i];
-    bt.ce[i] = a.ce[i];
-  }
+  for (int i = 1; i < POLYQ_MAX_BATCH; ++i) idx += (i < a.count && static_cast<int>(blockIdx.x) >= a.wg_begin[i]) ? 1 : 0;
+  const GemmItem& it = a.item[idx];
+  const int local = static_cast<int>(blockIdx.x) - a.wg_begin[idx];
+  const int mt = local % a.m_tiles, rp = local / a.m_tiles;
+  const int m0 = mt * kTokWG;
+  const int C = it.n_chunks;
+  auto cursor_at0 = [&]() { return ChunkCursor{0, 0, it.bits[0], 0, it.ce[0]}; };
+  auto advance = [&](ChunkCursor& u) {
+    ++u.c;
+    ++u.cl;
+    if (u.c == u.ce && u.c < C) {
+      ++u.bi;
+      u.bits = it.bits[u.bi];
+      u.ce = it.ce[u.bi];
+      u.cl = 0;
+    }
+  };
 
   // Dequantization role: packed tile dt, row sub-tile dr (wave-uniform), lane
   // slice lane; row drow of the tile.
   const int dp = wv >> 2, dr = wv & 3;
   const int dt = rp * TN + dp;
-  const bool dtile_ok = dt < a.n_tiles;
+  const bool dtile_ok = dt < it.n_tiles;
   const int drow = 16 * dr + (lane & 15);
   const int bofs = (dp * 64 + drow) * kLdsRow + 8 * (lane >> 4);
-  const bool s_writer = lane < 16;  // one thread per row writes the row's scale
   constexpr int kHalfB = kRows * kLdsRow;
 
   // Activations: buffer over rows m0 .. m0 + 255 of x' (reads past row m - 1
   // return zero); piece j of this thread is token piece/4, 16-byte segment piece%4.
   const __amdgpu_buffer_rsrc_t xrs =
-      make_rsrc(a.x + static_cast<int64_t>(m0) * a.k, static_cast<uint32_t>(min(a.m - m0, kTokWG)) * a.k * 2u);
+      make_rsrc(it.x + static_cast<int64_t>(m0) * it.k, static_cast<uint32_t>(min(a.m - m0, kTokWG)) * it.k * 2u);
   uint32_t avoff[kAPieces];
 #pragma unroll
   for (int j = 0; j < kAPieces; ++j) {
     const int piece = tid + j * kThreads;
-    avoff[j] = (static_cast<uint32_t>(piece >> 2) * a.k + (piece & 3) * 8) * 2u;
+    avoff[j] = (static_cast<uint32_t>(piece >> 2) * it.k + (piece & 3) * 8) * 2u;
   }
 
   // Load cursor: the next chunk to fetch, its block and a buffer over this
@@ -231,11 +234,11 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
   __amdgpu_buffer_rsrc_t wrs;
   auto set_block = [&](int b) {
     lb = b;
-    lbits = a.bits[b];
-    lce = a.ce[b];
-    lrb = static_cast<int>(a.rb[b]);
-    const int64_t tb = a.tb[b];
-    wrs = make_rsrc(a.packed + a.off[b] + static_cast<int64_t>(dtile_ok ? dt : 0) * tb,
+    lbits = it.bits[b];
+    lce = it.ce[b];
+    lrb = static_cast<int>(it.rb[b]);
+    const int64_t tb = it.tb[b];
+    wrs = make_rsrc(it.packed + it.off[b] + static_cast<int64_t>(dtile_ok ? dt : 0) * tb,
                     dtile_ok ? static_cast<uint32_t>(tb) : 0u);
     lvoff = static_cast<uint32_t>(lane * 4 * lbits + sub_offset(lbits, dr));
     lcl = 0;
@@ -255,13 +258,12 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
     if (lc == lce && lc < C) set_block(lb + 1);
   };
 
-  auto store = [&](int c, const Pre<TN>& pr, int st) {
+  auto store = [&](const ChunkCursor& ci, const Pre<TN>& pr, int st) {
 #pragma unroll
     for (int j = 0; j < kAPieces; ++j) {
       const int piece = tid + j * kThreads;
       *reinterpret_cast<u4v*>(&lds_a[st][(piece >> 2) * kLdsRow + (piece & 3) * 8]) = pr.av[j];
     }
-    const ChunkInfo ci = chunk_info(bt, c);
     uint16_t* hi = &lds_b[st][0][bofs];
     uint16_t* lo = hi + kHalfB;
     float v[8];
@@ -273,12 +275,12 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
         v[2 * i] = static_cast<float>(h.x);
         v[2 * i + 1] = static_cast<float>(h.y);
       }
-      if (s_writer) lds_s[st][dp * 64 + drow] = 1.f;
+      lds_s[st][dp * 64 + drow] = 1.f;  // the four threads of a row store the same value
       store_pair(v, hi, lo);
       return;
     }
     const float zf = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.z)));
-    if (s_writer) lds_s[st][dp * 64 + drow] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s)));
+    lds_s[st][dp * 64 + drow] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s)));
     uint32_t hp[4];
     switch (ci.bits) {
       case 2: sub_tile_pairs<2>(pr.w, dr, hp); break;
@@ -295,12 +297,12 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
       v[2 * j] = static_cast<float>(h.x) - zoff;
       v[2 * j + 1] = static_cast<float>(h.y) - zoff;
     }
-    if (zf == truncf(zf) && zf >= 0.f && zf <= 255.f) {
+    if (__all(zf == truncf(zf) && zf >= 0.f && zf <= 255.f)) {  // wave-uniform
       store_exact(v, hi);
       *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
     } else {
       store_pair(v, hi, lo);
-      lds_tag[st] = c + 1;  // any thread; every writer stores the same value
+      lds_tag[st] = ci.c + 1;  // any thread; every writer stores the same value
     }
   };
 
@@ -312,19 +314,20 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
 
   const int aofs = (tq * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
   const int bofs_m = (rt * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
-  // Chunk c: multiply stage c&1, dequantize chunk c+1 from `slot` into the
-  // other stage, fetch chunk c+3 into `slot`, fold a finished group.
-  auto step = [&](int c, Pre<TN>& slot) {
-    const int st = c & 1;
-    const ChunkInfo ci = chunk_info(bt, c);
-    const bool two = ci.bits == 16 || lds_tag[st] == c + 1;
+  // Chunk mc.c: multiply stage c&1, dequantize chunk c+1 (cursor sc) from
+  // `slot` into the other stage, fetch chunk c+3 into `slot`, fold a finished
+  // group.
+  ChunkCursor mc = cursor_at0(), sc = cursor_at0();
+  auto step = [&](Pre<TN>& slot) {
+    const int c = mc.c, st = c & 1;
+    const bool two = mc.bits == 16 || lds_tag[st] == c + 1;
     bf16x8 af[4], bfr[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       af[i] = *reinterpret_cast<const bf16x8*>(&lds_b[st][0][bofs_m + i * 16 * kLdsRow]);
       bfr[i] = *reinterpret_cast<const bf16x8*>(&lds_a[st][aofs + i * 16 * kLdsRow]);
     }
-    if ((ci.cl & 3) == 0) {  // first chunk of a group: fresh partial sums
+    if (mc.first()) {  // first chunk of a group: fresh partial sums
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -345,9 +348,12 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) part[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], part[i][j], 0, 0, 0);
     }
-    if (c + 1 < C) store(c + 1, slot, st ^ 1);
+    if (c + 1 < C) {
+      advance(sc);
+      store(sc, slot, st ^ 1);
+    }
     if (c + 3 < C) load(slot);
-    if (ci.last) {  // group fold: total += s * part, s of rows 16 i + 4 (lane/16) + e
+    if (mc.last()) {  // group fold: total += s * part, s of rows 16 i + 4 (lane/16) + e
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const f4 sv = *reinterpret_cast<const f4*>(&lds_s[st][rt * 64 + 16 * i + 4 * (lane >> 4)]);
@@ -357,6 +363,7 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
           for (int e = 0; e < 4; ++e) total[i][j][e] = fmaf(sv[e], part[i][j][e], total[i][j][e]);
       }
     }
+    advance(mc);
     __syncthreads();
   };
 
@@ -366,15 +373,15 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
   load(s0);
   if (C > 1) load(s1);
   __syncthreads();
-  store(0, s0, 0);
+  store(sc, s0, 0);
   if (C > 2) load(s0);
   __syncthreads();
   int c = 0;
   for (; c + 1 < C; c += 2) {
-    step(c, s1);
-    step(c + 1, s0);
+    step(s1);
+    step(s0);
   }
-  if (c < C) step(c, s1);
+  if (c < C) step(s1);
 
   // D layout: lane holds weight rows 16 i + 4 (lane/16) + e of token 16 j + lane%16.
   const int row0 = (rp * TN + rt) * kTileRows + 4 * (lane >> 4);
@@ -382,16 +389,16 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmArgs a) {
   for (int j = 0; j < 4; ++j) {
     const int tok = m0 + tq * 64 + 16 * j + (lane & 15);
     if (tok >= a.m) continue;
-    float* yr = a.y + static_cast<int64_t>(tok) * a.n;
+    float* yr = it.y + static_cast<int64_t>(tok) * it.n;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = row0 + 16 * i;
-      if (a.y_vec && row + 3 < a.n) {
+      if (it.y_vec && row + 3 < it.n) {
         *reinterpret_cast<f4*>(yr + row) = total[i][j];
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (row + e < a.n) yr[row + e] = total[i][j][e];
+          if (row + e < it.n) yr[row + e] = total[i][j][e];
       }
     }
   }
@@ -434,80 +441,149 @@ __global__ __launch_bounds__(256) void permute_rows_kernel(const int32_t* __rest
   out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
 }
 
-// Work-groups of a launch with TN packed tiles per work-group.
-int64_t gemm_groups(const polyq_layout& L, int32_t m, int tn) {
-  return static_cast<int64_t>((L.n_tiles + tn - 1) / tn) * ((m + kTokWG - 1) / kTokWG);
-}
-
 }  // namespace
 }  // namespace polyq
 
 using namespace polyq;
 
+namespace {
+
+size_t permuted_bytes(const polyq_layout& L, int32_t m) {
+  return static_cast<size_t>(align_up(static_cast<int64_t>(m) * L.k * 2, 256));
+}
+
+// Workspace regions of a batch: one permuted copy per distinct (x, perm) pair
+// with perm != NULL.  region[i] is the byte offset of item i's copy (or -1).
+polyq_status plan_gemm_batch(const polyq_gemv_item* items, int32_t count, int32_t m,
+                             int64_t* region, size_t* total) {
+  if (items == nullptr || count < 1 || m < 1) return POLYQ_ERR_ARG;
+  if (count > POLYQ_MAX_BATCH) return POLYQ_ERR_CAPACITY;
+  size_t off = 0;
+  for (int i = 0; i < count; ++i) {
+    if (!layout_is_valid(items[i].layout)) return POLYQ_ERR_ARG;
+    if (static_cast<int64_t>(m) * items[i].layout->k * 2 > 0x7FFFFFFFll) return POLYQ_ERR_CAPACITY;
+    region[i] = -1;
+    if (items[i].perm == nullptr) continue;
+    for (int j = 0; j < i; ++j)
+      if (items[j].perm == items[i].perm && items[j].x == items[i].x &&
+          items[j].layout->k == items[i].layout->k) {
+        region[i] = region[j];
+        break;
+      }
+    if (region[i] < 0) {
+      region[i] = static_cast<int64_t>(off);
+      off += permuted_bytes(*items[i].layout, m);
+    }
+  }
+  *total = off;
+  return POLYQ_OK;
+}
+
+}  // namespace
+
+extern "C" size_t polyq_gemm_batch_workspace_bytes(const polyq_gemm_item* items, int32_t count,
+                                                   int32_t m) {
+  int64_t region[POLYQ_MAX_BATCH];
+  size_t total = 0;
+  if (plan_gemm_batch(items, count, m, region, &total) != POLYQ_OK) return 0;
+  return total;
+}
+
 extern "C" size_t polyq_gemm_workspace_bytes(const polyq_layout* layout, int32_t m, int perm_given) {
   if (!layout_is_valid(layout) || m < 1) return 0;
   if (!perm_given) return 0;
-  return static_cast<size_t>(align_up(static_cast<int64_t>(m) * layout->k * 2, 256));
+  return permuted_bytes(*layout, m);
+}
+
+extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t count, int32_t m,
+                                         void* workspace, size_t workspace_bytes, void* stream) {
+  int64_t region[POLYQ_MAX_BATCH];
+  size_t need = 0;
+  const polyq_status pst = plan_gemm_batch(items, count, m, region, &need);
+  if (pst != POLYQ_OK) return pst;
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return POLYQ_ERR_CAPACITY;
+  if (need > 0 && reinterpret_cast<uintptr_t>(workspace) % 16 != 0) return POLYQ_ERR_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  GemmBatchArgs a;
+  memset(&a, 0, sizeof(a));
+  a.count = count;
+  a.m = m;
+  a.m_tiles = (m + kTokWG - 1) / kTokWG;
+  int64_t tiles1 = 0;
+  for (int i = 0; i < count; ++i) {
+    const polyq_gemv_item& itm = items[i];
+    const polyq_layout& L = *itm.layout;
+    if (itm.packed == nullptr || itm.x == nullptr || itm.y == nullptr) return POLYQ_ERR_ARG;
+    if (reinterpret_cast<uintptr_t>(itm.packed) % 256 != 0 || reinterpret_cast<uintptr_t>(itm.y) % 4 != 0)
+      return POLYQ_ERR_ARG;
+    if (L.packed_bytes > 0x7FFFFFFFll) return POLYQ_ERR_CAPACITY;
+    tiles1 += L.n_tiles;
+  }
+  // Permuted copies (one per distinct (x, perm)), then the products.
+  for (int i = 0; i < count; ++i) {
+    const polyq_gemv_item& itm = items[i];
+    const polyq_layout& L = *itm.layout;
+    const uint16_t* xp = itm.x;
+    if (itm.perm != nullptr) {
+      uint16_t* out = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(workspace) + region[i]);
+      bool first = true;
+      for (int j = 0; j < i; ++j) first = first && region[j] != region[i];
+      if (first) {
+        if (L.k <= kPermLdsK && reinterpret_cast<uintptr_t>(itm.x) % 16 == 0 &&
+            reinterpret_cast<uintptr_t>(itm.perm) % 16 == 0) {
+          hipLaunchKernelGGL(permute_rows_lds_kernel, dim3(static_cast<unsigned>(m)), dim3(256),
+                             static_cast<size_t>(L.k) * 2, st, itm.perm, itm.x, out, L.k);
+        } else {
+          const int64_t n_el = static_cast<int64_t>(m) * L.k;
+          hipLaunchKernelGGL(permute_rows_kernel, dim3(static_cast<unsigned>((n_el + 255) / 256)),
+                             dim3(256), 0, st, itm.perm, itm.x, out, m, L.k);
+        }
+      }
+      xp = out;
+    } else if (reinterpret_cast<uintptr_t>(itm.x) % 16 != 0) {
+      return POLYQ_ERR_ARG;  // activations are read as 16-byte vectors
+    }
+    GemmItem& g = a.item[i];
+    g.packed = static_cast<const uint8_t*>(itm.packed);
+    g.x = xp;
+    g.y = itm.y;
+    g.n = L.n;
+    g.k = L.k;
+    g.nblocks = L.nblocks;
+    g.n_tiles = L.n_tiles;
+    g.n_chunks = L.n_chunks;
+    g.y_vec = (L.n % 4 == 0 && reinterpret_cast<uintptr_t>(itm.y) % 16 == 0) ? 1 : 0;
+    for (int b = 0; b < POLYQ_MAX_BLOCKS; ++b) {
+      const bool used = b < L.nblocks;
+      g.bits[b] = used ? L.block[b].bits : 16;
+      g.cb[b] = used ? L.k_begin[b] / kChunk : L.n_chunks;
+      g.ce[b] = used ? (L.k_begin[b] + L.block[b].len) / kChunk : L.n_chunks;
+      g.off[b] = used ? L.block_offset[b] : 0;
+      g.tb[b] = used ? L.tile_bytes[b] : 0;
+      g.rb[b] = used ? L.record_bytes[b] : 0;
+    }
+  }
+  // One packed tile per work-group (two co-resident work-groups per CU with
+  // independent barriers), or two when there are work-groups to spare.
+  const bool wide = tiles1 * a.m_tiles > 1024;
+  const int tn = wide ? 2 : 1;
+  int64_t wg = 0;
+  for (int i = 0; i < count; ++i) {
+    a.wg_begin[i] = static_cast<int32_t>(wg);
+    wg += static_cast<int64_t>((items[i].layout->n_tiles + tn - 1) / tn) * a.m_tiles;
+    if (wg > 0x7FFFFFFF) return POLYQ_ERR_CAPACITY;
+  }
+  for (int i = count; i <= POLYQ_MAX_BATCH; ++i) a.wg_begin[i] = static_cast<int32_t>(wg);
+  if (wide)
+    hipLaunchKernelGGL(gemm_kernel<2>, dim3(static_cast<unsigned>(wg)), dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL(gemm_kernel<1>, dim3(static_cast<unsigned>(wg)), dim3(256), 0, st, a);
+  return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
 }
 
 extern "C" polyq_status polyq_gemm(const polyq_layout* layout, const void* packed,
                                    const int32_t* perm, const uint16_t* x, int32_t m, float* y,
                                    void* workspace, size_t workspace_bytes, void* stream) {
-  if (!layout_is_valid(layout)) return POLYQ_ERR_ARG;
-  const polyq_layout& L = *layout;
-  if (packed == nullptr || x == nullptr || y == nullptr || m < 1) return POLYQ_ERR_ARG;
-  if (reinterpret_cast<uintptr_t>(packed) % 256 != 0 || reinterpret_cast<uintptr_t>(y) % 4 != 0)
-    return POLYQ_ERR_ARG;
-  if (static_cast<int64_t>(m) * L.k > (static_cast<int64_t>(1) << 40)) return POLYQ_ERR_CAPACITY;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  const uint16_t* xp = x;
-  if (perm != nullptr) {
-    const size_t need = polyq_gemm_workspace_bytes(layout, m, 1);
-    if (workspace == nullptr || workspace_bytes < need) return POLYQ_ERR_CAPACITY;
-    if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0) return POLYQ_ERR_ARG;
-    uint16_t* out = static_cast<uint16_t*>(workspace);
-    if (L.k <= kPermLdsK && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
-        reinterpret_cast<uintptr_t>(perm) % 16 == 0) {
-      hipLaunchKernelGGL(permute_rows_lds_kernel, dim3(static_cast<unsigned>(m)), dim3(256),
-                         static_cast<size_t>(L.k) * 2, st, perm, x, out, L.k);
-    } else {
-      const int64_t items = static_cast<int64_t>(m) * L.k;
-      hipLaunchKernelGGL(permute_rows_kernel, dim3(static_cast<unsigned>((items + 255) / 256)),
-                         dim3(256), 0, st, perm, x, out, m, L.k);
-    }
-    xp = out;
-  } else if (reinterpret_cast<uintptr_t>(x) % 16 != 0) {
-    return POLYQ_ERR_ARG;  // activations are read as 16-byte vectors
-  }
-  GemmArgs a;
-  a.packed = static_cast<const uint8_t*>(packed);
-  a.x = xp;
-  a.y = y;
-  a.n = L.n;
-  a.k = L.k;
-  a.m = m;
-  a.nblocks = L.nblocks;
-  a.n_tiles = L.n_tiles;
-  a.n_chunks = L.n_chunks;
-  a.m_tiles = (m + kTokWG - 1) / kTokWG;
-  a.y_vec = (L.n % 4 == 0 && reinterpret_cast<uintptr_t>(y) % 16 == 0) ? 1 : 0;
-  for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) {
-    const bool used = i < L.nblocks;
-    a.bits[i] = used ? L.block[i].bits : 16;
-    a.cb[i] = used ? L.k_begin[i] / kChunk : L.n_chunks;
-    a.ce[i] = used ? (L.k_begin[i] + L.block[i].len) / kChunk : L.n_chunks;
-    a.off[i] = used ? L.block_offset[i] : 0;
-    a.tb[i] = used ? L.tile_bytes[i] : 0;
-    a.rb[i] = used ? L.record_bytes[i] : 0;
-  }
-  // Two packed tiles per work-group when that still gives a full round of
-  // work-groups, else one (twice as many work-groups, each half as wide).
-  const bool wide = gemm_groups(L, m, 2) >= 240;
-  const int64_t groups = gemm_groups(L, m, wide ? 2 : 1);
-  if (groups > 0x7FFFFFFF) return POLYQ_ERR_CAPACITY;
-  if (wide)
-    hipLaunchKernelGGL(gemm_kernel<2>, dim3(static_cast<unsigned>(groups)), dim3(512), 0, st, a);
-  else
-    hipLaunchKernelGGL(gemm_kernel<1>, dim3(static_cast<unsigned>(groups)), dim3(256), 0, st, a);
-  return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
+  const polyq_gemm_item item{layout, packed, perm, x, y};
+  return polyq_gemm_batch(&item, 1, m, workspace, workspace_bytes, stream);
 }

@@ -52,3 +52,14 @@ def decode_batch(linears: Sequence["PackedLinear"], xs: Sequence[torch.Tensor],
     items = [(pl.layout, pl.packed, None if pre_permuted else pl.perm, x, y)
              for pl, x, y in zip(linears, xs, ys)]
     return _lib.gemv_batch(items)
+
+
+def prefill_batch(linears: Sequence["PackedLinear"], xs: Sequence[torch.Tensor],
+                  pre_permuted: bool = False, ys: Optional[Sequence[Optional[torch.Tensor]]] = None):
+    """One polyq_gemm_batch launch over several linears (same token count): e.g.
+    the q/k/v projections of a layer, which share x and the permutation (one
+    permuted copy of x serves all of them)."""
+    ys = list(ys) if ys is not None else [None] * len(linears)
+    items = [(pl.layout, pl.packed, None if pre_permuted else pl.perm, x, y)
+             for pl, x, y in zip(linears, xs, ys)]
+    return _lib.gemm_batch(items)

@@ -95,3 +95,61 @@ def test_gemm_config3_llama2_13b_prefill():
         rows = np.sort(rng.choice(lin.n, 512, replace=False))
         y_ref, bound = oracle_ref(lin, x, rows=rows)
         assert_parity(np_(y)[:, rows], y_ref, bound, f"config 3 {lin.name}")
+
+
+def test_gemm_batch_matches_single_calls():
+    """q/k/v-like batch (shared x and permutation) equals the single-linear calls
+    bit for bit, and each item meets the oracle bound."""
+    blocks = [(2, 992), (3, 704), (4, 256), (8, 64), (16, 32)]
+    lins = [random_quant_linear(n, 2048, blocks, seed=70 + i, mode="gauss") for i, n in enumerate((320, 192, 64))]
+    perm = lins[0].perm
+    for lin in lins[1:]:
+        lin.perm = perm  # one input group: same channel permutation
+    pls = [packed_linear(lin) for lin in lins]
+    x = _xb(300, 2048, seed=5)
+    xd = x.to(dev())
+    ys = pq.prefill_batch(pls, [xd] * 3)
+    singles = [pl.prefill(xd) for pl in pls]
+    torch.cuda.synchronize()
+    for lin, y, y1 in zip(lins, ys, singles):
+        assert torch.equal(y, y1), lin.n
+        y_ref, bound = oracle_ref(lin, x)
+        assert_parity(y, y_ref, bound, f"gemm batch n={lin.n}")
+
+
+@pytest.mark.parametrize("m", [1, 77, 513])
+def test_gemm_batch_mixed_items(m):
+    """Items of different shapes and bit mixes, with and without a permutation."""
+    specs = [(100, [(2, 160), (3, 96), (4, 128), (8, 96), (16, 32)]), (257, [(4, 480), (16, 96)]),
+             (64, [(3, 32)]), (130, [(2, 992), (3, 704), (4, 256), (8, 64), (16, 32)])]
+    lins, xs = [], []
+    for i, (n, blocks) in enumerate(specs):
+        k = sum(l for _, l in blocks)
+        lin = random_quant_linear(n, k, blocks, seed=300 + i, mode="codes")
+        lins.append(lin)
+        xs.append(_xb(m, k, seed=40 + i))
+    pls = [packed_linear(lin) for lin in lins]
+    xd = [x.to(dev()) for x in xs]
+    items = []
+    for i, (pl, x) in enumerate(zip(pls, xd)):
+        if i % 2:
+            items.append((pl.layout, pl.packed, None, pl.permute(x), None))
+        else:
+            items.append((pl.layout, pl.packed, pl.perm, x, None))
+    ys = pq.gemm_batch(items)
+    torch.cuda.synchronize()
+    for lin, x, y in zip(lins, xs, ys):
+        y_ref, bound = oracle_ref(lin, x)
+        assert_parity(y, y_ref, bound, f"gemm batch mixed n={lin.n} m={m}")
+
+
+def test_gemm_batch_rejects_bad_requests():
+    lin = random_quant_linear(64, 128, [(4, 128)], seed=1, mode="codes")
+    pl = packed_linear(lin)
+    x = _xb(4, 128, seed=1).to(dev())
+    with pytest.raises(ValueError):
+        pq.gemm_batch([])
+    with pytest.raises(ValueError):
+        pq.gemm_batch([(pl.layout, pl.packed, pl.perm, x, None)] * (pq._lib.MAX_BATCH + 1))
+    with pytest.raises(ValueError):
+        pq.gemm_batch([(pl.layout, pl.packed, pl.perm, x, None), (pl.layout, pl.packed, pl.perm, x[:3], None)])
