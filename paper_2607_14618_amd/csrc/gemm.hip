@@ -565,7 +565,7 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
   }
   // One packed tile per work-group (two co-resident work-groups per CU with
   // independent barriers), or two when there are work-groups to spare.
-  const bool wide = tiles1 * a.m_tiles > 1024;
+  const bool wide = (tiles1 + count) / 2 * a.m_tiles >= 200;
   const int tn = wide ? 2 : 1;
   int64_t wg = 0;
   for (int i = 0; i < count; ++i) {
