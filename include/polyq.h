@@ -203,9 +203,12 @@ polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32
  *   x bf16 [m][k] bits, original channel order if perm != NULL, else clustered
  *   (then 16-byte aligned); m * k * 2 < 2^31.
  *   y fp32 [m][n], fully overwritten.
- *   workspace: at least polyq_gemm_workspace_bytes(layout, m) bytes of device
- *   scratch (holds the permuted activations when perm != NULL); contents on
- *   entry are ignored.
+ *   workspace: at least polyq_gemm_workspace_bytes(layout, m, perm != NULL)
+ *   bytes of device scratch (the permuted activations when perm != NULL, and
+ *   per-split partial sums when the launch splits K, which it does when the
+ *   output tiles alone would leave most compute units idle); contents on
+ *   entry are ignored.  The split sums are added in a fixed order, so results
+ *   do not depend on scheduling.
  * Computed with bf16 MFMA and fp32 accumulation: (q - z) enters as one exact
  * bf16 value when z is an integer in [0, 255], else as the bf16 pair hi + lo
  * (relative error below 2^-16); the group scale is applied in fp32; a 16-bit
@@ -223,9 +226,10 @@ polyq_status polyq_gemm(const polyq_layout* layout, const void* packed, const in
  * m, items[i].y, ...) computes, with the same argument rules per item (x holds
  * bf16 bits here).  Items with the same x and perm share one permuted copy.
  *   workspace: at least polyq_gemm_batch_workspace_bytes(items, count, m)
- *   bytes of device scratch (the permuted copies); contents on entry are
- *   ignored.  The query reads the layout, x and perm fields; 0 on an invalid
- *   request or when no item has a permutation.
+ *   bytes of device scratch (the permuted copies, and for count == 1 the
+ *   split partial sums as in polyq_gemm); contents on entry are ignored.  The
+ *   query reads the layout, x and perm fields; 0 on an invalid request or
+ *   when no scratch is needed.
  */
 typedef polyq_gemv_item polyq_gemm_item;
 

@@ -62,10 +62,17 @@ struct GemmItem {
 
 // A launch: the linears' work-groups one after another (item i owns
 // work-groups wg_begin[i] .. wg_begin[i + 1] - 1), all with the same m.
+// K is split (count == 1 only) into `splits` chunk ranges starting at group
+// boundaries (split_chunk, unused when splits == 1); split s writes its sums
+// to partial[s][m][n] and a second kernel adds the splits in order.
+constexpr int kMaxSplits = 8;
+
 struct GemmBatchArgs {
   GemmItem item[POLYQ_MAX_BATCH];
-  int32_t count, m, m_tiles, pad;
+  int32_t count, m, m_tiles, splits;
   int32_t wg_begin[POLYQ_MAX_BATCH + 1];
+  int32_t split_chunk[kMaxSplits + 1];
+  float* partial;
 };
 
 // Position of a pipeline stage in the chunk sequence: chunk c, chunk cl of
@@ -191,10 +198,16 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
   for (int i = 1; i < POLYQ_MAX_BATCH; ++i) idx += (i < a.count && static_cast<int>(blockIdx.x) >= a.wg_begin[i]) ? 1 : 0;
   const GemmItem& it = a.item[idx];
   const int local = static_cast<int>(blockIdx.x) - a.wg_begin[idx];
-  const int mt = local % a.m_tiles, rp = local / a.m_tiles;
+  const int mt = local % a.m_tiles, rest = local / a.m_tiles;
+  const int ks = rest % a.splits, rp = rest / a.splits;
   const int m0 = mt * kTokWG;
-  const int C = it.n_chunks;
-  auto cursor_at0 = [&]() { return ChunkCursor{0, 0, it.bits[0], 0, it.ce[0]}; };
+  // this work-group's chunks [c0, C)
+  const int c0 = a.splits > 1 ? a.split_chunk[ks] : 0;
+  const int C = a.splits > 1 ? a.split_chunk[ks + 1] : it.n_chunks;
+  int b0 = 0;
+#pragma unroll
+  for (int j = 0; j < POLYQ_MAX_BLOCKS - 1; ++j) b0 += (j + 1 < it.nblocks && c0 >= it.ce[j]) ? 1 : 0;
+  auto cursor_at0 = [&]() { return ChunkCursor{c0, b0, it.bits[b0], c0 - it.cb[b0], it.ce[b0]}; };
   auto advance = [&](ChunkCursor& u) {
     ++u.c;
     ++u.cl;
@@ -229,7 +242,7 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
   // Load cursor: the next chunk to fetch, its block and a buffer over this
   // thread's packed tile of that block (no records for a tile past the end,
   // so its reads return zero).
-  int lc = 0, lb = 0, lcl = 0, lbits = 0, lce = 0, lrb = 0;
+  int lc = c0, lb = 0, lcl = 0, lbits = 0, lce = 0, lrb = 0;
   uint32_t lvoff = 0;
   __amdgpu_buffer_rsrc_t wrs;
   auto set_block = [&](int b) {
@@ -319,7 +332,7 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
   // group.
   ChunkCursor mc = cursor_at0(), sc = cursor_at0();
   auto step = [&](Pre<TN>& slot) {
-    const int c = mc.c, st = c & 1;
+    const int c = mc.c, st = (c - c0) & 1;
     const bool two = mc.bits == 16 || lds_tag[st] == c + 1;
     bf16x8 af[4], bfr[4];
 #pragma unroll
@@ -369,14 +382,15 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
 
   Pre<TN> s0, s1;
   if (tid < 2) lds_tag[tid] = 0;
-  set_block(0);
+  set_block(b0);
+  lcl = c0 - it.cb[b0];
   load(s0);
-  if (C > 1) load(s1);
+  if (C - c0 > 1) load(s1);
   __syncthreads();
   store(sc, s0, 0);
-  if (C > 2) load(s0);
+  if (C - c0 > 2) load(s0);
   __syncthreads();
-  int c = 0;
+  int c = c0;
   for (; c + 1 < C; c += 2) {
     step(s1);
     step(s0);
@@ -389,11 +403,13 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
   for (int j = 0; j < 4; ++j) {
     const int tok = m0 + tq * 64 + 16 * j + (lane & 15);
     if (tok >= a.m) continue;
-    float* yr = it.y + static_cast<int64_t>(tok) * it.n;
+    float* yr = a.splits > 1 ? a.partial + (static_cast<int64_t>(ks) * a.m + tok) * it.n
+                             : it.y + static_cast<int64_t>(tok) * it.n;
+    const bool vec = a.splits > 1 ? (it.n & 3) == 0 : it.y_vec != 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = row0 + 16 * i;
-      if (it.y_vec && row + 3 < it.n) {
+      if (vec && row + 3 < it.n) {
         *reinterpret_cast<f4*>(yr + row) = total[i][j];
       } else {
 #pragma unroll
@@ -441,6 +457,17 @@ __global__ __launch_bounds__(256) void permute_rows_kernel(const int32_t* __rest
   out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
 }
 
+// y = partial[0] + partial[1] + ... (in split order), `count` elements each.
+__global__ __launch_bounds__(256) void sum_splits_kernel(const float* __restrict__ partial,
+                                                         float* __restrict__ y, int splits,
+                                                         int64_t count) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= count) return;
+  float v = partial[i];
+  for (int s = 1; s < splits; ++s) v += partial[s * count + i];
+  y[i] = v;
+}
+
 }  // namespace
 }  // namespace polyq
 
@@ -452,10 +479,28 @@ size_t permuted_bytes(const polyq_layout& L, int32_t m) {
   return static_cast<size_t>(align_up(static_cast<int64_t>(m) * L.k * 2, 256));
 }
 
-// Workspace regions of a batch: one permuted copy per distinct (x, perm) pair
-// with perm != NULL.  region[i] is the byte offset of item i's copy (or -1).
+// Work-groups of one linear with TN packed tiles per work-group.
+int64_t tile_groups(const polyq_layout& L, int32_t m, int tn) {
+  return static_cast<int64_t>((L.n_tiles + tn - 1) / tn) * ((m + kTokWG - 1) / kTokWG);
+}
+
+// K splits of a single-linear launch: enough work-groups for two per CU
+// (about 480), at least four groups per split, at most kMaxSplits.
+int plan_splits(const polyq_layout& L, int32_t m, int32_t count) {
+  if (count != 1) return 1;
+  const int64_t wg = tile_groups(L, m, 1);
+  if (wg >= 240) return 1;
+  int groups = 0;
+  for (int i = 0; i < L.nblocks; ++i) groups += (L.block[i].len / kChunk + kChunksPerGroup - 1) / kChunksPerGroup;
+  const int64_t want = (480 + wg - 1) / wg;
+  return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({want, kMaxSplits, groups / 4})));
+}
+
+// Workspace of a batch: one permuted copy per distinct (x, perm) pair with
+// perm != NULL (region[i] = byte offset of item i's copy, or -1), then the
+// split partial sums of a single-linear launch (at *partial_off).
 polyq_status plan_gemm_batch(const polyq_gemv_item* items, int32_t count, int32_t m,
-                             int64_t* region, size_t* total) {
+                             int64_t* region, size_t* partial_off, int* splits, size_t* total) {
   if (items == nullptr || count < 1 || m < 1) return POLYQ_ERR_ARG;
   if (count > POLYQ_MAX_BATCH) return POLYQ_ERR_CAPACITY;
   size_t off = 0;
@@ -475,6 +520,10 @@ polyq_status plan_gemm_batch(const polyq_gemv_item* items, int32_t count, int32_
       off += permuted_bytes(*items[i].layout, m);
     }
   }
+  *splits = plan_splits(*items[0].layout, m, count);
+  *partial_off = off;
+  if (*splits > 1)
+    off += static_cast<size_t>(align_up(static_cast<int64_t>(*splits) * m * items[0].layout->n * 4, 256));
   *total = off;
   return POLYQ_OK;
 }
@@ -484,22 +533,25 @@ polyq_status plan_gemm_batch(const polyq_gemv_item* items, int32_t count, int32_
 extern "C" size_t polyq_gemm_batch_workspace_bytes(const polyq_gemm_item* items, int32_t count,
                                                    int32_t m) {
   int64_t region[POLYQ_MAX_BATCH];
-  size_t total = 0;
-  if (plan_gemm_batch(items, count, m, region, &total) != POLYQ_OK) return 0;
+  size_t partial_off = 0, total = 0;
+  int splits = 1;
+  if (plan_gemm_batch(items, count, m, region, &partial_off, &splits, &total) != POLYQ_OK) return 0;
   return total;
 }
 
 extern "C" size_t polyq_gemm_workspace_bytes(const polyq_layout* layout, int32_t m, int perm_given) {
   if (!layout_is_valid(layout) || m < 1) return 0;
-  if (!perm_given) return 0;
-  return permuted_bytes(*layout, m);
+  const int32_t dummy = 0;
+  const polyq_gemm_item item{layout, nullptr, perm_given ? &dummy : nullptr, nullptr, nullptr};
+  return polyq_gemm_batch_workspace_bytes(&item, 1, m);
 }
 
 extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t count, int32_t m,
                                          void* workspace, size_t workspace_bytes, void* stream) {
   int64_t region[POLYQ_MAX_BATCH];
-  size_t need = 0;
-  const polyq_status pst = plan_gemm_batch(items, count, m, region, &need);
+  size_t need = 0, partial_off = 0;
+  int splits = 1;
+  const polyq_status pst = plan_gemm_batch(items, count, m, region, &partial_off, &splits, &need);
   if (pst != POLYQ_OK) return pst;
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return POLYQ_ERR_CAPACITY;
   if (need > 0 && reinterpret_cast<uintptr_t>(workspace) % 16 != 0) return POLYQ_ERR_ARG;
@@ -508,6 +560,7 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
   memset(&a, 0, sizeof(a));
   a.count = count;
   a.m = m;
+  a.splits = splits;
   a.m_tiles = (m + kTokWG - 1) / kTokWG;
   int64_t tiles1 = 0;
   for (int i = 0; i < count; ++i) {
@@ -564,20 +617,39 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
     }
   }
   // One packed tile per work-group (two co-resident work-groups per CU with
-  // independent barriers), or two when there are work-groups to spare.
-  const bool wide = (tiles1 + count) / 2 * a.m_tiles >= 200;
+  // independent barriers), or two when that still gives 200+ work-groups.
+  const bool wide = splits == 1 && (tiles1 + count) / 2 * a.m_tiles >= 200;
   const int tn = wide ? 2 : 1;
   int64_t wg = 0;
   for (int i = 0; i < count; ++i) {
     a.wg_begin[i] = static_cast<int32_t>(wg);
-    wg += static_cast<int64_t>((items[i].layout->n_tiles + tn - 1) / tn) * a.m_tiles;
+    wg += static_cast<int64_t>((items[i].layout->n_tiles + tn - 1) / tn) * a.m_tiles * splits;
     if (wg > 0x7FFFFFFF) return POLYQ_ERR_CAPACITY;
   }
   for (int i = count; i <= POLYQ_MAX_BATCH; ++i) a.wg_begin[i] = static_cast<int32_t>(wg);
+  // split s covers groups [G s / S, G (s + 1) / S) of the group sequence
+  {
+    const polyq_layout& L = *items[0].layout;
+    int gstart[POLYQ_MAX_K / POLYQ_GROUP + POLYQ_MAX_BLOCKS];
+    int G = 0;
+    if (splits > 1)
+      for (int b = 0; b < L.nblocks; ++b)
+        for (int c = L.k_begin[b] / kChunk; c < (L.k_begin[b] + L.block[b].len) / kChunk; c += kChunksPerGroup)
+          gstart[G++] = c;
+    for (int sp = 0; sp <= kMaxSplits; ++sp)
+      a.split_chunk[sp] = splits == 1 ? (sp == 0 ? 0 : L.n_chunks)
+                                      : (sp >= splits ? L.n_chunks : gstart[static_cast<int64_t>(G) * sp / splits]);
+    a.partial = splits > 1 ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + partial_off) : nullptr;
+  }
   if (wide)
     hipLaunchKernelGGL(gemm_kernel<2>, dim3(static_cast<unsigned>(wg)), dim3(512), 0, st, a);
   else
     hipLaunchKernelGGL(gemm_kernel<1>, dim3(static_cast<unsigned>(wg)), dim3(256), 0, st, a);
+  if (splits > 1) {
+    const int64_t n_el = static_cast<int64_t>(m) * items[0].layout->n;
+    hipLaunchKernelGGL(sum_splits_kernel, dim3(static_cast<unsigned>((n_el + 255) / 256)), dim3(256), 0, st,
+                       a.partial, items[0].y, splits, n_el);
+  }
   return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
 }
 

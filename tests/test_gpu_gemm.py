@@ -98,8 +98,8 @@ def test_gemm_config3_llama2_13b_prefill():
 
 
 def test_gemm_batch_matches_single_calls():
-    """q/k/v-like batch (shared x and permutation) equals the single-linear calls
-    bit for bit, and each item meets the oracle bound."""
+    """q/k/v-like batch (shared x and permutation) and the single-linear calls
+    (which may split K and add the splits in order) both meet the oracle bound."""
     blocks = [(2, 992), (3, 704), (4, 256), (8, 64), (16, 32)]
     lins = [random_quant_linear(n, 2048, blocks, seed=70 + i, mode="gauss") for i, n in enumerate((320, 192, 64))]
     perm = lins[0].perm
@@ -112,9 +112,9 @@ def test_gemm_batch_matches_single_calls():
     singles = [pl.prefill(xd) for pl in pls]
     torch.cuda.synchronize()
     for lin, y, y1 in zip(lins, ys, singles):
-        assert torch.equal(y, y1), lin.n
         y_ref, bound = oracle_ref(lin, x)
         assert_parity(y, y_ref, bound, f"gemm batch n={lin.n}")
+        assert_parity(y1, y_ref, bound, f"gemm single n={lin.n}")
 
 
 @pytest.mark.parametrize("m", [1, 77, 513])
