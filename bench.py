@@ -157,7 +157,12 @@ SHARED_INPUT = (("q_proj", "k_proj", "v_proj"), ("o_proj",), ("gate_proj", "up_p
 
 
 def schedule(layer, grouped):
-    """Launches of one layer step: lists of linear indices."""
+    """Launches of one layer step: lists of linear indices.  grouped: True (one
+    launch per shared-input group), False (one per linear) or "one" (every
+    linear in a single launch: a kernel capability figure, not a realizable
+    decode step, since o, gate/up and down consume earlier outputs)."""
+    if grouped == "one":
+        return [list(range(len(layer)))]
     if not grouped:
         return [[j] for j in range(len(layer))]
     names = [nm for nm, _, _ in layer]
@@ -322,6 +327,13 @@ def main_default(a, torch, pq, synth):
                      "avg_launch_us": round(avg_launch_ms * 1e3, 3),
                      "per_launch_evented": d["per_launch"]},
     }
+    one = decode_figure(torch, pq, synth, max(20, a.steps // 2), a.warmup, a.variant, grouped="one")
+    _log(f"decode, all 7 linears in one launch: {one['ms_step'] * 1e3:.1f} us/step, {one['gbs']:.1f} GB/s")
+    extra["one_launch"] = {
+        "note": "all seven linears in one polyq_gemv_batch launch: the kernel's rate without the "
+                "four-launch dependency chain of a real decode step (not the headline value)",
+        "us_per_step": round(one["ms_step"] * 1e3, 2), "gbs": round(one["gbs"], 1),
+        "pct_hbm_peak": round(100 * one["gbs"] / HBM_PEAK_GBS, 2)}
     if not a.no_prefill:
         _log("prefill GEMM, M=512")
         extra["prefill"] = prefill_figure(torch, pq, synth, 10, 3, grouped=not a.per_linear)
