@@ -420,6 +420,312 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wide-wave variant: a work-group of 4 waves owns 256 tokens x 128 rows (two
+// packed tiles) and each wave 128 tokens x 64 rows, so a chunk costs a wave 32
+// MFMAs against the same per-chunk bookkeeping.  To fit 128 accumulators per
+// lane the group fold is replaced by a running rescale: the accumulator T of
+// a row is kept in units of the current group's scale s_g (T = sum over
+// earlier groups of s_g' P_g' / s_g); at a group's first chunk T is multiplied
+// by s_{g-1} / s_g, the group's integer products (q - z) x are added by the
+// MFMAs, and the output is T * s_last.  Each rescale rounds once (relative
+// error below 2^-23 per group); a scale of 0 is treated as 1 with the row's
+// dequantized values set to 0, so its products vanish exactly.  The activation
+// tile is stored without padding, its 16-byte segments permuted per token
+// (seg ^ swz(token)) so that both the stores and the fragment reads are free
+// of bank conflicts.
+
+__device__ __forceinline__ int swz(int t) { return ((t >> 1) ^ (t >> 3)) & 3; }
+
+// Prefetched data of one chunk for one thread of the wide kernel.
+struct PreW {
+  u4v av[4];    // activation pieces
+  u4v w0, w1;   // packed words of the thread's two row sub-tiles (w1: 16-bit only)
+  uint32_t z2;  // fp16 zero points of the two rows (low, high half)
+  uint32_t s0, s1;  // fp16 scales of the two rows
+};
+
+// The 4 code pairs of row sub-tile r from the 16 bytes `w` that hold it (the
+// word(s) loaded at sub_offset(b, r) of the slice, or the whole 3-bit slice).
+template <int B>
+__device__ __forceinline__ void pairs_at(const u4v w, int r, int second, uint32_t* hp) {
+  if constexpr (B == 2) {  // sub-tiles 2k and 2k+1 share word k (w.x)
+    const int sh = 8 * second;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) hp[j] = pair_magic(w.x, sh + 2 * j, 0x00030003u);
+  } else if constexpr (B == 4) {  // word r (w.x for the first, w.y for the second)
+    const uint32_t wd = second ? w.y : w.x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) hp[j] = pair_magic(wd, 4 * j, 0x000F000Fu);
+  } else if constexpr (B == 8) {  // words 2r, 2r+1
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      hp[j] = pair_magic(second ? ((j >> 1) ? w.w : w.z) : ((j >> 1) ? w.y : w.x), 8 * (j & 1), 0x00FF00FFu);
+  } else {
+    sub_tile_pairs<3>(w, r, hp);
+  }
+}
+
+__global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
+  constexpr int kRows = 128;
+  __shared__ __attribute__((aligned(16))) uint16_t lds_a[2][kTokWG * kChunk];     // swizzled, no padding
+  __shared__ __attribute__((aligned(16))) uint16_t lds_b[2][2][kRows * kLdsRow];  // [stage][hi, lo]
+  __shared__ __attribute__((aligned(16))) float lds_r[2][kRows];  // rescale s_{g-1}/s_g at a group's first chunk
+  __shared__ int lds_tag[2];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int th = wv & 1, rt = wv >> 1;  // MFMA role: token half, packed tile
+  int idx = 0;
+#pragma unroll
+  for (int i = 1; i < POLYQ_MAX_BATCH; ++i) idx += (i < a.count && static_cast<int>(blockIdx.x) >= a.wg_begin[i]) ? 1 : 0;
+  const GemmItem& it = a.item[idx];
+  const int local = static_cast<int>(blockIdx.x) - a.wg_begin[idx];
+  const int mt = local % a.m_tiles, rest = local / a.m_tiles;
+  const int ks = rest % a.splits, rp = rest / a.splits;
+  const int m0 = mt * kTokWG;
+  const int c0 = a.splits > 1 ? a.split_chunk[ks] : 0;
+  const int C = a.splits > 1 ? a.split_chunk[ks + 1] : it.n_chunks;
+  int b0 = 0;
+#pragma unroll
+  for (int j = 0; j < POLYQ_MAX_BLOCKS - 1; ++j) b0 += (j + 1 < it.nblocks && c0 >= it.ce[j]) ? 1 : 0;
+  auto cursor_at0 = [&]() { return ChunkCursor{c0, b0, it.bits[b0], c0 - it.cb[b0], it.ce[b0]}; };
+  auto advance = [&](ChunkCursor& u) {
+    ++u.c;
+    ++u.cl;
+    if (u.c == u.ce && u.c < C) {
+      ++u.bi;
+      u.bits = it.bits[u.bi];
+      u.ce = it.ce[u.bi];
+      u.cl = 0;
+    }
+  };
+
+  // Dequantization role: packed tile dp, row sub-tiles dr and dr + 1, lane
+  // slice `lane`; rows R0 = 16 dr + lane % 16 and R0 + 16.
+  const int dp = wv >> 1, dr = 2 * (wv & 1);
+  const int dt = rp * 2 + dp;
+  const bool dtile_ok = dt < it.n_tiles;
+  const int R0 = 16 * dr + (lane & 15);
+  const int bofs = (dp * 64 + R0) * kLdsRow + 8 * (lane >> 4);
+  constexpr int kHalfB = kRows * kLdsRow;
+
+  const __amdgpu_buffer_rsrc_t xrs =
+      make_rsrc(it.x + static_cast<int64_t>(m0) * it.k, static_cast<uint32_t>(min(a.m - m0, kTokWG)) * it.k * 2u);
+  uint32_t avoff[4];
+  int aofs_st[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int piece = tid + j * 256, t = piece >> 2, sg = piece & 3;
+    avoff[j] = (static_cast<uint32_t>(t) * it.k + sg * 8) * 2u;
+    aofs_st[j] = t * kChunk + 8 * (sg ^ swz(t));
+  }
+
+  int lc = c0, lb = 0, lcl = 0, lbits = 0, lce = 0, lrb = 0;
+  uint32_t lvoff = 0;
+  __amdgpu_buffer_rsrc_t wrs;
+  auto set_block = [&](int b) {
+    lb = b;
+    lbits = it.bits[b];
+    lce = it.ce[b];
+    lrb = static_cast<int>(it.rb[b]);
+    const int64_t tb = it.tb[b];
+    wrs = make_rsrc(it.packed + it.off[b] + static_cast<int64_t>(dtile_ok ? dt : 0) * tb,
+                    dtile_ok ? static_cast<uint32_t>(tb) : 0u);
+    lvoff = static_cast<uint32_t>(lane * 4 * lbits + sub_offset(lbits, dr));
+    lcl = 0;
+  };
+  const uint32_t zvoff = 2 * meta_z_half(R0);  // both rows' z (halves 4 (lane%16) + dr, + 1)
+  const uint32_t svoff0 = 2 * meta_s_half(R0), svoff1 = 2 * meta_s_half(R0 + 16);
+  auto load = [&](PreW& pr) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      pr.av[j] = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, avoff[j], lc * 64, 0));
+    const int rec = (lcl >> 2) * lrb;
+    const int soff = rec + (lbits <= 8 ? kMetaBytes : 0) + (lcl & 3) * 256 * lbits;
+    pr.w0 = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(wrs, lvoff, soff, 0));
+    pr.w1 = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(wrs, lvoff + 16, soff, 0));
+    pr.z2 = __builtin_amdgcn_raw_buffer_load_b32(wrs, zvoff, rec, 0);
+    pr.s0 = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff0, rec, 0);
+    pr.s1 = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff1, rec, 0);
+    ++lc;
+    ++lcl;
+    if (lc == lce && lc < C) set_block(lb + 1);
+  };
+
+  // Group scale of the two rows (0 read as 1), kept from the previous group.
+  float sig_prev0 = 1.f, sig_prev1 = 1.f;
+  auto store = [&](const ChunkCursor& ci, const PreW& pr, int st) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) *reinterpret_cast<u4v*>(&lds_a[st][aofs_st[j]]) = pr.av[j];
+    float sg0 = 1.f, sg1 = 1.f;
+    bool dead0 = false, dead1 = false;
+    if (ci.bits <= 8) {
+      const float s0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s0)));
+      const float s1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s1)));
+      dead0 = s0 == 0.f;
+      dead1 = s1 == 0.f;
+      sg0 = dead0 ? 1.f : s0;
+      sg1 = dead1 ? 1.f : s1;
+    }
+    if ((ci.cl & 3) == 0) {  // first chunk of a group: rescale factors of its rows
+      lds_r[st][dp * 64 + R0] = sig_prev0 / sg0;  // the four threads of a row store the same value
+      lds_r[st][dp * 64 + R0 + 16] = sig_prev1 / sg1;
+      sig_prev0 = sg0;
+      sig_prev1 = sg1;
+    }
+    uint16_t* hi = &lds_b[st][0][bofs];
+    uint16_t* lo = hi + kHalfB;
+    constexpr int kRowStep = 16 * kLdsRow;  // row R0 + 16
+    float v0[8], v1[8];
+    if (ci.bits == 16) {
+      const uint32_t ww[8] = {pr.w0.x, pr.w0.y, pr.w0.z, pr.w0.w, pr.w1.x, pr.w1.y, pr.w1.z, pr.w1.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const h2 h = __builtin_bit_cast(h2, ww[i]), g = __builtin_bit_cast(h2, ww[4 + i]);
+        v0[2 * i] = static_cast<float>(h.x);
+        v0[2 * i + 1] = static_cast<float>(h.y);
+        v1[2 * i] = static_cast<float>(g.x);
+        v1[2 * i + 1] = static_cast<float>(g.y);
+      }
+      store_pair(v0, hi, lo);
+      store_pair(v1, hi + kRowStep, lo + kRowStep);
+      return;
+    }
+    const h2 zz = __builtin_bit_cast(h2, pr.z2);
+    const float z0 = static_cast<float>(zz.x), z1 = static_cast<float>(zz.y);
+    uint32_t hp0[4], hp1[4];
+    switch (ci.bits) {
+      case 2: pairs_at<2>(pr.w0, dr, 0, hp0); pairs_at<2>(pr.w0, dr + 1, 1, hp1); break;
+      case 3: pairs_at<3>(pr.w0, dr, 0, hp0); pairs_at<3>(pr.w0, dr + 1, 1, hp1); break;
+      case 4: pairs_at<4>(pr.w0, dr, 0, hp0); pairs_at<4>(pr.w0, dr + 1, 1, hp1); break;
+      default: pairs_at<8>(pr.w0, dr, 0, hp0); pairs_at<8>(pr.w0, dr + 1, 1, hp1); break;
+    }
+    // (1024 + q) - (1024 + z) = q - z, exact in fp32 (and in bf16 when z is an
+    // integer in [0, 255])
+    const float zo0 = 1024.f + z0, zo1 = 1024.f + z1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const h2 h = __builtin_bit_cast(h2, hp0[j]), g = __builtin_bit_cast(h2, hp1[j]);
+      v0[2 * j] = static_cast<float>(h.x) - zo0;
+      v0[2 * j + 1] = static_cast<float>(h.y) - zo0;
+      v1[2 * j] = static_cast<float>(g.x) - zo1;
+      v1[2 * j + 1] = static_cast<float>(g.y) - zo1;
+    }
+    if (__any(dead0 || dead1)) {  // rows whose scale is 0 contribute nothing
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        v0[e] = dead0 ? 0.f : v0[e];
+        v1[e] = dead1 ? 0.f : v1[e];
+      }
+    }
+    const bool ok0 = z0 == truncf(z0) && z0 >= 0.f && z0 <= 255.f;
+    const bool ok1 = z1 == truncf(z1) && z1 >= 0.f && z1 <= 255.f;
+    if (__all(ok0 && ok1)) {  // wave-uniform
+      store_exact(v0, hi);
+      store_exact(v1, hi + kRowStep);
+      *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<uint4*>(lo + kRowStep) = uint4{0u, 0u, 0u, 0u};
+    } else {
+      store_pair(v0, hi, lo);
+      store_pair(v1, hi + kRowStep, lo + kRowStep);
+      lds_tag[st] = ci.c + 1;
+    }
+  };
+
+  f4 T[4][8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) T[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  const int bofs_m = (rt * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
+  auto bfrag = [&](int st, int j) {
+    const int t = th * 128 + 16 * j + (lane & 15);
+    return *reinterpret_cast<const bf16x8*>(&lds_a[st][t * kChunk + 8 * ((lane >> 4) ^ swz(t))]);
+  };
+  ChunkCursor mc = cursor_at0(), sc = cursor_at0();
+  auto step = [&](PreW& slot) {
+    const int c = mc.c, st = (c - c0) & 1;
+    const bool two = mc.bits == 16 || lds_tag[st] == c + 1;
+    if ((mc.cl & 3) == 0 && c != c0) {  // a new group: T to the new scale's units
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f4 r = *reinterpret_cast<const f4*>(&lds_r[st][rt * 64 + 16 * i + 4 * (lane >> 4)]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) T[i][j][e] *= r[e];
+      }
+    }
+    bf16x8 af[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(&lds_b[st][0][bofs_m + i * 16 * kLdsRow]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bf16x8 b = bfrag(st, j);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) T[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], b, T[i][j], 0, 0, 0);
+    }
+    if (two) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(&lds_b[st][1][bofs_m + i * 16 * kLdsRow]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const bf16x8 b = bfrag(st, j);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) T[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], b, T[i][j], 0, 0, 0);
+      }
+    }
+    if (c + 1 < C) {
+      advance(sc);
+      store(sc, slot, st ^ 1);
+    }
+    if (c + 2 < C) load(slot);
+    advance(mc);
+    __syncthreads();
+  };
+
+  PreW pre;
+  if (tid < 2) lds_tag[tid] = 0;
+  set_block(b0);
+  lcl = c0 - it.cb[b0];
+  load(pre);
+  __syncthreads();
+  store(sc, pre, 0);
+  if (C - c0 > 1) load(pre);
+  __syncthreads();
+  for (int c = c0; c < C; ++c) step(pre);
+
+  // Output: T in units of the last group's scale; that scale goes through LDS.
+  lds_r[0][dp * 64 + R0] = sig_prev0;
+  lds_r[0][dp * 64 + R0 + 16] = sig_prev1;
+  __syncthreads();
+  const int row0 = (rp * 2 + rt) * kTileRows + 4 * (lane >> 4);
+  float* ybase = a.splits > 1 ? a.partial + static_cast<int64_t>(ks) * a.m * it.n : it.y;
+  const bool vec = a.splits > 1 ? (it.n & 3) == 0 : it.y_vec != 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const f4 sl = *reinterpret_cast<const f4*>(&lds_r[0][rt * 64 + 16 * i + 4 * (lane >> 4)]);
+    const int row = row0 + 16 * i;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int tok = m0 + th * 128 + 16 * j + (lane & 15);
+      if (tok >= a.m) continue;
+      float* yr = ybase + static_cast<int64_t>(tok) * it.n;
+      const f4 v = T[i][j] * sl;
+      if (vec && row + 3 < it.n) {
+        *reinterpret_cast<f4*>(yr + row) = v;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (row + e < it.n) yr[row + e] = v[e];
+      }
+    }
+  }
+}
+
 // x'[i][j] = x[i][perm[j]] for one token row per work-group: the row is staged
 // in LDS with 16-byte loads, then gathered there and written with 16-byte
 // stores (k <= kPermLdsK, rows 16-byte aligned).
@@ -616,9 +922,14 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
       g.rb[b] = used ? L.record_bytes[b] : 0;
     }
   }
-  // One packed tile per work-group (two co-resident work-groups per CU with
-  // independent barriers), or two when that still gives 200+ work-groups.
-  const bool wide = splits == 1 && (tiles1 + count) / 2 * a.m_tiles >= 200;
+  // Work-group shape by launch size: 4-wave work-groups of 256 tokens x 128
+  // rows with 128 x 64 wave tiles (gemm_wide_kernel) when there are enough of
+  // them for two per CU; else 8-wave work-groups of the same tile
+  // (gemm_kernel<2>) when those fill most CUs; else one packed tile per
+  // 4-wave work-group (gemm_kernel<1>, two co-resident per CU).
+  const int64_t wg2 = (tiles1 + count) / 2 * a.m_tiles;
+  const int kind = splits > 1 ? 1 : wg2 >= 400 ? 3 : wg2 >= 200 ? 2 : 1;
+  const bool wide = kind >= 2;
   const int tn = wide ? 2 : 1;
   int64_t wg = 0;
   for (int i = 0; i < count; ++i) {
@@ -641,7 +952,9 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
                                       : (sp >= splits ? L.n_chunks : gstart[static_cast<int64_t>(G) * sp / splits]);
     a.partial = splits > 1 ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + partial_off) : nullptr;
   }
-  if (wide)
+  if (kind == 3)
+    hipLaunchKernelGGL(gemm_wide_kernel, dim3(static_cast<unsigned>(wg)), dim3(256), 0, st, a);
+  else if (kind == 2)
     hipLaunchKernelGGL(gemm_kernel<2>, dim3(static_cast<unsigned>(wg)), dim3(512), 0, st, a);
   else
     hipLaunchKernelGGL(gemm_kernel<1>, dim3(static_cast<unsigned>(wg)), dim3(256), 0, st, a);

@@ -153,3 +153,29 @@ def test_gemm_batch_rejects_bad_requests():
         pq.gemm_batch([(pl.layout, pl.packed, pl.perm, x, None)] * (pq._lib.MAX_BATCH + 1))
     with pytest.raises(ValueError):
         pq.gemm_batch([(pl.layout, pl.packed, pl.perm, x, None), (pl.layout, pl.packed, pl.perm, x[:3], None)])
+
+
+def test_gemm_wide_path_rescale():
+    """A launch large enough for the wide-wave kernel (running rescale between
+    groups instead of a per-group fold): mixed blocks, a 16-bit block, rows
+    whose scale is zero, a non-integer zero point, ragged M."""
+    blocks = [(2, 160), (3, 96), (4, 128), (8, 96), (16, 32)]
+    lins = []
+    for i in range(2):
+        lin = random_quant_linear(25600, 512, blocks, seed=900 + i, mode="codes")
+        sc = lin.scales.clone()
+        sc[7, :] = 0           # row 7: every group scale zero
+        sc[4097, 1] = 0        # one group of one row
+        lin.scales = sc
+        if i == 1:
+            zz = lin.zeros.clone()
+            zz[100, 0] = 3.5   # a non-integer zero point (lo tile, second MFMA pass)
+            lin.zeros = zz
+        lins.append(lin)
+    pls = [packed_linear(lin) for lin in lins]
+    x = _xb(200, 512, seed=17)
+    ys = pq.prefill_batch(pls, [x.to(dev())] * 2)
+    torch.cuda.synchronize()
+    for lin, y in zip(lins, ys):
+        y_ref, bound = oracle_ref(lin, x)
+        assert_parity(y, y_ref, bound, f"gemm wide n={lin.n}")
