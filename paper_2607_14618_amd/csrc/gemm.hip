@@ -790,12 +790,12 @@ int64_t tile_groups(const polyq_layout& L, int32_t m, int tn) {
   return static_cast<int64_t>((L.n_tiles + tn - 1) / tn) * ((m + kTokWG - 1) / kTokWG);
 }
 
-// K splits of a single-linear launch: enough work-groups for two per CU
-// (about 480), at least four groups per split, at most kMaxSplits.
+// K splits of a single-linear launch whose one-tile work-groups would leave
+// CUs idle: enough wide-wave work-groups for two per CU (about 480), at least
+// four groups per split, at most kMaxSplits.
 int plan_splits(const polyq_layout& L, int32_t m, int32_t count) {
-  if (count != 1) return 1;
-  const int64_t wg = tile_groups(L, m, 1);
-  if (wg >= 240) return 1;
+  if (count != 1 || tile_groups(L, m, 1) >= 240) return 1;
+  const int64_t wg = tile_groups(L, m, 2);  // split launches run the wide-wave kernel
   int groups = 0;
   for (int i = 0; i < L.nblocks; ++i) groups += (L.block[i].len / kChunk + kChunksPerGroup - 1) / kChunksPerGroup;
   const int64_t want = (480 + wg - 1) / wg;
@@ -924,11 +924,11 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
   }
   // Work-group shape by launch size: 4-wave work-groups of 256 tokens x 128
   // rows with 128 x 64 wave tiles (gemm_wide_kernel) when there are enough of
-  // them for two per CU; else 8-wave work-groups of the same tile
+  // them for two per CU, or K is split; else 8-wave work-groups of the same tile
   // (gemm_kernel<2>) when those fill most CUs; else one packed tile per
   // 4-wave work-group (gemm_kernel<1>, two co-resident per CU).
   const int64_t wg2 = (tiles1 + count) / 2 * a.m_tiles;
-  const int kind = splits > 1 ? 1 : wg2 >= 400 ? 3 : wg2 >= 200 ? 2 : 1;
+  const int kind = splits > 1 || wg2 >= 400 ? 3 : wg2 >= 200 ? 2 : 1;
   const bool wide = kind >= 2;
   const int tn = wide ? 2 : 1;
   int64_t wg = 0;
