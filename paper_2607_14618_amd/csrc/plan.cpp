@@ -15,7 +15,11 @@ bool bits_in_palette(int b) { return b == 2 || b == 3 || b == 4 || b == 8 || b =
 constexpr int kWavesPerWG = 4;
 constexpr int kResidentWGs = 768;        // 256 CUs x 3 co-resident 4-wave work-groups (<= 168 VGPRs)
 constexpr int kMinChunksPerWave = 4;      // below this the per-wave setup dominates
-constexpr size_t kLdsBudget = 64 * 1024;  // per work-group
+constexpr size_t kLdsBudget = 64 * 1024;  // per work-group, one token
+// With several tokens the staged activations grow with M; a larger budget
+// (two work-groups per CU instead of three) keeps the split count, and with
+// it the number of work-group rounds, down.
+constexpr size_t kLdsBudgetTokens = 80 * 1024;
 
 }  // namespace
 
@@ -183,7 +187,7 @@ int plan_gemv(const polyq_layout& L, int32_t m, int32_t launch_tiles, GemvPlan* 
     }
     p->lds_chunks = worst;
     p->lds_groups = worst_groups;
-    if (gemv_lds_bytes(*p, m) <= kLdsBudget) return 0;
+    if (gemv_lds_bytes(*p, m) <= (m > 1 ? kLdsBudgetTokens : kLdsBudget)) return 0;
     if (S * W >= kMaxSplitEntries || S >= C) return 1;
     ++S;
   }
