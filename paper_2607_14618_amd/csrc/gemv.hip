@@ -477,80 +477,122 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   // LDS of this wave: x' rows 0..m-1 and a zero row m (MFMA columns of absent
   // tokens) for its channels, then its group metadata.
   const int range = has_work ? (c1 - c0) * kChunk : 0;
-  const int kbase = c0 * kChunk;
+  // first channel of the range (0 for a wave without work, whose index loads
+  // must still stay inside the permutation array)
+  const int kbase = has_work ? c0 * kChunk : 0;
   uint16_t* xs16 = reinterpret_cast<uint16_t*>(reinterpret_cast<uint8_t*>(smem) +
                                                static_cast<size_t>(wave) * ITEM(int32_t, wave_lds));
   uint8_t* wmeta = reinterpret_cast<uint8_t*>(xs16) + align16((m + 1) * range * 2);
 
-  // (1) Permutation of this wave's channels: 8 consecutive channels per lane
-  // in each of kFastRounds rounds of 512.  The code is branch-free so that every
-  // load is issued before the first use: indices are clamped, results masked,
-  // and without a permutation the (ignored) index loads read the packed
-  // buffer, which always holds more than 4k bytes.
+  // Steps (1)-(5) run for exactly the number of 512-channel rounds the range
+  // needs (one code copy per count and per form of x), so that every load of
+  // a step is issued before the first of them is used.
   constexpr int kRound = 64 * 8;
   constexpr int kFastRounds = 4;
   const int fast_end = min(range, kFastRounds * kRound);
+  const int rounds = max((fast_end + kRound - 1) / kRound, 1);
   const bool use_perm = perm != nullptr;
+  // index source of the slow staging path (without a permutation its loads
+  // are ignored and read the packed buffer, which holds more than 4k bytes)
   const int32_t* pbase = use_perm ? perm : reinterpret_cast<const int32_t*>(packed);
-  int src[kFastRounds][8];
-#pragma unroll
-  for (int u = 0; u < kFastRounds; ++u) {
-    const int kk = u * kRound + lane * 8;
-    const bool has = kk < fast_end;
-    const int kp0 = kbase + (has ? kk : 0);
-    const uint4 p0 = ldg16(pbase + kp0), p1 = ldg16(pbase + kp0 + 4);
-    const int pv[8] = {static_cast<int>(p0.x), static_cast<int>(p0.y), static_cast<int>(p0.z),
-                       static_cast<int>(p0.w), static_cast<int>(p1.x), static_cast<int>(p1.y),
-                       static_cast<int>(p1.z), static_cast<int>(p1.w)};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int v = use_perm ? pv[e] : kp0 + e;
-      src[u][e] = has && static_cast<unsigned>(v) < static_cast<unsigned>(kdim) ? v : -1;
-    }
-  }
-  // (2) Activations of token 0 for those channels.
-  uint32_t q[kFastRounds][4];
-  {
-    const auto xr = gl(xg);
-#pragma unroll
-    for (int u = 0; u < kFastRounds; ++u) {
-      uint32_t h[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t v = xr[max(src[u][e], 0)];
-        h[e] = src[u][e] >= 0 ? v : 0u;
-      }
-#pragma unroll
-      for (int d = 0; d < 4; ++d) q[u][d] = h[2 * d] | (h[2 * d + 1] << 16);
-    }
-  }
-  // (3) Metadata of the wave's first groups (four 16-byte pieces per lane).
+  // Token 0's activations as a raw buffer of k halves: a byte offset at or
+  // past 2k (an index outside [0, k)) reads 0.
+  const __amdgpu_buffer_rsrc_t xrs =
+      tile_rsrc(reinterpret_cast<const uint8_t*>(xg), 2 * static_cast<int64_t>(kdim));
   const int fg0 = fl0 >> 2, fpieces = (fb <= 8 && fl0 < fl1) ? ((((fl1 - 1) >> 2) + 1 - fg0) * 16) : 0;
-  uint4 mv[4];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int j = min(u * 64 + lane, max(fpieces - 1, 0));
-    mv[u] = ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16);
-  }
-  // (4) The first two weight slots.
+  uint4 mv[kFastRounds];
   Slot sa, sb;
-  if (has_work) {
-    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, ftb);
-    switch (fb) {
-      case 2: preload<2>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-      case 3: preload<3>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-      case 4: preload<4>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-      case 8: preload<8>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-      default: preload<16>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-    }
-  }
-  // (5) x' of token 0 and the zero row into LDS.
+  // (3) Metadata of the wave's first groups, 16-byte pieces, one per lane per
+  // round (a range of R rounds has at most 64 R pieces within its first four
+  // rounds), then (4) the first two weight slots.
+  auto issue_meta_and_weights = [&](auto rounds_tag) {
+    constexpr int R = decltype(rounds_tag)::value;
 #pragma unroll
-  for (int u = 0; u < kFastRounds; ++u) {
+    for (int u = 0; u < R; ++u) {
+      const int j = min(u * 64 + lane, max(fpieces - 1, 0));
+      mv[u] = ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16);
+    }
+    if (has_work) {
+      const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, ftb);
+      switch (fb) {
+        case 2: preload<2>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+        case 3: preload<3>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+        case 4: preload<4>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+        case 8: preload<8>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+        default: preload<16>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+      }
+    }
+  };
+  // (5) x' of token 0 (8 channels per lane and round) and the zero row into LDS.
+  auto store_x = [&](int u, uint4 q) {
     const int kk = u * kRound + lane * 8;
     if (kk < fast_end) {
-      *reinterpret_cast<uint4*>(xs16 + kk) = uint4{q[u][0], q[u][1], q[u][2], q[u][3]};
+      *reinterpret_cast<uint4*>(xs16 + kk) = q;
       *reinterpret_cast<uint4*>(xs16 + m * range + kk) = uint4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto stage_fast = [&](auto rounds_tag, auto perm_tag) {
+    constexpr int R = decltype(rounds_tag)::value;
+    // lanes past the range load the range's first channels again; their
+    // values are never stored
+    int kp[R];
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int kk = u * kRound + lane * 8;
+      kp[u] = kbase + (kk < fast_end ? kk : 0);
+    }
+    if constexpr (!decltype(perm_tag)::value) {
+      // x already clustered: 8 consecutive channels per lane and round.
+      uint4 xv[R];
+#pragma unroll
+      for (int u = 0; u < R; ++u) xv[u] = ldg16(xg + kp[u]);
+      issue_meta_and_weights(rounds_tag);
+#pragma unroll
+      for (int u = 0; u < R; ++u) store_x(u, xv[u]);
+    } else {
+      // (1) The permutation of the lane's 8 channels per round, then (2) one
+      // 2-byte gather per channel (one memory round trip each).
+      uint4 pv[R][2];
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        pv[u][0] = ldg16(perm + kp[u]);
+        pv[u][1] = ldg16(perm + kp[u] + 4);
+      }
+      uint32_t h[R][8];
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        const uint32_t p8[8] = {pv[u][0].x, pv[u][0].y, pv[u][0].z, pv[u][0].w,
+                                pv[u][1].x, pv[u][1].y, pv[u][1].z, pv[u][1].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          h[u][e] = __builtin_amdgcn_raw_buffer_load_b16(xrs, min(p8[e], static_cast<uint32_t>(kdim)) << 1, 0, 0);
+      }
+      issue_meta_and_weights(rounds_tag);
+#pragma unroll
+      for (int u = 0; u < R; ++u)
+        store_x(u, uint4{h[u][0] | (h[u][1] << 16), h[u][2] | (h[u][3] << 16),
+                         h[u][4] | (h[u][5] << 16), h[u][6] | (h[u][7] << 16)});
+    }
+  };
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
+  using Gather = std::true_type;
+  using Clustered = std::false_type;
+  if (use_perm) {
+    switch (rounds) {
+      case 4: stage_fast(I4{}, Gather{}); break;
+      case 3: stage_fast(I3{}, Gather{}); break;
+      case 2: stage_fast(I2{}, Gather{}); break;
+      default: stage_fast(I1{}, Gather{}); break;
+    }
+  } else {
+    switch (rounds) {
+      case 4: stage_fast(I4{}, Clustered{}); break;
+      case 3: stage_fast(I3{}, Clustered{}); break;
+      case 2: stage_fast(I2{}, Clustered{}); break;
+      default: stage_fast(I1{}, Clustered{}); break;
     }
   }
   // (6) Rare: more tokens, or channels past the fast rounds (these loads wait
@@ -611,8 +653,10 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     }
   };
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int u = 0; u < kFastRounds; ++u) {
+    if (u >= rounds) break;
     if (u * 64 + lane < fpieces) meta_store(u * 64 + lane, mv[u]);
+  }
   for (int j = 4 * 64 + lane; j < fpieces; j += 64)
     meta_store(j, ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16));
   const bool exact = __all(z_ok);

@@ -113,6 +113,28 @@ def test_gemv_non_integer_zero_points():
     assert_parity(y, y_ref, bound, "non-integer z")
 
 
+@pytest.mark.parametrize("m", [1, 3])
+def test_gemv_out_of_range_permutation_entries_read_zero(m):
+    """A permutation entry outside [0, k) must not fault; its channel reads 0."""
+    blocks = [(2, 640), (3, 256), (4, 128), (8, 96), (16, 32)]
+    k = sum(l for _, l in blocks)
+    lin = random_quant_linear(192, k, blocks, seed=31, mode="codes")
+    perm = np_(lin.perm).astype(np.int64).copy()
+    bad = np.array([0, 5, 300, 700, 1000, k - 1])
+    vals = np.array([-1, k, k + 7, 2**31 - 1, -2**31, 4 * k])
+    perm[bad] = vals
+    lin.perm = torch.from_numpy(perm.astype(np.int32))
+    pl = packed_linear(lin)
+    x = _x(m, k, 11)
+    y = pl.decode(x.to(dev()))
+    torch.cuda.synchronize()
+    xc = np.zeros((m, k), dtype=np.float16)
+    ok = (perm >= 0) & (perm < k)
+    xc[:, ok] = np_(x)[:, perm[ok]]
+    y_ref, bound = oracle_ref(lin, torch.from_numpy(xc), pre_permuted=True)
+    assert_parity(y, y_ref, bound, f"out-of-range perm entries m={m}")
+
+
 def test_gemv_adversarial_outliers_inside_2bit_groups():
     """One huge activation inside each 2-bit group, zero points at both ends."""
     blocks = [(2, 512), (16, 32)]
