@@ -446,8 +446,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   const int m = ITEM(int32_t, m), nblocks = ITEM(int32_t, nblocks), n_chunks = ITEM(int32_t, n_chunks);
   const Blocks bd{kv, nblocks, n_chunks};
   // this wave's chunks [c0, c1): one block's share (wave_range)
-  int c0, c1;
-  wave_range(s * kWaves + wave, nblocks, n_chunks, bd, &c0, &c1);
+  int c0, c1, first;
+  wave_range(s * kWaves + wave, nblocks, n_chunks, bd, &c0, &c1, &first);
   const uint8_t* packed = ITEM(const uint8_t*, packed);
   const int32_t* perm = ITEM(const int32_t*, perm);
   const uint16_t* xg = ITEM(const uint16_t*, x);
@@ -459,10 +459,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   // flight.  Each wave stages only its own channels: the waves of a
   // work-group share no x', so no work-group barrier is needed before the
   // main loop.
-  int first = 0;
-#pragma unroll
-  for (int i = 0; i < POLYQ_MAX_BLOCKS; ++i) first += (i < nblocks && bd.ce(i) <= c0) ? 1 : 0;
-  const bool has_work = c0 < c1 && first < nblocks;
+  const bool has_work = c0 < c1 && first >= 0;
   const int fb = has_work ? bd.bits(first) : 16, fcb = has_work ? bd.cb(first) : 0;
   const int fl0 = c0 - fcb, fl1 = has_work ? c1 - fcb : 0;
   const int frb = has_work ? bd.rb(first) : 0;
@@ -759,19 +756,22 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       float v[TB];
 #pragma unroll
       for (int j = 0; j < TB; ++j) v[j] = 0.f;
-      for (int s0 = 0; s0 < S; s0 += 8) {  // eight splits of TB tokens in flight at a time
-        float t[TB][8];
+      // SB splits of TB tokens in flight at a time (one round trip for up to
+      // 16 splits of one token)
+      constexpr int SB = TB == 1 ? 16 : 8;
+      for (int s0 = 0; s0 < S; s0 += SB) {
+        float t[TB][SB];
 #pragma unroll
         for (int j = 0; j < TB; ++j)
 #pragma unroll
-          for (int u = 0; u < 8; ++u)
+          for (int u = 0; u < SB; ++u)
             t[j][u] = __hip_atomic_exchange(
                 &partial[(static_cast<int64_t>(min(s0 + u, S - 1)) * m + min(t0 + j, m - 1)) * rows_pad + row],
                 0.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
         for (int j = 0; j < TB; ++j)
 #pragma unroll
-          for (int u = 0; u < 8; ++u) v[j] += t[j][u];
+          for (int u = 0; u < SB; ++u) v[j] += t[j][u];
       }
 #pragma unroll
       for (int j = 0; j < TB; ++j)

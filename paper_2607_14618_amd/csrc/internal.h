@@ -47,15 +47,17 @@ __host__ __device__ inline uint32_t div_by_magic(uint32_t a, uint32_t magic) {
 // index), cb(i) / ce(i) (chunk range), w0(i), nw(i) and magic(i) =
 // div_magic(nw(i)).  Shared by the host planner and the kernel, which must
 // agree exactly; the kernel evaluates it in scalar registers, so the block is
-// found with a handful of compares and read once.
+// found with a handful of compares and read once.  `block` (optional) receives
+// the block index i (or -1); the range is empty unless w < w0(i) + nw(i).
 template <class Blk>
 __host__ __device__ inline void wave_range(int w, int nblocks, int n_chunks, const Blk& blk,
-                                           int* lo, int* hi) {
+                                           int* lo, int* hi, int* block = nullptr) {
   int i = -1;
 #pragma unroll
   for (int b = 0; b < POLYQ_MAX_BLOCKS; ++b)
     if (b < nblocks && blk.w0(b) <= w) i = b;
   *lo = *hi = n_chunks;
+  if (block) *block = i;
   if (i < 0) return;
   const int w0 = blk.w0(i), nw = blk.nw(i);
   if (w >= w0 + nw) return;
