@@ -427,7 +427,7 @@ def main():
     a = _args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the library has no multi-GPU path "
-              "(the sharding design is described in DESIGN.md)", file=sys.stderr)
+              "(a sharded deployment runs one shard of every linear per GPU)", file=sys.stderr)
         sys.exit(2)
     import torch
     if a.copy_probe:
