@@ -163,9 +163,11 @@ polyq_status polyq_permute(const int32_t* perm, const uint16_t* x, uint16_t* x_o
  *           is 0).  It must be zero-filled before its first use and is left
  *           zero-filled by every completed call; calls that share a workspace
  *           must be ordered (same stream).
- * Precision: every w_hat * x product is exact in fp32 (q - z is an exact
- * integer, s is applied once per group); |y - y_ref| stays far inside
- * 1e-3 * sum |w_hat x| for integer zero points.
+ * Precision: for zero points that are integers of magnitude <= 1023 every
+ * w_hat * x product is exact in fp32 (q - z is an exact integer, s is applied
+ * once per group) and only fp32 accumulation rounds.  Any other z is applied
+ * as zi = rint(z) (clamped to [-1023, 1023]) plus the fp32 correction
+ * -(z - zi) * sum x' per group.  |y - y_ref| <= 1e-3 * sum |w_hat x|.
  */
 size_t polyq_gemv_workspace_bytes(const polyq_layout* layout, int32_t m);
 polyq_status polyq_gemv(const polyq_layout* layout, const void* packed, const int32_t* perm,

@@ -12,8 +12,10 @@
 //
 // Unpacking: a code field placed at mantissa bits [f, f+b) of an fp16 half is
 // turned into the exact fp16 value (2^(10-f) + q) by OR-ing in the exponent
-// field 25-f (one v_and_or_b32 for two codes); adding -(2^(10-f) + z) (exact
-// for integer zero points) gives q - z exactly.  Each 128-channel group
+// field 25-f (one v_and_or_b32 for two codes); adding -(2^(10-f) + z) gives
+// q - z exactly for an integer zero point |z| <= 1023 (any other z enters as
+// its nearest such integer zi, and the group's fold subtracts
+// (z - zi) * sum x' in fp32).  Each 128-channel group
 // accumulates into its own fp32 tile, scaled once by the row's fp16 scale:
 // y += s * sum_group (q - z) x'.  All products are exact; only fp32
 // accumulation rounds.  16-bit channels enter the MFMA as their fp16 weights.
@@ -55,7 +57,7 @@ struct GemvItem {
   int32_t wave_lds;       // LDS bytes of one wave's staging region
   int32_t n_tiles, n_chunks;
   uint32_t tiles_magic;   // div_magic(n_tiles)
-  int32_t pad0;
+  int32_t fix_offset;     // offset of the zero-point corrections in a wave's region
   int32_t bits[POLYQ_MAX_BLOCKS];
   int32_t chunk_begin[POLYQ_MAX_BLOCKS];
   int32_t wave_begin[POLYQ_MAX_BLOCKS];  // first wave (per tile) of each block
@@ -231,15 +233,14 @@ __device__ __forceinline__ void issue(Slot& sl, __amdgpu_buffer_rsrc_t r, int re
 }
 
 // State of the group being accumulated: the per-pair constants subtracted
-// from the unpacked raw values, and the group's own accumulators (one f4 per
-// 16-row sub-tile).
-//   kExact (every zero point an integer of magnitude <= 1023):
-//     c[P] = -(2^(10-f) + z_row): one exact add leaves q - z.
-//   otherwise: c[P] = -2^(10-f) leaves q, and -z_row is added in fp16
-//     (q - z rounded to fp16 before the exact product).
+// from the unpacked raw values, c[P] = -(2^(10-f) + z_row) with z_row an
+// integer of magnitude <= 1023 (one exact add leaves q - z_row), and the
+// group's own accumulators (one f4 per 16-row sub-tile).  A zero point that is
+// not such an integer is staged as its nearest one, zi = rint(z) clamped to
+// [-1023, 1023], and the fold adds the remainder: s (sum (q - zi) x' -
+// (z - zi) sum x').
 struct Group {
   h2 c[16];
-  h2 nz[4];
   f4 part[4];
 };
 
@@ -250,7 +251,7 @@ __device__ __forceinline__ h8 frag(const uint32_t* w4) {
 
 // Group start: this lane's zero points (A-fragment rows 16r + l%16, r = 0..3,
 // one 8-byte LDS read) -> the pair constants.
-template <int B, bool kExact>
+template <int B>
 __device__ __forceinline__ void start_group(const uint8_t* gm, int lane, Group& gs) {
   using U = Unpack<B>;
   const uint2 zz = *reinterpret_cast<const uint2*>(gm + (lane & 15) * 8);
@@ -259,17 +260,15 @@ __device__ __forceinline__ void start_group(const uint8_t* gm, int lane, Group& 
 #pragma unroll
   for (int P = 0; P < 16; ++P) {
     const h2 off = splat(U::offset[U::which[P]]);
-    gs.c[P] = kExact ? -(zs[P >> 2] + off) : -off;
+    gs.c[P] = -(zs[P >> 2] + off);
   }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) gs.nz[r] = -zs[r];
 #pragma unroll
   for (int r = 0; r < 4; ++r) gs.part[r] = f4{0.f, 0.f, 0.f, 0.f};
 }
 
 // Unpack one lane slice of a b <= 8 block into fp16 (q - z) fragments and run
 // the four MFMAs of its 16-row sub-tiles.
-template <int B, bool kExact>
+template <int B>
 __device__ __forceinline__ void quant_slice(const uint32_t* w, h8 xb, Group& gs) {
   using U = Unpack<B>;
   uint32_t v[16];
@@ -277,19 +276,30 @@ __device__ __forceinline__ void quant_slice(const uint32_t* w, h8 xb, Group& gs)
   uint32_t d[16];
 #pragma unroll
   for (int P = 0; P < 16; ++P) {
-    h2 t = as_h2(v[P]) + gs.c[P];
-    if constexpr (!kExact) t = t + gs.nz[P >> 2];
-    d[P] = as_u32(t);
+    d[P] = as_u32(as_h2(v[P]) + gs.c[P]);
   }
 #pragma unroll
   for (int r = 0; r < 4; ++r)
     gs.part[r] = __builtin_amdgcn_mfma_f32_16x16x32_f16(frag(&d[4 * r]), xb, gs.part[r], 0, 0, 0);
 }
 
-// Group end: acc += s * part.  Lane l holds rows 16r + 4(l/16) + e; their
-// scales are 16 consecutive halves.
-__device__ __forceinline__ void fold_group(const uint8_t* gm, int lane, const Group& gs,
-                                           f4 (&acc)[4]) {
+// Group end: acc += s * part.  Lane l holds rows 16r + 4(l/16) + e of token
+// l%16; their scales are 16 consecutive halves.  With `fixed` (wave-uniform),
+// part first takes the zero-point remainders: part -= (z - zi) * sum x' (the
+// 16 remainders of the lane's rows and the token's sum from the group's
+// correction record `gf`).
+__device__ __forceinline__ void fold_group(const uint8_t* gm, const uint8_t* gf, bool fixed,
+                                           int lane, Group& gs, f4 (&acc)[4]) {
+  if (fixed) {
+    const float xsum = reinterpret_cast<const float*>(gf)[kTileRows + (lane & 15)];
+    const f4* dz = reinterpret_cast<const f4*>(gf) + (lane >> 4) * 4;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const f4 d = dz[r];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) gs.part[r][e] = fmaf(-d[e], xsum, gs.part[r][e]);
+    }
+  }
   const uint4* sp = reinterpret_cast<const uint4*>(gm + 128 + (lane >> 4) * 32);
   const uint4 s0 = sp[0], s1 = sp[1];
   const uint32_t sw[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
@@ -309,10 +319,12 @@ __device__ __forceinline__ void fold_group(const uint8_t* gm, int lane, const Gr
 // b <= 4 a slot holds whole groups and slot position j starts a group when
 // j % 4 == 0; an 8-bit group spans two slots.  `xlane` is this lane's
 // activation fragment of block-local chunk 0 (LDS); `meta` is the LDS copy of
-// the metadata of block-local group 0.
-template <int B, bool kExact>
+// the metadata of block-local group 0 and `fix` its zero-point correction
+// record (read only when `fixed`).
+template <int B>
 __device__ __forceinline__ void compute(const Slot& sl, int c, int l1, const uint32_t* xlane,
-                                        const uint8_t* meta, int lane, Group& gs, f4 (&acc)[4]) {
+                                        const uint8_t* meta, const uint8_t* fix, bool fixed,
+                                        int lane, Group& gs, f4 (&acc)[4]) {
   using G = Geo<B>;
 #pragma unroll
   for (int j = 0; j < G::NS; ++j) {
@@ -326,10 +338,10 @@ __device__ __forceinline__ void compute(const Slot& sl, int c, int l1, const uin
     } else {
       const uint8_t* gm = meta + (pos >> 2) * kMetaBytes;
       const bool start = B <= 4 ? (j & 3) == 0 : (j == 0 && (c & 3) == 0);
-      if (start) start_group<B, kExact>(gm, lane, gs);
-      quant_slice<B, kExact>(&sl.w[j * G::SW], xb, gs);
+      if (start) start_group<B>(gm, lane, gs);
+      quant_slice<B>(&sl.w[j * G::SW], xb, gs);
       const bool end = (B <= 4 && (j & 3) == 3) || (B == 8 && (pos & 3) == 3) || pos == l1 - 1;
-      if (end) fold_group(gm, lane, gs, acc);
+      if (end) fold_group(gm, fix + (pos >> 2) * kFixBytes, fixed, lane, gs, acc);
     }
   }
 }
@@ -339,25 +351,26 @@ __device__ __forceinline__ void compute(const Slot& sl, int c, int l1, const uin
 // the segment end it re-reads the last chunk, an L1/L2 hit), so the number of
 // loads between a slot's issue and its use is fixed and each wait leaves the
 // two younger slots outstanding.  `sa`/`sb` already hold the first two slots.
-template <int B, bool kExact>
+template <int B>
 __device__ __forceinline__ void run_segment(__amdgpu_buffer_rsrc_t rs, int record_bytes, int l0,
                                             int l1, const uint32_t* xlane, const uint8_t* meta,
-                                            int lane, Slot& sa, Slot& sb, f4 (&acc)[4]) {
+                                            const uint8_t* fix, bool fixed, int lane, Slot& sa,
+                                            Slot& sb, f4 (&acc)[4]) {
   constexpr int NS = Geo<B>::NS;
   const int voff = lane * Geo<B>::CB;
   Slot sc;
   Group gs;
   for (int c = l0;;) {
     issue<B>(sc, rs, record_bytes, c + 2 * NS, l1, voff);
-    compute<B, kExact>(sa, c, l1, xlane, meta, lane, gs, acc);
+    compute<B>(sa, c, l1, xlane, meta, fix, fixed, lane, gs, acc);
     c += NS;
     if (c >= l1) break;
     issue<B>(sa, rs, record_bytes, c + 2 * NS, l1, voff);
-    compute<B, kExact>(sb, c, l1, xlane, meta, lane, gs, acc);
+    compute<B>(sb, c, l1, xlane, meta, fix, fixed, lane, gs, acc);
     c += NS;
     if (c >= l1) break;
     issue<B>(sb, rs, record_bytes, c + 2 * NS, l1, voff);
-    compute<B, kExact>(sc, c, l1, xlane, meta, lane, gs, acc);
+    compute<B>(sc, c, l1, xlane, meta, fix, fixed, lane, gs, acc);
     c += NS;
     if (c >= l1) break;
   }
@@ -634,8 +647,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   if (range > fast_end) stage_slow(fast_end, range, 0, true);
 
   // (7) The wave's metadata into LDS (the zero points are checked on the way:
-  // the fast unpack needs every one to be an integer with |z| <= 1023), then
-  // any groups beyond the first 16.
+  // the unpack subtracts integers with |z| <= 1023 exactly), then any groups
+  // beyond the first 16.
   bool z_ok = true;
   auto meta_store = [&](int j, uint4 v) {
     reinterpret_cast<uint4*>(wmeta)[j] = v;
@@ -658,6 +671,36 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     meta_store(j, ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16));
   const bool exact = __all(z_ok);
 
+  // Zero points that are not all integers of magnitude <= 1023 (rare): each
+  // staged one becomes zi = rint(z) clamped to [-1023, 1023] for the unpack,
+  // and the wave's correction records receive z - zi per row (in the scales'
+  // row order) and, per token, the sum of the group's staged activations.
+  uint8_t* wfix = reinterpret_cast<uint8_t*>(xs16) + ITEM(int32_t, fix_offset);
+  const bool fixed = !exact;
+  if (fixed) {
+    const int ngr = fpieces >> 4;
+    const int ia = (lane & 15) * 4 + (lane >> 4);                              // row `lane`, zero-point order
+    const int id = ((lane >> 2) & 3) * 16 + 4 * (lane >> 4) + (lane & 3);      // and scale order
+    for (int j = 0; j < ngr; ++j) {
+      _Float16* zp = reinterpret_cast<_Float16*>(wmeta + j * kMetaBytes) + ia;
+      const float z = static_cast<float>(*zp);
+      const float zi = fminf(fmaxf(rintf(z), -1023.f), 1023.f);
+      *zp = static_cast<_Float16>(zi);
+      reinterpret_cast<float*>(wfix + j * kFixBytes)[id] = z - zi;
+    }
+    for (int task = lane; task < m * ngr; task += 64) {
+      const int t = task / ngr, j = task - t * ngr;
+      const int k1 = min((j + 1) * kGroup, range);
+      float sum = 0.f;
+      for (int kk = j * kGroup; kk < k1; kk += 8) {
+        const h8 v = __builtin_bit_cast(h8, *reinterpret_cast<const uint4*>(xs16 + t * range + kk));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sum += static_cast<float>(v[e]);
+      }
+      reinterpret_cast<float*>(wfix + j * kFixBytes)[kTileRows + t] = sum;
+    }
+  }
+
   // ---- Main loop over the wave's block range.
   f4 acc[4];
 #pragma unroll
@@ -671,22 +714,14 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
                             ((tok < m ? tok : m) * range + 8 * (lane >> 4)) / 2 + (fcb - c0) * 16;
     // metadata of block-local group 0 (only groups >= fl0 / 4 are read)
     const uint8_t* meta = wmeta - fg0 * kMetaBytes;
-    if (exact) {
-      switch (fb) {
-        case 2: run_segment<2, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
-        case 3: run_segment<3, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
-        case 4: run_segment<4, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
-        case 8: run_segment<8, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
-        default: run_segment<16, true>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
-      }
-    } else {
-      switch (fb) {
-        case 2: run_segment<2, false>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
-        case 3: run_segment<3, false>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
-        case 4: run_segment<4, false>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
-        case 8: run_segment<8, false>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
-        default: break;  // 16-bit blocks have no zero points
-      }
+    // correction record of block-local group 0 (read only when `fixed`)
+    const uint8_t* fix = wfix - fg0 * kFixBytes;
+    switch (fb) {
+      case 2: run_segment<2>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
+      case 3: run_segment<3>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
+      case 4: run_segment<4>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
+      case 8: run_segment<8>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
+      default: run_segment<16>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
     }
   }
 
@@ -881,6 +916,7 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
     g.rows_pad = L.n_tiles * kTileRows;
     g.S = p.S;
     g.wave_lds = static_cast<int32_t>(gemv_wave_lds_bytes(p, m));
+    g.fix_offset = static_cast<int32_t>(gemv_wave_fix_offset(p, m));
     g.n_tiles = L.n_tiles;
     g.n_chunks = L.n_chunks;
     g.tiles_magic = div_magic(static_cast<uint32_t>(L.n_tiles));

@@ -98,11 +98,16 @@ bool layout_is_valid(const polyq_layout* L) {
   return memcmp(&ref, L, sizeof(ref)) == 0;
 }
 
-size_t gemv_wave_lds_bytes(const GemvPlan& p, int32_t m) {
+size_t gemv_wave_fix_offset(const GemvPlan& p, int32_t m) {
   // x' rows + a zero row of the wave's channels (16-byte aligned), then its
   // group metadata
   return static_cast<size_t>(align_up(static_cast<int64_t>(p.lds_chunks) * kChunk * (m + 1) * 2, 16)) +
          static_cast<size_t>(p.lds_groups) * kMetaBytes;
+}
+
+size_t gemv_wave_lds_bytes(const GemvPlan& p, int32_t m) {
+  // ... then the zero-point corrections of its groups
+  return gemv_wave_fix_offset(p, m) + static_cast<size_t>(p.lds_groups) * kFixBytes;
 }
 
 size_t gemv_lds_bytes(const GemvPlan& p, int32_t m) {

@@ -100,17 +100,28 @@ def test_gemv_zero_weights_give_exact_zero():
     assert torch.all(y == 0)
 
 
-def test_gemv_non_integer_zero_points():
-    blocks = [(2, 128), (3, 128), (8, 128)]
-    lin = random_quant_linear(96, 384, blocks, seed=8, mode="codes")
-    rng = np.random.default_rng(0)
-    lin.zeros = torch.from_numpy(rng.uniform(0, 3, size=lin.zeros.shape).astype(np.float16))
+@pytest.mark.parametrize("m", [1, 2, 16])
+@pytest.mark.parametrize("blocks", [[(2, 128), (3, 128), (8, 128)],
+                                    [(2, 992), (3, 704), (4, 256), (8, 64), (16, 32)],
+                                    [(2, 160), (4, 96), (8, 32)]])
+def test_gemv_non_integer_zero_points(m, blocks):
+    """Zero points off the integers (fractions, halves, magnitudes past 1023) take the
+    staged nearest integer plus the per-group correction (z - zi) * sum x'."""
+    k = sum(l for _, l in blocks)
+    lin = random_quant_linear(96, k, blocks, seed=8 + m, mode="codes")
+    rng = np.random.default_rng(m)
+    z = rng.uniform(0, 3, size=lin.zeros.shape)
+    z[rng.random(z.shape) < 0.2] = 2.5                      # exact halves (ties to even)
+    z[rng.random(z.shape) < 0.05] = 1500.5                  # beyond the exact range
+    z[rng.random(z.shape) < 0.05] = -2047.0
+    z[:, 0] = np.round(z[:, 0])                              # some groups integer
+    lin.zeros = torch.from_numpy(z.astype(np.float16))
     pl = packed_linear(lin)
-    x = _x(2, 384, 4)
+    x = _x(m, k, 4)
     y = pl.decode(x.to(dev()))
     torch.cuda.synchronize()
     y_ref, bound = oracle_ref(lin, x)
-    assert_parity(y, y_ref, bound, "non-integer z")
+    assert_parity(y, y_ref, bound, f"non-integer z m={m}")
 
 
 @pytest.mark.parametrize("m", [1, 3])
