@@ -460,7 +460,10 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   const Blocks bd{kv, nblocks, n_chunks};
   // this wave's chunks [c0, c1): one block's share (wave_range)
   int c0, c1, first;
-  wave_range(s * kWaves + wave, nblocks, n_chunks, bd, &c0, &c1, &first);
+  wave_range(__builtin_amdgcn_readfirstlane(s * kWaves + wave), nblocks, n_chunks, bd, &c0, &c1, &first);
+  c0 = __builtin_amdgcn_readfirstlane(c0);
+  c1 = __builtin_amdgcn_readfirstlane(c1);
+  first = __builtin_amdgcn_readfirstlane(first);
   const uint8_t* packed = ITEM(const uint8_t*, packed);
   const int32_t* perm = ITEM(const int32_t*, perm);
   const uint16_t* xg = ITEM(const uint16_t*, x);
