@@ -251,6 +251,27 @@ def test_gemv_batch_llama_qkv_and_gate_up():
             assert_parity(y[:, rows], y_ref, bound, f"batch {lin.name}")
 
 
+def test_gemv_batch_whole_layer_one_launch():
+    """All seven linears of the Llama2-13B layer in one launch (832 tiles: the plan
+    with the fewest splits), variant G for some items and P for others; sampled
+    rows of every output against the oracle."""
+    lins, groups = make_layer(1, device=dev())
+    pls = [packed_linear(l) for l in lins]
+    xs, pre = [], []
+    for i, (lin, pl) in enumerate(zip(lins, pls)):
+        x = groups[lin.group].x.to(dev())
+        xs.append(pl.permute(x) if i % 2 else x)
+        pre.append(bool(i % 2))
+    items = [(pl.layout, pl.packed, None if p else pl.perm, x, None) for pl, x, p in zip(pls, xs, pre)]
+    ys = pq.gemv_batch(items)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    for lin, y in zip(lins, ys):
+        rows = np.sort(rng.choice(lin.n, 256, replace=False))
+        y_ref, bound = oracle_ref(lin, groups[lin.group].x, rows=rows)
+        assert_parity(y[:, rows], y_ref, bound, f"one launch {lin.name}")
+
+
 @pytest.mark.parametrize("m", [1, 4])
 def test_gemv_batch_mixed_items(m):
     """Items of different shapes and block lists, one pre-permuted, two sharing
