@@ -16,7 +16,8 @@ events on the launch stream), the prefill GEMM at M=512 (4.0-bit mix, bf16) as
 a secondary figure, and the fp64 CPU oracle timed on a bounded sample.
 
 Other modes (each prints its own single JSON line):
-  --sweep        budget sweep 3/4/5/6 b x M in {1, 4, 16} on the Llama2-13B layer
+  --sweep        budget sweep 3/4/5/6 b x M in {1, 4, 16} on the Llama2-13B layer (M > 1 also
+                 with the explicit shuffle: polyq_permute + GEMV on clustered x)
   --qwen         Qwen3-32B-shaped stack of 64 layers, variants G and P
   --copy-probe   a plain device copy of known size (HBM counter calibration)
 """
@@ -42,8 +43,9 @@ def _args():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--variant", choices=["G", "P"], default="G",
-                   help="G: permutation gathered in-kernel; P: activations pre-permuted")
+    p.add_argument("--variant", choices=["G", "P", "S"], default="G",
+                   help="G: permutation gathered in-kernel; P: activations pre-permuted; "
+                        "S: explicit polyq_permute inside every step, then clustered x")
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--no-prefill", action="store_true", help="skip the prefill GEMM figure")
@@ -177,13 +179,28 @@ def schedule(layer, grouped):
 
 
 def decode_launches(torch, pq, copies, variant, grouped=True):
+    """Variants: G gathers x' in the GEMV; P reads x' permuted beforehand (outside
+    the timed step); S permutes explicitly inside the step (one polyq_permute per
+    launch into a preallocated buffer, then the GEMV on clustered x')."""
     dev = torch.device("cuda", 0)
     ys = [torch.empty((x.shape[0], pl.n), dtype=torch.float32, device=dev) for _, pl, x in copies[0]]
-    xs = [pl.permute(x) if variant == "P" else x for _, pl, x in copies[0]]
-    pre = variant == "P"
+    xs = [pl.permute(x) if variant in ("P", "S") else x for _, pl, x in copies[0]]
+    pre = variant in ("P", "S")
     sched = schedule(copies[0], grouped)
 
     def launch(copy, idx):
+        if variant == "S":
+            j0 = idx[0]
+            perm, x, out = copy[j0][1].perm, copy[j0][2], xs[j0]
+
+            def run():
+                pq.permute(perm, x, out=out)
+                if len(idx) == 1:
+                    copy[j0][1].decode(out, pre_permuted=True, y=ys[j0])
+                else:
+                    pq.decode_batch([copy[j][1] for j in idx], [out] * len(idx), pre_permuted=True,
+                                    ys=[ys[j] for j in idx])
+            return run
         if len(idx) == 1:
             j = idx[0]
             return lambda: copy[j][1].decode(xs[j], pre_permuted=pre, y=ys[j])
@@ -363,6 +380,13 @@ def main_sweep(a, torch, pq, synth):
             rows.append({"avg_bits": bits, "m": m, "weight_bytes": d["step_bytes"],
                          "us_per_step": round(d["ms_step"] * 1e3, 2), "gbs": round(d["gbs"], 1),
                          "launches": d["launches"]})
+            if m > 1 and a.variant == "G":
+                # the explicit shuffle of the paper (Sec. 4.1): one polyq_permute per launch
+                # inside the step, then the GEMV on clustered activations
+                e = decode_figure(torch, pq, synth, a.steps, a.warmup, "S", config=2,
+                                  mix=synth.SWEEP_MIXES[bits], target_bits=bits, m=m)
+                rows[-1]["us_per_step_shuffle"] = round(e["ms_step"] * 1e3, 2)
+                rows[-1]["gbs_shuffle"] = round(e["gbs"], 1)
             _log(json.dumps(rows[-1]))
     base = [r for r in rows if r["avg_bits"] == 3 and r["m"] == 1][0]
     for r in rows:

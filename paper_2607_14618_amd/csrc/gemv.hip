@@ -505,9 +505,6 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   const int fast_end = min(range, kFastRounds * kRound);
   const int rounds = max((fast_end + kRound - 1) / kRound, 1);
   const bool use_perm = perm != nullptr;
-  // index source of the slow staging path (without a permutation its loads
-  // are ignored and read the packed buffer, which holds more than 4k bytes)
-  const int32_t* pbase = use_perm ? perm : reinterpret_cast<const int32_t*>(packed);
   // Token 0's activations as a raw buffer of k halves: a byte offset at or
   // past 2k (an index outside [0, k)) reads 0.
   const __amdgpu_buffer_rsrc_t xrs =
@@ -608,39 +605,47 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       default: stage_fast(I1{}, Clustered{}); break;
     }
   }
-  // (6) Rare: more tokens, or channels past the fast rounds (these loads wait
-  // behind the weight slots).
+  // (6) More tokens, or channels past the fast rounds (these loads wait behind
+  // the weight slots).  Tokens go in batches of kTokBatch, every load of a
+  // batch issued before the first of them is used (one memory round trip per
+  // batch): a 16-byte load per token for clustered x, else one 2-byte gather
+  // per channel and token through the token row's bounded buffer (indices
+  // outside [0, k) read 0).
   auto stage_slow = [&](int k_lo, int k_hi, int t_lo, bool zero_row) {
+    constexpr int kTokBatch = 8;
     for (int kk = k_lo + lane * 8; kk < k_hi; kk += kRound) {
-      int sr[8];
-      const uint4 p0 = ldg16(pbase + kbase + kk), p1 = ldg16(pbase + kbase + kk + 4);
-      const int pv[8] = {static_cast<int>(p0.x), static_cast<int>(p0.y), static_cast<int>(p0.z),
-                         static_cast<int>(p0.w), static_cast<int>(p1.x), static_cast<int>(p1.y),
-                         static_cast<int>(p1.z), static_cast<int>(p1.w)};
+      if (!use_perm) {
+        for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
+          uint4 v[kTokBatch];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int v = use_perm ? pv[e] : kbase + kk + e;
-        sr[e] = static_cast<unsigned>(v) < static_cast<unsigned>(kdim) ? v : -1;
-      }
-      // Tokens in batches of kTokBatch: every gather of a batch is issued
-      // before the first of them is used (one memory round trip per batch).
-      constexpr int kTokBatch = 8;
-      for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
-        uint32_t h[kTokBatch][8];
+          for (int j = 0; j < kTokBatch; ++j)
+            v[j] = ldg16(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim + kbase + kk);
 #pragma unroll
-        for (int j = 0; j < kTokBatch; ++j) {
-          const auto xr = gl(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) h[j][e] = xr[max(sr[e], 0)];
+          for (int j = 0; j < kTokBatch; ++j)
+            if (t0 + j < m) *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) = v[j];
         }
+      } else {
+        const uint4 p0 = ldg16(perm + kbase + kk), p1 = ldg16(perm + kbase + kk + 4);
+        const uint32_t p8[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+        uint32_t off[8];
 #pragma unroll
-        for (int j = 0; j < kTokBatch; ++j) {
-          uint32_t v[8];
+        for (int e = 0; e < 8; ++e) off[e] = min(p8[e], static_cast<uint32_t>(kdim)) << 1;
+        for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
+          uint32_t h[kTokBatch][8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = sr[e] >= 0 ? h[j][e] : 0u;
-          if (t0 + j < m)
-            *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) =
-                uint4{v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16)};
+          for (int j = 0; j < kTokBatch; ++j) {
+            const __amdgpu_buffer_rsrc_t rrow = tile_rsrc(
+                reinterpret_cast<const uint8_t*>(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim),
+                2 * static_cast<int64_t>(kdim));
+#pragma unroll
+            for (int e = 0; e < 8; ++e) h[j][e] = __builtin_amdgcn_raw_buffer_load_b16(rrow, off[e], 0, 0);
+          }
+#pragma unroll
+          for (int j = 0; j < kTokBatch; ++j)
+            if (t0 + j < m)
+              *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) =
+                  uint4{h[j][0] | (h[j][1] << 16), h[j][2] | (h[j][3] << 16), h[j][4] | (h[j][5] << 16),
+                        h[j][6] | (h[j][7] << 16)};
         }
       }
       if (zero_row) *reinterpret_cast<uint4*>(xs16 + m * range + kk) = uint4{0u, 0u, 0u, 0u};
@@ -770,7 +775,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     for (int w = 0; w < kWaves; ++w) v += red[(w * m + mi) * 64 + lane];
     return v;
   };
-  // Tokens go in batches of TB, all swaps of a batch in flight at once.
+  // Tokens go in batches of TB (1, 4 or 16), all swaps of a batch in flight at
+  // once.
   // Indices past the last token are clamped to it: a repeated swap writes the
   // same value again, and in the finisher a repeated read-and-zero (issued
   // after the real one, from the same lane) returns 0.
@@ -794,9 +800,9 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       float v[TB];
 #pragma unroll
       for (int j = 0; j < TB; ++j) v[j] = 0.f;
-      // SB splits of TB tokens in flight at a time (one round trip for up to
-      // 16 splits of one token)
-      constexpr int SB = TB == 1 ? 16 : 8;
+      // SB splits of TB tokens in flight at a time (64 swaps per lane, or 16
+      // for one token)
+      constexpr int SB = TB == 16 ? 4 : 16;
       for (int s0 = 0; s0 < S; s0 += SB) {
         float t[TB][SB];
 #pragma unroll
@@ -818,10 +824,13 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   };
   using One = std::integral_constant<int, 1>;
   using Four = std::integral_constant<int, 4>;
+  using Sixteen = std::integral_constant<int, 16>;
   if (m == 1)
     write_partials(One{});
-  else
+  else if (m <= 4)
     write_partials(Four{});
+  else
+    write_partials(Sixteen{});
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __builtin_amdgcn_s_waitcnt(0);  // the swaps have returned
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -832,8 +841,10 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   if (ticket % static_cast<uint32_t>(S) != static_cast<uint32_t>(S - 1)) return;
   if (m == 1)
     finish(One{});
-  else
+  else if (m <= 4)
     finish(Four{});
+  else
+    finish(Sixteen{});
   if (lane == 0) __hip_atomic_store(&counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
