@@ -20,10 +20,11 @@
 // y += s * sum_group (q - z) x'.  All products are exact; only fp32
 // accumulation rounds.  16-bit channels enter the MFMA as their fp16 weights.
 //
-// A work-group (tile, split) stages its slice of the permuted activations
-// x'[k'] = x[perm[k']] (Eq. 9) and the group metadata into LDS once, its waves
-// reduce through LDS, and splits of a tile across work-groups are combined by
-// the last-arriving work-group (fixed order).
+// Each wave stages its own channel range of the permuted activations
+// x'[k'] = x[perm[k']] (Eq. 9) and of the group metadata into LDS; the waves of
+// a work-group (tile, split) reduce through LDS, and the splits of a tile
+// across work-groups are combined by the last-arriving work-group (fixed
+// order).
 #include <hip/hip_runtime.h>
 #include <string.h>
 
@@ -441,7 +442,7 @@ __device__ __forceinline__ uint4 ldg16(const void* p) {
 }
 
 // One work-group = (linear, 64-row tile, split); its four waves each take one
-// block's range of the split (wave_range) and share the split's staged x'.
+// block's range of the split (wave_range) and stage their own x'.
 __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a) {
   extern __shared__ uint32_t smem[];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
