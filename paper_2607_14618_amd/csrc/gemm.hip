@@ -738,18 +738,35 @@ __global__ __launch_bounds__(256) void permute_rows_lds_kernel(const int32_t* __
   const uint16_t* row = reinterpret_cast<const uint16_t*>(row4);
   const int64_t base = static_cast<int64_t>(blockIdx.x) * k;
   const uint4* src = reinterpret_cast<const uint4*>(x + base);
+  const int4* p4 = reinterpret_cast<const int4*>(perm);
+  // The indices of the first kPre passes are loaded together with the row (one
+  // memory round trip for both).
+  constexpr int kPre = 4;
+  int4 pp[kPre][2];
+#pragma unroll
+  for (int u = 0; u < kPre; ++u) {
+    const int j = threadIdx.x + u * 256;
+    if (j < k / 8) {
+      pp[u][0] = p4[2 * j];
+      pp[u][1] = p4[2 * j + 1];
+    }
+  }
   for (int j = threadIdx.x; j < k / 8; j += 256) row4[j] = src[j];
   __syncthreads();
   uint4* dst = reinterpret_cast<uint4*>(out + base);
-  const int4* p4 = reinterpret_cast<const int4*>(perm);
-  for (int j = threadIdx.x; j < k / 8; j += 256) {
-    const int4 p0 = p4[2 * j], p1 = p4[2 * j + 1];
+  auto gather = [&](int j, int4 p0, int4 p1) {
     const int p[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
     uint32_t h[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) h[e] = static_cast<unsigned>(p[e]) < static_cast<unsigned>(k) ? row[p[e]] : 0u;
     dst[j] = uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+  };
+#pragma unroll
+  for (int u = 0; u < kPre; ++u) {
+    const int j = threadIdx.x + u * 256;
+    if (j < k / 8) gather(j, pp[u][0], pp[u][1]);
   }
+  for (int j = threadIdx.x + kPre * 256; j < k / 8; j += 256) gather(j, p4[2 * j], p4[2 * j + 1]);
 }
 
 // Fallback gather, one element per thread (any k, any alignment).
