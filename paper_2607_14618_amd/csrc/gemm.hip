@@ -29,6 +29,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "codec.h"
 #include "internal.h"
@@ -645,8 +646,12 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
     return *reinterpret_cast<const bf16x8*>(&lds_a[st][t * kChunk + 8 * ((lane >> 4) ^ swz(t))]);
   };
   ChunkCursor mc = cursor_at0(), sc = cursor_at0();
-  auto step = [&](PreW& slot) {
-    const int c = mc.c, st = (c - c0) & 1;
+  // st: the LDS stage of chunk c (chunks alternate, starting with stage 0 at
+  // c0), a compile-time constant in the loop below, which runs two chunks per
+  // iteration.
+  auto step = [&](PreW& slot, auto st_tag) {
+    constexpr int st = decltype(st_tag)::value;
+    const int c = mc.c;
     const bool two = mc.bits == 16 || lds_tag[st] == c + 1;
     if ((mc.cl & 3) == 0 && c != c0) {  // a new group: T to the new scale's units
 #pragma unroll
@@ -696,7 +701,14 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
   store(sc, pre, 0);
   if (C - c0 > 1) load(pre);
   __syncthreads();
-  for (int c = c0; c < C; ++c) step(pre);
+  {
+    int c = c0;
+    for (; c + 1 < C; c += 2) {
+      step(pre, std::integral_constant<int, 0>{});
+      step(pre, std::integral_constant<int, 1>{});
+    }
+    if (c < C) step(pre, std::integral_constant<int, 0>{});
+  }
 
   // Output: T in units of the last group's scale; that scale goes through LDS.
   lds_r[0][dp * 64 + R0] = sig_prev0;
