@@ -332,8 +332,9 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
   // `slot` into the other stage, fetch chunk c+3 into `slot`, fold a finished
   // group.
   ChunkCursor mc = cursor_at0(), sc = cursor_at0();
-  auto step = [&](Pre<TN>& slot) {
-    const int c = mc.c, st = (c - c0) & 1;
+  auto step = [&](Pre<TN>& slot, auto st_tag) {  // st = (c - c0) & 1, known at each call
+    constexpr int st = decltype(st_tag)::value;
+    const int c = mc.c;
     const bool two = mc.bits == 16 || lds_tag[st] == c + 1;
     bf16x8 af[4], bfr[4];
 #pragma unroll
@@ -393,10 +394,10 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
   __syncthreads();
   int c = c0;
   for (; c + 1 < C; c += 2) {
-    step(s1);
-    step(s0);
+    step(s1, std::integral_constant<int, 0>{});
+    step(s0, std::integral_constant<int, 1>{});
   }
-  if (c < C) step(s1);
+  if (c < C) step(s1, std::integral_constant<int, 0>{});
 
   // D layout: lane holds weight rows 16 i + 4 (lane/16) + e of token 16 j + lane%16.
   const int row0 = (rp * TN + rt) * kTileRows + 4 * (lane >> 4);
