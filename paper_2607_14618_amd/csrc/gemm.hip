@@ -547,31 +547,45 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
     const int soff = rec + (lbits <= 8 ? kMetaBytes : 0) + (lcl & 3) * 256 * lbits;
     pr.w0 = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(wrs, lvoff, soff, 0));
     pr.w1 = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(wrs, lvoff + 16, soff, 0));
-    pr.z2 = __builtin_amdgcn_raw_buffer_load_b32(wrs, zvoff, rec, 0);
-    pr.s0 = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff0, rec, 0);
-    pr.s1 = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff1, rec, 0);
+    if ((lcl & 3) == 0) {  // z and s are read at a group's first chunk only
+      pr.z2 = __builtin_amdgcn_raw_buffer_load_b32(wrs, zvoff, rec, 0);
+      pr.s0 = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff0, rec, 0);
+      pr.s1 = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff1, rec, 0);
+    }
     ++lc;
     ++lcl;
     if (lc == lce && lc < C) set_block(lb + 1);
   };
 
-  // Group scale of the two rows (0 read as 1), kept from the previous group.
+  // Group scale of the two rows (0 read as 1), kept from the previous group,
+  // and the values a group's first chunk derives from its metadata for the
+  // group's other chunks: 1024 + z of both rows, rows whose scale is 0, and
+  // whether every zero point of the wave is an integer in [0, 255].
   float sig_prev0 = 1.f, sig_prev1 = 1.f;
+  float gzo0 = 1024.f, gzo1 = 1024.f;
+  bool gdead0 = false, gdead1 = false, gdead = false, gexact = true;
   auto store = [&](const ChunkCursor& ci, const PreW& pr, int st) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) *reinterpret_cast<u4v*>(&lds_a[st][aofs_st[j]]) = pr.av[j];
-    float sg0 = 1.f, sg1 = 1.f;
-    bool dead0 = false, dead1 = false;
-    if (ci.bits <= 8) {
-      const float s0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s0)));
-      const float s1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s1)));
-      dead0 = s0 == 0.f;
-      dead1 = s1 == 0.f;
-      sg0 = dead0 ? 1.f : s0;
-      sg1 = dead1 ? 1.f : s1;
-    }
-    if ((ci.cl & 3) == 0) {  // first chunk of a group: rescale factors of its rows
-      lds_r[st][dp * 64 + R0] = sig_prev0 / sg0;  // the four threads of a row store the same value
+    if ((ci.cl & 3) == 0) {  // first chunk of a group: its rows' scales and zero points
+      float sg0 = 1.f, sg1 = 1.f;
+      if (ci.bits <= 8) {
+        const float s0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s0)));
+        const float s1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s1)));
+        gdead0 = s0 == 0.f;
+        gdead1 = s1 == 0.f;
+        sg0 = gdead0 ? 1.f : s0;
+        sg1 = gdead1 ? 1.f : s1;
+        const h2 zz = __builtin_bit_cast(h2, pr.z2);
+        const float z0 = static_cast<float>(zz.x), z1 = static_cast<float>(zz.y);
+        gzo0 = 1024.f + z0;
+        gzo1 = 1024.f + z1;
+        const bool ok0 = z0 == truncf(z0) && z0 >= 0.f && z0 <= 255.f;
+        const bool ok1 = z1 == truncf(z1) && z1 >= 0.f && z1 <= 255.f;
+        gexact = __all(ok0 && ok1);  // wave-uniform
+        gdead = __any(gdead0 || gdead1);
+      }
+      lds_r[st][dp * 64 + R0] = sig_prev0 / sg0;  // rescale factors (the four threads of a row store the same value)
       lds_r[st][dp * 64 + R0 + 16] = sig_prev1 / sg1;
       sig_prev0 = sg0;
       sig_prev1 = sg1;
@@ -594,8 +608,6 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
       store_pair(v1, hi + kRowStep, lo + kRowStep);
       return;
     }
-    const h2 zz = __builtin_bit_cast(h2, pr.z2);
-    const float z0 = static_cast<float>(zz.x), z1 = static_cast<float>(zz.y);
     uint32_t hp0[4], hp1[4];
     switch (ci.bits) {
       case 2: pairs_at<2>(pr.w0, dr, 0, hp0); pairs_at<2>(pr.w0, dr + 1, 1, hp1); break;
@@ -605,25 +617,24 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
     }
     // (1024 + q) - (1024 + z) = q - z, exact in fp32 (and in bf16 when z is an
     // integer in [0, 255])
-    const float zo0 = 1024.f + z0, zo1 = 1024.f + z1;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const h2 h = __builtin_bit_cast(h2, hp0[j]), g = __builtin_bit_cast(h2, hp1[j]);
-      v0[2 * j] = static_cast<float>(h.x) - zo0;
-      v0[2 * j + 1] = static_cast<float>(h.y) - zo0;
-      v1[2 * j] = static_cast<float>(g.x) - zo1;
-      v1[2 * j + 1] = static_cast<float>(g.y) - zo1;
+      v0[2 * j] = static_cast<float>(h.x) - gzo0;
+      v0[2 * j + 1] = static_cast<float>(h.y) - gzo0;
+      v1[2 * j] = static_cast<float>(g.x) - gzo1;
+      v1[2 * j + 1] = static_cast<float>(g.y) - gzo1;
     }
-    if (__any(dead0 || dead1)) {  // rows whose scale is 0 contribute nothing
+    if (gdead) {  // rows whose scale is 0 contribute nothing
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        v0[e] = dead0 ? 0.f : v0[e];
-        v1[e] = dead1 ? 0.f : v1[e];
+        v0[e] = gdead0 ? 0.f : v0[e];
+        v1[e] = gdead1 ? 0.f : v1[e];
       }
     }
-    const bool ok0 = z0 == truncf(z0) && z0 >= 0.f && z0 <= 255.f;
-    const bool ok1 = z1 == truncf(z1) && z1 >= 0.f && z1 <= 255.f;
-    if (__all(ok0 && ok1)) {  // wave-uniform
+    if (gexact) {
+      // lo stays zero: another wave of the work-group may store its rows of
+      // this chunk as pairs, and then the second MFMA pass reads all rows
       store_exact(v0, hi);
       store_exact(v1, hi + kRowStep);
       *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
