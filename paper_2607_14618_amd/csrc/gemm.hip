@@ -633,12 +633,12 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
       }
     }
     if (gexact) {
-      // lo stays zero: another wave of the work-group may store its rows of
-      // this chunk as pairs, and then the second MFMA pass reads all rows
+      // lo is left as it is: zero, unless a chunk stored as pairs used this
+      // stage last, and then the owner of each slot clears it before the
+      // stage is stored again (clear_lo), because another wave may store its
+      // rows of this chunk as pairs and the second MFMA pass reads all rows
       store_exact(v0, hi);
       store_exact(v1, hi + kRowStep);
-      *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
-      *reinterpret_cast<uint4*>(lo + kRowStep) = uint4{0u, 0u, 0u, 0u};
     } else {
       store_pair(v0, hi, lo);
       store_pair(v1, hi + kRowStep, lo + kRowStep);
@@ -658,6 +658,15 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
     return *reinterpret_cast<const bf16x8*>(&lds_a[st][t * kChunk + 8 * ((lane >> 4) ^ swz(t))]);
   };
   ChunkCursor mc = cursor_at0(), sc = cursor_at0();
+  // The lo tile of a stage is zero except where a chunk stored as pairs wrote
+  // it; each thread clears its own two lo slots of a stage whose chunk used
+  // the second pass, before it stores into that stage again.
+  bool lo_dirty[2] = {false, false};
+  auto clear_lo = [&](int st) {
+    uint16_t* lo = &lds_b[st][1][bofs];
+    *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
+    *reinterpret_cast<uint4*>(lo + 16 * kLdsRow) = uint4{0u, 0u, 0u, 0u};
+  };
   // st: the LDS stage of chunk c (chunks alternate, starting with stage 0 at
   // c0), a compile-time constant in the loop below, which runs two chunks per
   // iteration.
@@ -695,8 +704,13 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
         for (int i = 0; i < 4; ++i) T[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], b, T[i][j], 0, 0, 0);
       }
     }
+    lo_dirty[st] = two;  // this chunk's pairs sit in stage st until cleared
     if (c + 1 < C) {
       advance(sc);
+      if (lo_dirty[st ^ 1]) {  // read by the previous step, before this step's barrier
+        clear_lo(st ^ 1);
+        lo_dirty[st ^ 1] = false;
+      }
       store(sc, slot, st ^ 1);
     }
     if (c + 2 < C) load(slot);
@@ -706,6 +720,8 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
 
   PreW pre;
   if (tid < 2) lds_tag[tid] = 0;
+  clear_lo(0);
+  clear_lo(1);
   set_block(b0);
   lcl = c0 - it.cb[b0];
   load(pre);
