@@ -179,3 +179,21 @@ def test_gemm_wide_path_rescale():
     for lin, y in zip(lins, ys):
         y_ref, bound = oracle_ref(lin, x)
         assert_parity(y, y_ref, bound, f"gemm wide n={lin.n}")
+
+
+def test_gemm_and_gemv_beyond_the_lds_row_gather():
+    """K = 40960 > 32768: the prefill row gather takes its global-memory form; the
+    decode GEMV plans many splits of one tile."""
+    blocks = [(2, 20480), (3, 12288), (4, 6144), (8, 1024), (16, 1024)]
+    k = sum(l for _, l in blocks)
+    lin = random_quant_linear(96, k, blocks, seed=77, mode="codes")
+    pl = packed_linear(lin)
+    xb = _xb(5, k, seed=3)
+    y = pl.prefill(xb.to(dev()))
+    xh = (torch.randn((3, k), generator=torch.Generator().manual_seed(4))).half()
+    yv = pl.decode(xh.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, xb)
+    assert_parity(y, y_ref, bound, "gemm k=40960")
+    yv_ref, bv = oracle_ref(lin, xh)
+    assert_parity(yv, yv_ref, bv, "gemv k=40960")
