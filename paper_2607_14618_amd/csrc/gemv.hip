@@ -454,7 +454,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   const uint32_t kv = kargs[blockIdx.y * 64 + lane];
   const int n_tiles = ITEM(int32_t, n_tiles), S = ITEM(int32_t, S);
   const int local = blockIdx.x;
-  const int s = static_cast<int>(div_by_magic(static_cast<uint32_t>(local), ITEM(uint32_t, tiles_magic)));
+  const int s = static_cast<int>(
+      div_by_magic(static_cast<uint32_t>(local), ITEM(uint32_t, tiles_magic), static_cast<uint32_t>(n_tiles)));
   if (s >= S) return;  // this linear has fewer work-groups than the launch's widest
   const int tile = local - s * n_tiles;
   const int m = ITEM(int32_t, m), nblocks = ITEM(int32_t, nblocks), n_chunks = ITEM(int32_t, n_chunks);

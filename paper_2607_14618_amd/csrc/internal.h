@@ -23,7 +23,7 @@ constexpr int kFixBytes = kTileRows * 4 + 16 * 4;
 // of W waves; wave w (0 <= w < S * W, across the tile's splits) covers the
 // chunk range wave_range(w).  Every wave stays inside one block: block i gets
 // waves[i] waves per tile.
-constexpr int kMaxSplitEntries = 256;  // S * W <= this
+constexpr int kMaxSplitEntries = 4096;  // S * W <= this
 
 struct GemvPlan {
   int32_t S;                        // WG splits per 64-row tile
@@ -33,14 +33,21 @@ struct GemvPlan {
   int32_t lds_groups;               // most group records one wave stages (b <= 8 blocks)
 };
 
-// ceil(2^32 / d) for 2 <= d, or 0 for d == 1: floor(a / d) == mul_hi(a, M) for
-// every a < 2^24 (the rounding error a * (M d - 2^32) / (d 2^32) < 1/d never
-// crosses an integer).
+// Exact floor(a / d) for 1 <= d and 0 <= a < 2^31 by a multiply and shifts
+// (round-up multiplier, Granlund and Montgomery 1994): with l = floor(log2 d)
+// and M = ceil(2^(32+l) / d), a M / 2^(32+l) = a / d + a e / (d 2^(32+l)) where
+// e = M d - 2^(32+l) < d < 2^(l+1); since a e < 2^31 2^(l+1) = 2^(32+l) the
+// excess stays below 1/d and cannot reach the next integer.  M < 2^32 unless d
+// is a power of two, where div_magic returns 0 and the quotient is a >> l.
+__host__ __device__ inline int div_log2(uint32_t d) { return d <= 1 ? 0 : 31 - __builtin_clz(d); }
 __host__ __device__ inline uint32_t div_magic(uint32_t d) {
-  return d <= 1 ? 0u : static_cast<uint32_t>((0x100000000ull + d - 1) / d);
+  if ((d & (d - 1)) == 0) return 0u;  // 0, 1 and powers of two
+  return static_cast<uint32_t>(((1ull << (32 + div_log2(d))) + d - 1) / d);
 }
-__host__ __device__ inline uint32_t div_by_magic(uint32_t a, uint32_t magic) {
-  return magic == 0 ? a : static_cast<uint32_t>((static_cast<uint64_t>(a) * magic) >> 32);
+__host__ __device__ inline uint32_t div_by_magic(uint32_t a, uint32_t magic, uint32_t d) {
+  const uint32_t hi =
+      magic == 0 ? a : static_cast<uint32_t>((static_cast<uint64_t>(a) * magic) >> 32);
+  return hi >> div_log2(d);
 }
 
 // Chunk range [lo, hi) of wave w of every tile: waves are handed to the blocks
@@ -68,8 +75,8 @@ __host__ __device__ inline void wave_range(int w, int nblocks, int n_chunks, con
   const int cb = blk.cb(i), nch = blk.ce(i) - cb;
   const int ngr = (nch + kChunksPerGroup - 1) / kChunksPerGroup, j = w - w0;
   const uint32_t magic = blk.magic(i);
-  const int a = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * j), magic));
-  const int b = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * (j + 1)), magic));
+  const int a = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * j), magic, nw));
+  const int b = kChunksPerGroup * static_cast<int>(div_by_magic(static_cast<uint32_t>(ngr * (j + 1)), magic, nw));
   *lo = cb + (a < nch ? a : nch);
   *hi = cb + (b < nch ? b : nch);
 }

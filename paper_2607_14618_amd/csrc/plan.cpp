@@ -194,7 +194,8 @@ int plan_gemv(const polyq_layout& L, int32_t m, int32_t launch_tiles, GemvPlan* 
     p->lds_groups = worst_groups;
     if (gemv_lds_bytes(*p, m) <= (m > 1 ? kLdsBudgetTokens : kLdsBudget)) return 0;
     if (S * W >= kMaxSplitEntries || S >= C) return 1;
-    ++S;
+    // one split at a time while splits are few, then doubling (very long k)
+    S = S < 64 ? S + 1 : std::min(std::min(2 * S, kMaxSplitEntries / W), C);
   }
 }
 

@@ -316,3 +316,40 @@ def test_gemv_batch_rejects_bad_requests():
     assert lib.polyq_gemv_batch(arr, 9, 1, None, 0, None) == 5   # POLYQ_ERR_CAPACITY
     assert lib.polyq_gemv_batch(arr, 0, 1, None, 0, None) == 1   # POLYQ_ERR_ARG
     assert lib.polyq_gemv_batch_workspace_bytes(arr, 0, 1) == 0
+
+
+@pytest.mark.parametrize("m", [1, 16])
+def test_gemv_and_gemm_at_the_maximum_k(m):
+    """K = POLYQ_MAX_K = 2^20 with every bit-width: the GEMV splits K a thousand
+    ways (more splits than 64-row tiles), the GEMM streams it whole."""
+    k = 1 << 20
+    blocks = [(2, k // 2), (3, k // 4), (4, k // 8), (8, k // 16), (16, k // 16)]
+    lin = random_quant_linear(64, k, blocks, seed=90 + m, mode="codes")
+    pl = packed_linear(lin)
+    x = _x(m, k, seed=91 + m)
+    y = pl.decode(x.to(dev()))
+    xb = x.float().bfloat16()
+    yg = pl.prefill(xb.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, x)
+    assert_parity(y, y_ref, bound, f"gemv k=2^20 m={m}")
+    yb_ref, bb = oracle_ref(lin, xb)
+    assert_parity(yg, yb_ref, bb, f"gemm k=2^20 m={m}")
+
+
+def test_gemv_more_than_65536_row_tiles():
+    """65537 tiles of 64 rows in one split: every work-group finds its tile
+    (the work-group index is divided exactly by the tile count at any size)."""
+    n, blocks = 65537 * 64, [(2, 32), (4, 32)]
+    k = sum(l for _, l in blocks)
+    lin = random_quant_linear(n, k, blocks, seed=93, mode="codes")
+    pl = packed_linear(lin)
+    x = _x(1, k, seed=94)
+    y = torch.full((1, n), float("nan"), dtype=torch.float32, device=dev())
+    pl.decode(x.to(dev()), y=y)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(y).all()), "rows left unwritten"
+    rng = np.random.default_rng(95)
+    rows = np.unique(np.concatenate([np.arange(n - 256, n), rng.integers(0, n, 512)]))
+    y_ref, bound = oracle_ref(lin, x, rows=rows)
+    assert_parity(np_(y)[:, rows], y_ref, bound, "n_tiles=65537")

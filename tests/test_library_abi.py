@@ -77,3 +77,16 @@ def test_workspace_query_is_host_only():
 def test_status_strings():
     for s in range(8):
         assert pq.lib().polyq_status_str(s)
+
+
+@pytest.mark.parametrize("k", [1 << 16, 1 << 18, 1 << 20])
+@pytest.mark.parametrize("m", [1, 16])
+def test_gemv_plans_up_to_the_maximum_k(k, m):
+    """Every k up to POLYQ_MAX_K has a GEMV plan: its workspace query returns the
+    counters plus S x m x 64 fp32 partials for some S > 1 (a 0 would mean that
+    no split fits the work-group's LDS)."""
+    L = pq.plan(64, k, [(2, k // 2), (3, k // 4), (4, k // 8), (8, k // 16), (16, k // 16)])
+    ws = pq.gemv_workspace_bytes(L, m)
+    part = ws - 256
+    assert part > 0 and part % (m * 64 * 4) == 0
+    assert 1 < part // (m * 64 * 4) <= 1024
