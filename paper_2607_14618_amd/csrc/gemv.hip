@@ -58,7 +58,7 @@ struct GemvItem {
   int32_t wave_lds;       // LDS bytes of one wave's staging region
   int32_t n_tiles, n_chunks;
   uint32_t tiles_magic;   // div_magic(n_tiles)
-  int32_t fix_offset;     // offset of the zero-point corrections in a wave's region
+  int32_t zero_offset;    // LDS offset of the work-group's zero row
   int32_t bits[POLYQ_MAX_BLOCKS];
   int32_t chunk_begin[POLYQ_MAX_BLOCKS];
   int32_t wave_begin[POLYQ_MAX_BLOCKS];  // first wave (per tile) of each block
@@ -236,10 +236,10 @@ __device__ __forceinline__ void issue(Slot& sl, __amdgpu_buffer_rsrc_t r, int re
 // State of the group being accumulated: the per-pair constants subtracted
 // from the unpacked raw values, c[P] = -(2^(10-f) + z_row) with z_row an
 // integer of magnitude <= 1023 (one exact add leaves q - z_row), and the
-// group's own accumulators (one f4 per 16-row sub-tile).  A zero point that is
-// not such an integer is staged as its nearest one, zi = rint(z) clamped to
-// [-1023, 1023], and the fold adds the remainder: s (sum (q - zi) x' -
-// (z - zi) sum x').
+// group's own accumulators (one f4 per 16-row sub-tile).  In a wave whose zero
+// points are not all such integers (`fixed`), the unpack subtracts the nearest
+// one, zi = rint(z) clamped to [-1023, 1023], and the fold adds the remainder:
+// s (sum (q - zi) x' - (z - zi) sum x').
 struct Group {
   h2 c[16];
   f4 part[4];
@@ -250,13 +250,38 @@ __device__ __forceinline__ h8 frag(const uint32_t* w4) {
   return __builtin_bit_cast(h8, u);
 }
 
+// Zero for a pair of fp16 zero points (one dword) that are both integers of
+// magnitude <= 1023, else nonzero.  With a = |z| (sign bit cleared), a + 1024
+// is exact and lies in [1024, 2048), where the fp16 spacing is 1, exactly when
+// a is such an integer: otherwise the sum rounds (then (a + 1024) - 1024 != a)
+// or reaches 2048 or beyond (exponent field above 25; NaN and inf included).
+// Both halves at once with packed fp16 adds (round to nearest even).
+__device__ __forceinline__ uint32_t z_pair_bad(uint32_t w) {
+  const uint32_t a = w & 0x7FFF7FFFu;
+  const uint32_t k1024 = 0x64006400u;  // fp16 1024 in both halves
+  uint32_t u, t;
+  asm("v_pk_add_f16 %0, %1, %2" : "=v"(u) : "v"(a), "v"(k1024));
+  asm("v_pk_add_f16 %0, %1, %2 neg_lo:[0,1] neg_hi:[0,1]" : "=v"(t) : "v"(u), "v"(k1024));
+  return (t ^ a) | ((u & 0x7C007C00u) ^ 0x64006400u);
+}
+
+// Zero point used by the unpack in a `fixed` wave: rint(z) clamped to
+// [-1023, 1023] (an integer, exact in fp16).
+__device__ __forceinline__ float z_int(float z) { return fminf(fmaxf(rintf(z), -1023.f), 1023.f); }
+
 // Group start: this lane's zero points (A-fragment rows 16r + l%16, r = 0..3,
 // one 8-byte LDS read) -> the pair constants.
-template <int B>
+template <int B, bool Fixed>
 __device__ __forceinline__ void start_group(const uint8_t* gm, int lane, Group& gs) {
   using U = Unpack<B>;
   const uint2 zz = *reinterpret_cast<const uint2*>(gm + (lane & 15) * 8);
-  const h2 z01 = as_h2(zz.x), z23 = as_h2(zz.y);
+  h2 z01 = as_h2(zz.x), z23 = as_h2(zz.y);
+  if constexpr (Fixed) {
+    z01 = h2{static_cast<_Float16>(z_int(static_cast<float>(z01[0]))),
+             static_cast<_Float16>(z_int(static_cast<float>(z01[1])))};
+    z23 = h2{static_cast<_Float16>(z_int(static_cast<float>(z23[0]))),
+             static_cast<_Float16>(z_int(static_cast<float>(z23[1])))};
+  }
   const h2 zs[4] = {h2{z01[0], z01[0]}, h2{z01[1], z01[1]}, h2{z23[0], z23[0]}, h2{z23[1], z23[1]}};
 #pragma unroll
   for (int P = 0; P < 16; ++P) {
@@ -285,21 +310,37 @@ __device__ __forceinline__ void quant_slice(const uint32_t* w, h8 xb, Group& gs)
 }
 
 // Group end: acc += s * part.  Lane l holds rows 16r + 4(l/16) + e of token
-// l%16; their scales are 16 consecutive halves.  With `fixed` (wave-uniform),
-// part first takes the zero-point remainders: part -= (z - zi) * sum x' (the
-// 16 remainders of the lane's rows and the token's sum from the group's
-// correction record `gf`).
-__device__ __forceinline__ void fold_group(const uint8_t* gm, const uint8_t* gf, bool fixed,
+// l%16; their scales are 16 consecutive halves.  With Fixed (the wave's zero
+// points are not all small integers), part first takes the zero-point remainders: part -= (z - zi) * sum x'.  The
+// token's sum runs over the group's staged chunks [g0, g1] (block-local): each
+// lane adds its quarter (8 channels per chunk, the B fragment it read) and the
+// lanes l ^ 16, l ^ 32 hold the other quarters of the same token.  The
+// remainders come from the zero points: rows 16r + 4(l/16) + e are halves
+// 16(l/16) + 4e + r of the group's zero-point array.
+template <bool Fixed>
+__device__ __forceinline__ void fold_group(const uint8_t* gm, const uint32_t* xlane, int g0, int g1,
                                            int lane, Group& gs, f4 (&acc)[4]) {
-  if (fixed) {
-    const float xsum = reinterpret_cast<const float*>(gf)[kTileRows + (lane & 15)];
-    const f4* dz = reinterpret_cast<const f4*>(gf) + (lane >> 4) * 4;
+  if constexpr (Fixed) {
+    float xsum = 0.f;
+    for (int q = g0; q <= g1; ++q) {
+      const h8 v = __builtin_bit_cast(h8, *reinterpret_cast<const uint4*>(xlane + q * 16));
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const f4 d = dz[r];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) gs.part[r][e] = fmaf(-d[e], xsum, gs.part[r][e]);
+      for (int e = 0; e < 8; ++e) xsum += static_cast<float>(v[e]);
     }
+    xsum += __shfl_xor(xsum, 16);
+    xsum += __shfl_xor(xsum, 32);
+    const uint4* zp = reinterpret_cast<const uint4*>(gm + 32 * (lane >> 4));
+    const uint4 za = zp[0], zb = zp[1];
+    const uint32_t zw[8] = {za.x, za.y, za.z, za.w, zb.x, zb.y, zb.z, zb.w};
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = 4 * e + r;
+        const float z = static_cast<float>(
+            __builtin_bit_cast(_Float16, static_cast<uint16_t>(zw[i >> 1] >> (16 * (i & 1)))));
+        gs.part[r][e] = fmaf(-(z - z_int(z)), xsum, gs.part[r][e]);
+      }
   }
   const uint4* sp = reinterpret_cast<const uint4*>(gm + 128 + (lane >> 4) * 32);
   const uint4 s0 = sp[0], s1 = sp[1];
@@ -320,12 +361,11 @@ __device__ __forceinline__ void fold_group(const uint8_t* gm, const uint8_t* gf,
 // b <= 4 a slot holds whole groups and slot position j starts a group when
 // j % 4 == 0; an 8-bit group spans two slots.  `xlane` is this lane's
 // activation fragment of block-local chunk 0 (LDS); `meta` is the LDS copy of
-// the metadata of block-local group 0 and `fix` its zero-point correction
-// record (read only when `fixed`).
-template <int B>
+// the metadata of block-local group 0.  Fixed: the wave's zero points are not
+// all integers of magnitude <= 1023 (a separate copy of the loop).
+template <int B, bool Fixed>
 __device__ __forceinline__ void compute(const Slot& sl, int c, int l1, const uint32_t* xlane,
-                                        const uint8_t* meta, const uint8_t* fix, bool fixed,
-                                        int lane, Group& gs, f4 (&acc)[4]) {
+                                        const uint8_t* meta, int lane, Group& gs, f4 (&acc)[4]) {
   using G = Geo<B>;
 #pragma unroll
   for (int j = 0; j < G::NS; ++j) {
@@ -339,10 +379,10 @@ __device__ __forceinline__ void compute(const Slot& sl, int c, int l1, const uin
     } else {
       const uint8_t* gm = meta + (pos >> 2) * kMetaBytes;
       const bool start = B <= 4 ? (j & 3) == 0 : (j == 0 && (c & 3) == 0);
-      if (start) start_group<B>(gm, lane, gs);
+      if (start) start_group<B, Fixed>(gm, lane, gs);
       quant_slice<B>(&sl.w[j * G::SW], xb, gs);
       const bool end = (B <= 4 && (j & 3) == 3) || (B == 8 && (pos & 3) == 3) || pos == l1 - 1;
-      if (end) fold_group(gm, fix + (pos >> 2) * kFixBytes, fixed, lane, gs, acc);
+      if (end) fold_group<Fixed>(gm, xlane, pos & ~3, pos, lane, gs, acc);
     }
   }
 }
@@ -352,26 +392,25 @@ __device__ __forceinline__ void compute(const Slot& sl, int c, int l1, const uin
 // the segment end it re-reads the last chunk, an L1/L2 hit), so the number of
 // loads between a slot's issue and its use is fixed and each wait leaves the
 // two younger slots outstanding.  `sa`/`sb` already hold the first two slots.
-template <int B>
+template <int B, bool Fixed>
 __device__ __forceinline__ void run_segment(__amdgpu_buffer_rsrc_t rs, int record_bytes, int l0,
                                             int l1, const uint32_t* xlane, const uint8_t* meta,
-                                            const uint8_t* fix, bool fixed, int lane, Slot& sa,
-                                            Slot& sb, f4 (&acc)[4]) {
+                                            int lane, Slot& sa, Slot& sb, f4 (&acc)[4]) {
   constexpr int NS = Geo<B>::NS;
   const int voff = lane * Geo<B>::CB;
   Slot sc;
   Group gs;
   for (int c = l0;;) {
     issue<B>(sc, rs, record_bytes, c + 2 * NS, l1, voff);
-    compute<B>(sa, c, l1, xlane, meta, fix, fixed, lane, gs, acc);
+    compute<B, Fixed>(sa, c, l1, xlane, meta, lane, gs, acc);
     c += NS;
     if (c >= l1) break;
     issue<B>(sa, rs, record_bytes, c + 2 * NS, l1, voff);
-    compute<B>(sb, c, l1, xlane, meta, fix, fixed, lane, gs, acc);
+    compute<B, Fixed>(sb, c, l1, xlane, meta, lane, gs, acc);
     c += NS;
     if (c >= l1) break;
     issue<B>(sb, rs, record_bytes, c + 2 * NS, l1, voff);
-    compute<B>(sc, c, l1, xlane, meta, fix, fixed, lane, gs, acc);
+    compute<B, Fixed>(sc, c, l1, xlane, meta, lane, gs, acc);
     c += NS;
     if (c >= l1) break;
   }
@@ -489,21 +528,25 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   int fvoff;
   asm volatile("v_mul_u32_u24 %0, %1, %2" : "=v"(fvoff) : "v"(lane), "s"(4 * fb));
 
-  // LDS of this wave: x' rows 0..m-1 and a zero row m (MFMA columns of absent
-  // tokens) for its channels, then its group metadata.
+  // LDS of this wave: x' rows 0..m-1 for its channels, then its group
+  // metadata.  The MFMA columns of absent tokens read the work-group's zero
+  // row, which every wave fills for the length of its own range (the same
+  // zeros: no barrier needed before its reads).
   const int range = has_work ? (c1 - c0) * kChunk : 0;
   // first channel of the range (0 for a wave without work, whose index loads
   // must still stay inside the permutation array)
   const int kbase = has_work ? c0 * kChunk : 0;
   uint16_t* xs16 = reinterpret_cast<uint16_t*>(reinterpret_cast<uint8_t*>(smem) +
                                                static_cast<size_t>(wave) * ITEM(int32_t, wave_lds));
-  uint8_t* wmeta = reinterpret_cast<uint8_t*>(xs16) + align16((m + 1) * range * 2);
+  uint8_t* wmeta = reinterpret_cast<uint8_t*>(xs16) + align16(m * range * 2);
+  uint16_t* zs16 = reinterpret_cast<uint16_t*>(reinterpret_cast<uint8_t*>(smem) + ITEM(int32_t, zero_offset));
 
   // Steps (1)-(5) run for exactly the number of 512-channel rounds the range
   // needs (one code copy per count and per form of x), so that every load of
   // a step is issued before the first of them is used.
   constexpr int kRound = 64 * 8;
   constexpr int kFastRounds = 4;
+  constexpr int kTokBatch = 8;  // tokens gathered per memory round trip (m > 1)
   const int fast_end = min(range, kFastRounds * kRound);
   const int rounds = max((fast_end + kRound - 1) / kRound, 1);
   const bool use_perm = perm != nullptr;
@@ -524,23 +567,39 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       const int j = min(u * 64 + lane, max(fpieces - 1, 0));
       mv[u] = ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16);
     }
-    if (has_work) {
-      const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, ftb);
-      switch (fb) {
-        case 2: preload<2>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-        case 3: preload<3>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-        case 4: preload<4>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-        case 8: preload<8>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-        default: preload<16>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
-      }
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, ftb);
+    switch (fb) {
+      case 2: preload<2>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+      case 3: preload<3>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+      case 4: preload<4>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+      case 8: preload<8>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
+      default: preload<16>(rs, frb, fl0, fl1, fvoff, sa, sb); break;
     }
+  };
+  // (3') The wave's metadata pieces into LDS, the zero points checked on the
+  // way (the unpack subtracts integers with |z| <= 1023 exactly), right after
+  // the x' stores of each staging form.
+  uint32_t z_bad = 0;  // nonzero once a zero point is not such an integer
+  auto meta_store = [&](int j, uint4 v) {
+    reinterpret_cast<uint4*>(wmeta)[j] = v;
+    if ((j & 15) < kMetaBytes / 32) {  // a piece of zero points
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) z_bad |= z_pair_bad(w[h]);
+    }
+  };
+  auto store_meta = [&](auto rounds_tag) {
+    constexpr int R = decltype(rounds_tag)::value;
+#pragma unroll
+    for (int u = 0; u < R; ++u)
+      if (u * 64 + lane < fpieces) meta_store(u * 64 + lane, mv[u]);
   };
   // (5) x' of token 0 (8 channels per lane and round) and the zero row into LDS.
   auto store_x = [&](int u, uint4 q) {
     const int kk = u * kRound + lane * 8;
     if (kk < fast_end) {
       *reinterpret_cast<uint4*>(xs16 + kk) = q;
-      *reinterpret_cast<uint4*>(xs16 + m * range + kk) = uint4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<uint4*>(zs16 + kk) = uint4{0u, 0u, 0u, 0u};
     }
   };
   auto stage_fast = [&](auto rounds_tag, auto perm_tag) {
@@ -561,6 +620,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       issue_meta_and_weights(rounds_tag);
 #pragma unroll
       for (int u = 0; u < R; ++u) store_x(u, xv[u]);
+      store_meta(rounds_tag);
     } else {
       // (1) The permutation of the lane's 8 channels per round, then (2) one
       // 2-byte gather per channel (one memory round trip each).
@@ -584,6 +644,38 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       for (int u = 0; u < R; ++u)
         store_x(u, uint4{h[u][0] | (h[u][1] << 16), h[u][2] | (h[u][3] << 16),
                          h[u][4] | (h[u][5] << 16), h[u][6] | (h[u][7] << 16)});
+      store_meta(rounds_tag);
+      // (2') Tokens 1..m-1 through the same permutation slices (still in
+      // registers): per round, one 2-byte gather per channel and token through
+      // the token row's bounded buffer, kTokBatch tokens per memory round trip.
+      if (m > 1) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+          const uint32_t p8[8] = {pv[u][0].x, pv[u][0].y, pv[u][0].z, pv[u][0].w,
+                                  pv[u][1].x, pv[u][1].y, pv[u][1].z, pv[u][1].w};
+          uint32_t off[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) off[e] = min(p8[e], static_cast<uint32_t>(kdim)) << 1;
+          const int kk = u * kRound + lane * 8;
+          for (int t0 = 1; t0 < m; t0 += kTokBatch) {
+            uint32_t g[kTokBatch][8];
+#pragma unroll
+            for (int j = 0; j < kTokBatch; ++j) {
+              const __amdgpu_buffer_rsrc_t rrow = tile_rsrc(
+                  reinterpret_cast<const uint8_t*>(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim),
+                  2 * static_cast<int64_t>(kdim));
+#pragma unroll
+              for (int e = 0; e < 8; ++e) g[j][e] = __builtin_amdgcn_raw_buffer_load_b16(rrow, off[e], 0, 0);
+            }
+#pragma unroll
+            for (int j = 0; j < kTokBatch; ++j)
+              if (t0 + j < m && kk < fast_end)
+                *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) =
+                    uint4{g[j][0] | (g[j][1] << 16), g[j][2] | (g[j][3] << 16), g[j][4] | (g[j][5] << 16),
+                          g[j][6] | (g[j][7] << 16)};
+          }
+        }
+      }
     }
   };
   using I1 = std::integral_constant<int, 1>;
@@ -592,124 +684,82 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   using I4 = std::integral_constant<int, 4>;
   using Gather = std::true_type;
   using Clustered = std::false_type;
-  if (use_perm) {
-    switch (rounds) {
-      case 4: stage_fast(I4{}, Gather{}); break;
-      case 3: stage_fast(I3{}, Gather{}); break;
-      case 2: stage_fast(I2{}, Gather{}); break;
-      default: stage_fast(I1{}, Gather{}); break;
+  // A wave without work stages nothing (and waits for nothing).
+  bool exact = true;
+  if (has_work) {
+    if (use_perm) {
+      switch (rounds) {
+        case 4: stage_fast(I4{}, Gather{}); break;
+        case 3: stage_fast(I3{}, Gather{}); break;
+        case 2: stage_fast(I2{}, Gather{}); break;
+        default: stage_fast(I1{}, Gather{}); break;
+      }
+    } else {
+      switch (rounds) {
+        case 4: stage_fast(I4{}, Clustered{}); break;
+        case 3: stage_fast(I3{}, Clustered{}); break;
+        case 2: stage_fast(I2{}, Clustered{}); break;
+        default: stage_fast(I1{}, Clustered{}); break;
+      }
     }
-  } else {
-    switch (rounds) {
-      case 4: stage_fast(I4{}, Clustered{}); break;
-      case 3: stage_fast(I3{}, Clustered{}); break;
-      case 2: stage_fast(I2{}, Clustered{}); break;
-      default: stage_fast(I1{}, Clustered{}); break;
-    }
-  }
-  // (6) More tokens, or channels past the fast rounds (these loads wait behind
-  // the weight slots).  Tokens go in batches of kTokBatch, every load of a
-  // batch issued before the first of them is used (one memory round trip per
-  // batch): a 16-byte load per token for clustered x, else one 2-byte gather
-  // per channel and token through the token row's bounded buffer (indices
-  // outside [0, k) read 0).
-  auto stage_slow = [&](int k_lo, int k_hi, int t_lo, bool zero_row) {
-    constexpr int kTokBatch = 8;
-    for (int kk = k_lo + lane * 8; kk < k_hi; kk += kRound) {
-      if (!use_perm) {
-        for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
-          uint4 v[kTokBatch];
+    // (6) More tokens, or channels past the fast rounds (these loads wait behind
+    // the weight slots).  Tokens go in batches of kTokBatch, every load of a
+    // batch issued before the first of them is used (one memory round trip per
+    // batch): a 16-byte load per token for clustered x, else one 2-byte gather
+    // per channel and token through the token row's bounded buffer (indices
+    // outside [0, k) read 0).
+    auto stage_slow = [&](int k_lo, int k_hi, int t_lo, bool zero_row) {
+      for (int kk = k_lo + lane * 8; kk < k_hi; kk += kRound) {
+        if (!use_perm) {
+          for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
+            uint4 v[kTokBatch];
 #pragma unroll
-          for (int j = 0; j < kTokBatch; ++j)
-            v[j] = ldg16(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim + kbase + kk);
+            for (int j = 0; j < kTokBatch; ++j)
+              v[j] = ldg16(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim + kbase + kk);
 #pragma unroll
-          for (int j = 0; j < kTokBatch; ++j)
-            if (t0 + j < m) *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) = v[j];
-        }
-      } else {
-        const uint4 p0 = ldg16(perm + kbase + kk), p1 = ldg16(perm + kbase + kk + 4);
-        const uint32_t p8[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-        uint32_t off[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) off[e] = min(p8[e], static_cast<uint32_t>(kdim)) << 1;
-        for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
-          uint32_t h[kTokBatch][8];
-#pragma unroll
-          for (int j = 0; j < kTokBatch; ++j) {
-            const __amdgpu_buffer_rsrc_t rrow = tile_rsrc(
-                reinterpret_cast<const uint8_t*>(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim),
-                2 * static_cast<int64_t>(kdim));
-#pragma unroll
-            for (int e = 0; e < 8; ++e) h[j][e] = __builtin_amdgcn_raw_buffer_load_b16(rrow, off[e], 0, 0);
+            for (int j = 0; j < kTokBatch; ++j)
+              if (t0 + j < m) *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) = v[j];
           }
+        } else {
+          const uint4 p0 = ldg16(perm + kbase + kk), p1 = ldg16(perm + kbase + kk + 4);
+          const uint32_t p8[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+          uint32_t off[8];
 #pragma unroll
-          for (int j = 0; j < kTokBatch; ++j)
-            if (t0 + j < m)
-              *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) =
-                  uint4{h[j][0] | (h[j][1] << 16), h[j][2] | (h[j][3] << 16), h[j][4] | (h[j][5] << 16),
-                        h[j][6] | (h[j][7] << 16)};
+          for (int e = 0; e < 8; ++e) off[e] = min(p8[e], static_cast<uint32_t>(kdim)) << 1;
+          for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
+            uint32_t h[kTokBatch][8];
+#pragma unroll
+            for (int j = 0; j < kTokBatch; ++j) {
+              const __amdgpu_buffer_rsrc_t rrow = tile_rsrc(
+                  reinterpret_cast<const uint8_t*>(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim),
+                  2 * static_cast<int64_t>(kdim));
+#pragma unroll
+              for (int e = 0; e < 8; ++e) h[j][e] = __builtin_amdgcn_raw_buffer_load_b16(rrow, off[e], 0, 0);
+            }
+#pragma unroll
+            for (int j = 0; j < kTokBatch; ++j)
+              if (t0 + j < m)
+                *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) =
+                    uint4{h[j][0] | (h[j][1] << 16), h[j][2] | (h[j][3] << 16), h[j][4] | (h[j][5] << 16),
+                          h[j][6] | (h[j][7] << 16)};
+          }
         }
+        if (zero_row) *reinterpret_cast<uint4*>(zs16 + kk) = uint4{0u, 0u, 0u, 0u};
       }
-      if (zero_row) *reinterpret_cast<uint4*>(xs16 + m * range + kk) = uint4{0u, 0u, 0u, 0u};
-    }
-  };
-  if (m > 1) stage_slow(0, fast_end, 1, false);
-  if (range > fast_end) stage_slow(fast_end, range, 0, true);
+    };
+    if (m > 1 && !use_perm) stage_slow(0, fast_end, 1, false);
+    if (range > fast_end) stage_slow(fast_end, range, 0, true);
 
-  // (7) The wave's metadata into LDS (the zero points are checked on the way:
-  // the unpack subtracts integers with |z| <= 1023 exactly), then any groups
-  // beyond the first 16.
-  bool z_ok = true;
-  auto meta_store = [&](int j, uint4 v) {
-    reinterpret_cast<uint4*>(wmeta)[j] = v;
-    if ((j & 15) < kMetaBytes / 32) {  // a piece of zero points
-      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int h = 0; h < 8; ++h) {
-        const float z = static_cast<float>(
-            __builtin_bit_cast(_Float16, static_cast<uint16_t>(w[h >> 1] >> (16 * (h & 1)))));
-        z_ok = z_ok && z == truncf(z) && fabsf(z) <= 1023.f;
-      }
-    }
-  };
-#pragma unroll
-  for (int u = 0; u < kFastRounds; ++u) {
-    if (u >= rounds) break;
-    if (u * 64 + lane < fpieces) meta_store(u * 64 + lane, mv[u]);
+      // (7) Metadata pieces past the first four rounds (groups beyond the first
+    // 16), stored and checked as in (3').
+    for (int j = 4 * 64 + lane; j < fpieces; j += 64)
+      meta_store(j, ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16));
+    exact = __all(z_bad == 0);
   }
-  for (int j = 4 * 64 + lane; j < fpieces; j += 64)
-    meta_store(j, ldg16(ftile + static_cast<int64_t>(fg0 + (j >> 4)) * frb + (j & 15) * 16));
-  const bool exact = __all(z_ok);
 
-  // Zero points that are not all integers of magnitude <= 1023 (rare): each
-  // staged one becomes zi = rint(z) clamped to [-1023, 1023] for the unpack,
-  // and the wave's correction records receive z - zi per row (in the scales'
-  // row order) and, per token, the sum of the group's staged activations.
-  uint8_t* wfix = reinterpret_cast<uint8_t*>(xs16) + ITEM(int32_t, fix_offset);
+  // Zero points that are not all integers of magnitude <= 1023 (rare): the
+  // group start and fold of this wave take the `fixed` path.
   const bool fixed = !exact;
-  if (fixed) {
-    const int ngr = fpieces >> 4;
-    const int ia = (lane & 15) * 4 + (lane >> 4);                              // row `lane`, zero-point order
-    const int id = ((lane >> 2) & 3) * 16 + 4 * (lane >> 4) + (lane & 3);      // and scale order
-    for (int j = 0; j < ngr; ++j) {
-      _Float16* zp = reinterpret_cast<_Float16*>(wmeta + j * kMetaBytes) + ia;
-      const float z = static_cast<float>(*zp);
-      const float zi = fminf(fmaxf(rintf(z), -1023.f), 1023.f);
-      *zp = static_cast<_Float16>(zi);
-      reinterpret_cast<float*>(wfix + j * kFixBytes)[id] = z - zi;
-    }
-    for (int task = lane; task < m * ngr; task += 64) {
-      const int t = task / ngr, j = task - t * ngr;
-      const int k1 = min((j + 1) * kGroup, range);
-      float sum = 0.f;
-      for (int kk = j * kGroup; kk < k1; kk += 8) {
-        const h8 v = __builtin_bit_cast(h8, *reinterpret_cast<const uint4*>(xs16 + t * range + kk));
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sum += static_cast<float>(v[e]);
-      }
-      reinterpret_cast<float*>(wfix + j * kFixBytes)[kTileRows + t] = sum;
-    }
-  }
 
   // ---- Main loop over the wave's block range.
   f4 acc[4];
@@ -720,19 +770,24 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     const __amdgpu_buffer_rsrc_t rs = tile_rsrc(ftile, ftb);
     // this lane's activation fragment of block-local chunk 0 (token lane%16,
     // or the zero row; channel quarter lane/16), relative to the staged range
-    const uint32_t* xlane = reinterpret_cast<const uint32_t*>(xs16) +
-                            ((tok < m ? tok : m) * range + 8 * (lane >> 4)) / 2 + (fcb - c0) * 16;
+    const uint32_t* xlane = reinterpret_cast<const uint32_t*>(tok < m ? xs16 + tok * range : zs16) +
+                            4 * (lane >> 4) + (fcb - c0) * 16;
     // metadata of block-local group 0 (only groups >= fl0 / 4 are read)
     const uint8_t* meta = wmeta - fg0 * kMetaBytes;
-    // correction record of block-local group 0 (read only when `fixed`)
-    const uint8_t* fix = wfix - fg0 * kFixBytes;
-    switch (fb) {
-      case 2: run_segment<2>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
-      case 3: run_segment<3>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
-      case 4: run_segment<4>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
-      case 8: run_segment<8>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
-      default: run_segment<16>(rs, frb, fl0, fl1, xlane, meta, fix, fixed, lane, sa, sb, acc); break;
-    }
+    auto run = [&](auto fixed_tag) {
+      constexpr bool F = decltype(fixed_tag)::value;
+      switch (fb) {
+        case 2: run_segment<2, F>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        case 3: run_segment<3, F>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        case 4: run_segment<4, F>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        case 8: run_segment<8, F>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+        default: run_segment<16, false>(rs, frb, fl0, fl1, xlane, meta, lane, sa, sb, acc); break;
+      }
+    };
+    if (fixed)
+      run(std::true_type{});
+    else
+      run(std::false_type{});
   }
 
   // Reduce the waves' partial sums (fixed order).  MFMA result layout: lane l
@@ -932,7 +987,7 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
     g.rows_pad = L.n_tiles * kTileRows;
     g.S = p.S;
     g.wave_lds = static_cast<int32_t>(gemv_wave_lds_bytes(p, m));
-    g.fix_offset = static_cast<int32_t>(gemv_wave_fix_offset(p, m));
+    g.zero_offset = static_cast<int32_t>(gemv_zero_offset(p, m));
     g.n_tiles = L.n_tiles;
     g.n_chunks = L.n_chunks;
     g.tiles_magic = div_magic(static_cast<uint32_t>(L.n_tiles));

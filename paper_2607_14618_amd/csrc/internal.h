@@ -14,10 +14,6 @@ constexpr int kChunk = POLYQ_QUANTUM;       // channels per chunk
 constexpr int kGroup = POLYQ_GROUP;         // channels per quantization group
 constexpr int kChunksPerGroup = kGroup / kChunk;
 constexpr int kMetaBytes = kTileRows * 4;   // {fp16 s, fp16 z} per row of a tile
-// Decode GEMV, per staged group of a wave whose zero points are not all small
-// integers: fp32 z - rint(z) of the tile's 64 rows, then the fp32 sums of the
-// group's activations for up to 16 tokens.
-constexpr int kFixBytes = kTileRows * 4 + 16 * 4;
 
 // Decode GEMV launch plan: the work-groups of one linear are n_tiles x S, each
 // of W waves; wave w (0 <= w < S * W, across the tile's splits) covers the
@@ -93,11 +89,11 @@ size_t gemv_workspace_for(const polyq_layout& L, int32_t m, const GemvPlan& p);
 // True when `L` is exactly what polyq_plan produces for its own n, k, blocks.
 bool layout_is_valid(const polyq_layout* L);
 
-// LDS bytes of one GEMV wave's staging region, and of a work-group, for plan p
-// and m tokens.
+// LDS bytes of one GEMV wave's staging region (x' of m tokens, then group
+// metadata), the offset of the work-group's shared zero row (after the W wave
+// regions) and the LDS of a work-group, for plan p and m tokens.
 size_t gemv_wave_lds_bytes(const GemvPlan& p, int32_t m);
-// Offset of the zero-point correction area inside a wave's staging region.
-size_t gemv_wave_fix_offset(const GemvPlan& p, int32_t m);
+size_t gemv_zero_offset(const GemvPlan& p, int32_t m);
 size_t gemv_lds_bytes(const GemvPlan& p, int32_t m);
 
 // Block accessor of a layout for wave_range (host side).

@@ -98,22 +98,22 @@ bool layout_is_valid(const polyq_layout* L) {
   return memcmp(&ref, L, sizeof(ref)) == 0;
 }
 
-size_t gemv_wave_fix_offset(const GemvPlan& p, int32_t m) {
-  // x' rows + a zero row of the wave's channels (16-byte aligned), then its
-  // group metadata
-  return static_cast<size_t>(align_up(static_cast<int64_t>(p.lds_chunks) * kChunk * (m + 1) * 2, 16)) +
+size_t gemv_wave_lds_bytes(const GemvPlan& p, int32_t m) {
+  // x' rows of the wave's channels (16-byte aligned), then its group metadata
+  return static_cast<size_t>(align_up(static_cast<int64_t>(p.lds_chunks) * kChunk * m * 2, 16)) +
          static_cast<size_t>(p.lds_groups) * kMetaBytes;
 }
 
-size_t gemv_wave_lds_bytes(const GemvPlan& p, int32_t m) {
-  // ... then the zero-point corrections of its groups
-  return gemv_wave_fix_offset(p, m) + static_cast<size_t>(p.lds_groups) * kFixBytes;
+size_t gemv_zero_offset(const GemvPlan& p, int32_t m) {
+  return static_cast<size_t>(p.W) * gemv_wave_lds_bytes(p, m);
 }
 
 size_t gemv_lds_bytes(const GemvPlan& p, int32_t m) {
-  // every wave's staging region; reused for the reduction
+  // every wave's staging region and the work-group's zero row; the start is
+  // reused for the reduction
+  const size_t zero = static_cast<size_t>(align_up(static_cast<int64_t>(p.lds_chunks) * kChunk * 2, 16));
   const size_t red = static_cast<size_t>(p.W) * m * kTileRows * 4;
-  return std::max(static_cast<size_t>(p.W) * gemv_wave_lds_bytes(p, m), red);
+  return std::max(gemv_zero_offset(p, m) + zero, red);
 }
 
 // Group records of b <= 8 blocks that overlap the chunk range [lo, hi).
