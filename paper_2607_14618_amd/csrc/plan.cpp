@@ -15,7 +15,9 @@ bool bits_in_palette(int b) { return b == 2 || b == 3 || b == 4 || b == 8 || b =
 constexpr int kWavesPerWG = 4;
 constexpr int kResidentWGs = 768;        // 256 CUs x 3 co-resident 4-wave work-groups (<= 168 VGPRs)
 constexpr int kMinChunksPerWave = 4;      // below this the per-wave setup dominates
-constexpr size_t kLdsBudget = 64 * 1024;  // per work-group, one token
+// Per work-group, one token: a third of the CU's 160 KB, so that the three
+// work-groups the VGPR budget allows stay co-resident.
+constexpr size_t kLdsBudget = (160 * 1024 / 3) & ~static_cast<size_t>(15);
 // With several tokens the staged activations grow with M; a larger budget
 // (two work-groups per CU instead of three) keeps the split count, and with
 // it the number of work-group rounds, down.
