@@ -124,6 +124,26 @@ def test_gemv_non_integer_zero_points(m, blocks):
     assert_parity(y, y_ref, bound, f"non-integer z m={m}")
 
 
+@pytest.mark.parametrize("zval", [1023.0, -1023.0, 0.0, 1024.0, -1024.0, 1023.5, 2.0 ** -24, 65504.0])
+@pytest.mark.parametrize("m", [1, 4])
+def test_gemv_zero_points_at_the_exact_range_edges(zval, m):
+    """One group of every row holds z = zval, the others integers: +-1023 and 0 stay
+    on the exact path, 1024, -1024, 1023.5, the smallest subnormal and 65504 need the
+    correction (the packed fp16 test of the zero points decides per wave)."""
+    blocks = [(2, 256), (3, 128), (4, 128), (8, 128)]
+    k = sum(l for _, l in blocks)
+    lin = random_quant_linear(128, k, blocks, seed=31, mode="codes")
+    z = lin.zeros.float().numpy().copy()
+    z[:, 1] = zval
+    lin.zeros = torch.from_numpy(z.astype(np.float16))
+    pl = packed_linear(lin)
+    x = _x(m, k, 5)
+    y = pl.decode(x.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, x)
+    assert_parity(y, y_ref, bound, f"z={zval} m={m}")
+
+
 @pytest.mark.parametrize("m", [1, 3])
 def test_gemv_out_of_range_permutation_entries_read_zero(m):
     """A permutation entry outside [0, k) must not fault; its channel reads 0."""
