@@ -820,15 +820,31 @@ __global__ __launch_bounds__(256) void permute_rows_kernel(const int32_t* __rest
   out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
 }
 
-// y = partial[0] + partial[1] + ... (in split order), `count` elements each.
+// y = partial[0] + partial[1] + ... (in split order), `count` elements each,
+// four consecutive elements per thread (16-byte accesses when count is a
+// multiple of 4 and y is 16-byte aligned; the partials always are).
 __global__ __launch_bounds__(256) void sum_splits_kernel(const float* __restrict__ partial,
                                                          float* __restrict__ y, int splits,
                                                          int64_t count) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * 4;
   if (i >= count) return;
-  float v = partial[i];
-  for (int s = 1; s < splits; ++s) v += partial[s * count + i];
-  y[i] = v;
+  if ((count & 3) == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0) {
+    float4 v = *reinterpret_cast<const float4*>(partial + i);
+    for (int s = 1; s < splits; ++s) {
+      const float4 w = *reinterpret_cast<const float4*>(partial + s * count + i);
+      v.x += w.x;
+      v.y += w.y;
+      v.z += w.z;
+      v.w += w.w;
+    }
+    *reinterpret_cast<float4*>(y + i) = v;
+  } else {
+    for (int64_t j = i; j < count && j < i + 4; ++j) {
+      float v = partial[j];
+      for (int s = 1; s < splits; ++s) v += partial[s * count + j];
+      y[j] = v;
+    }
+  }
 }
 
 }  // namespace
@@ -1017,7 +1033,7 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
     hipLaunchKernelGGL(gemm_kernel<1>, dim3(static_cast<unsigned>(wg)), dim3(256), 0, st, a);
   if (splits > 1) {
     const int64_t n_el = static_cast<int64_t>(m) * items[0].layout->n;
-    hipLaunchKernelGGL(sum_splits_kernel, dim3(static_cast<unsigned>((n_el + 255) / 256)), dim3(256), 0, st,
+    hipLaunchKernelGGL(sum_splits_kernel, dim3(static_cast<unsigned>((n_el + 1023) / 1024)), dim3(256), 0, st,
                        a.partial, items[0].y, splits, n_el);
   }
   return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
