@@ -90,3 +90,21 @@ def test_gemv_plans_up_to_the_maximum_k(k, m):
     part = ws - 256
     assert part > 0 and part % (m * 64 * 4) == 0
     assert 1 < part // (m * 64 * 4) <= 1024
+
+
+@pytest.mark.parametrize("m,want", [(0, 1), (-3, 1), (17, 5)])
+def test_gemv_token_count_is_checked_before_any_launch(m, want):
+    """m outside [1, 16] is refused on the host (POLYQ_ERR_ARG for m < 1,
+    POLYQ_ERR_CAPACITY above 16): no device pointer is touched and nothing is
+    launched (there is no GPU here, so a launch would report POLYQ_ERR_DEVICE)."""
+    L = pq.plan(64, 64, [(2, 64)])
+    fake = ctypes.c_void_p(1 << 20)  # aligned, never dereferenced on the host
+    got = pq.lib().polyq_gemv(ctypes.byref(L), fake, None, fake, m, fake, None, 0, None)
+    assert got == want
+
+
+@pytest.mark.parametrize("m", [0, -1])
+def test_gemm_empty_token_count_is_refused_before_any_launch(m):
+    L = pq.plan(64, 64, [(2, 64)])
+    fake = ctypes.c_void_p(1 << 20)
+    assert pq.lib().polyq_gemm(ctypes.byref(L), fake, None, fake, m, fake, None, 0, None) == 1
