@@ -136,6 +136,26 @@ polyq_status polyq_pack(const polyq_layout* layout, const uint16_t* codes, const
                         const uint16_t* zeros, void* packed, void* stream);
 
 /*
+ * polyq_pack_rows -- polyq_pack with the output rows reordered: the producer
+ * side of the cross-layer permutation merge (Sec. 4.3, Eq. 10).  A consumer
+ * that wants its input in basis P (its own channel permutation) receives it
+ * without an activation shuffle when the producer's weight is stored as
+ * W P^T, i.e. with its output rows permuted by P at compile time.
+ *   row_perm  int32 [n] (device, not NULL): packed row r holds source row
+ *             row_perm[r] of codes, scales and zeros, so polyq_gemv /
+ *             polyq_gemm on the packed buffer produce y'[i][r] =
+ *             y[i][row_perm[r]].  Passing the consumer's perm (consumer k ==
+ *             producer n) makes y' the consumer's clustered input (call it
+ *             with perm = NULL).  An entry outside [0, n) packs a zero row
+ *             (codes, scales and zeros 0): its output is 0.
+ *   Other arguments, layout and errors as for polyq_pack (NULL row_perm:
+ *   POLYQ_ERR_ARG).  codes, scales, zeros and row_perm are read only.
+ */
+polyq_status polyq_pack_rows(const polyq_layout* layout, const uint16_t* codes,
+                             const uint16_t* scales, const uint16_t* zeros,
+                             const int32_t* row_perm, void* packed, void* stream);
+
+/*
  * polyq_unpack -- inverse of polyq_pack: writes codes [n][k], scales and zeros
  * [n][n_groups] (fp16 bits) from a packed buffer.  Any of the three outputs may
  * be NULL to skip it.  Codes of b <= 8 come back masked to b bits.

@@ -18,6 +18,9 @@ What it computes (fp64, from the *stored* values):
 * Sec. 4.2: one block kernel per bit block, all accumulating into one output:
   y[m, n] = sum over all clustered channels k' of w_hat[n, k'] * x'[m, k'].
 * Eq. 7: the realized budget B_real = (1/d_in) * sum_j b_j.
+* Eq. 10 (Sec. 4.3): a producer whose consumer wants its input in basis P
+  stores W P^T, its output rows reordered by P, and so emits y[:, P] with no
+  activation shuffle (``linear_emitting``).
 
 Every function below is the plain definition, computed with NumPy (a BLAS
 matmul is the only library step) or with scalar ``math.fsum`` loops.
@@ -138,6 +141,27 @@ def linear(blocks: Blocks, codes, scales, zeros, perm, x, rows: Optional[np.ndar
         y[:, a:a + r.size] = xp @ w.T
         bound[:, a:a + r.size] = axp @ np.abs(w).T
     return y, bound
+
+
+def linear_emitting(blocks: Blocks, codes, scales, zeros, perm, x, out_perm
+                    ) -> Tuple[np.ndarray, np.ndarray]:
+    """The producer side of Eq. 10 (Sec. 4.3): the stored weight is W P^T, so
+    stored output row r is original row out_perm[r] and the product is
+    y'[m, r] = y[m, out_perm[r]].  An entry outside [0, n) stores a zero row
+    (codes, scale and zero point 0), whose output is 0.  Returns (y', bound)
+    as ``linear`` does, computed on the reordered stored rows.
+    """
+    codes = np.asarray(codes).view(np.uint16)
+    scales = np.asarray(scales)
+    zeros = np.asarray(zeros)
+    n = codes.shape[0]
+    out_perm = np.asarray(out_perm, dtype=np.int64)
+    valid = (out_perm >= 0) & (out_perm < n)
+    src = np.where(valid, out_perm, 0)
+    codes_s = np.where(valid[:, None], codes[src], 0).astype(np.uint16)
+    scales_s = np.where(valid[:, None], scales[src], 0).astype(scales.dtype) if scales.size else scales
+    zeros_s = np.where(valid[:, None], zeros[src], 0).astype(zeros.dtype) if zeros.size else zeros
+    return linear(blocks, codes_s, scales_s, zeros_s, perm, x)
 
 
 def linear_scalar(blocks: Blocks, codes, scales, zeros, perm, x) -> np.ndarray:

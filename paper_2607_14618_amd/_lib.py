@@ -28,7 +28,7 @@ STATUS = {0: "POLYQ_OK", 1: "POLYQ_ERR_ARG", 2: "POLYQ_ERR_BITS", 3: "POLYQ_ERR_
           7: "POLYQ_ERR_DEVICE"}
 
 # every symbol include/polyq.h declares
-EXPORTS = ("polyq_plan", "polyq_pack", "polyq_unpack", "polyq_permute", "polyq_gemv_workspace_bytes",
+EXPORTS = ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq_permute", "polyq_gemv_workspace_bytes",
            "polyq_gemv", "polyq_gemv_batch_workspace_bytes", "polyq_gemv_batch",
            "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_gemm_batch_workspace_bytes",
            "polyq_gemm_batch", "polyq_status_str")
@@ -92,6 +92,7 @@ def lib() -> ctypes.CDLL:
             lp = ctypes.POINTER(Layout)
             L.polyq_plan.argtypes = [i32, i32, ctypes.POINTER(Block), i32, lp]
             L.polyq_pack.argtypes = [lp, vp, vp, vp, vp, vp]
+            L.polyq_pack_rows.argtypes = [lp, vp, vp, vp, vp, vp, vp]
             L.polyq_unpack.argtypes = [lp, vp, vp, vp, vp, vp]
             L.polyq_permute.argtypes = [vp, vp, vp, i32, i32, vp]
             L.polyq_gemv_workspace_bytes.argtypes = [lp, i32]
@@ -109,7 +110,7 @@ def lib() -> ctypes.CDLL:
             L.polyq_gemm_batch.argtypes = [ip, i32, i32, vp, sz, vp]
             L.polyq_status_str.argtypes = [ctypes.c_int]
             L.polyq_status_str.restype = ctypes.c_char_p
-            for name in ("polyq_plan", "polyq_pack", "polyq_unpack", "polyq_permute",
+            for name in ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq_permute",
                          "polyq_gemv", "polyq_gemv_batch", "polyq_gemm", "polyq_gemm_batch"):
                 getattr(L, name).restype = ctypes.c_int
             _lib = L
@@ -188,6 +189,27 @@ def pack(layout: Layout, codes: torch.Tensor, scales: torch.Tensor, zeros: torch
     _check(lib().polyq_pack(ctypes.byref(layout), _ptr(codes), _ptr(scales) if layout.n_groups else None,
                             _ptr(zeros) if layout.n_groups else None, _ptr(packed), _stream(dev)),
            "polyq_pack")
+    return packed
+
+
+def pack_rows(layout: Layout, codes: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor,
+              row_perm: torch.Tensor) -> torch.Tensor:
+    """Packed buffer whose row r is source row row_perm[r] (Eq. 10: the layer then
+    emits y'[:, r] = y[:, row_perm[r]], a consumer's clustered input when
+    row_perm is that consumer's permutation)."""
+    dev = _need_cuda(codes, scales, zeros, row_perm)
+    _as_u16(codes), _as_u16(scales), _as_u16(zeros)
+    if tuple(codes.shape) != (layout.n, layout.k):
+        raise ValueError(f"codes shape {tuple(codes.shape)} != ({layout.n}, {layout.k})")
+    if tuple(scales.shape) != (layout.n, layout.n_groups) or scales.shape != zeros.shape:
+        raise ValueError("scales/zeros must be [n][n_groups]")
+    if row_perm.dtype != torch.int32 or tuple(row_perm.shape) != (layout.n,) or not row_perm.is_contiguous():
+        raise ValueError(f"row_perm must be contiguous int32 [{layout.n}]")
+    packed = _aligned_empty(layout.packed_bytes, dev)
+    _check(lib().polyq_pack_rows(ctypes.byref(layout), _ptr(codes), _ptr(scales) if layout.n_groups else None,
+                                 _ptr(zeros) if layout.n_groups else None, _ptr(row_perm), _ptr(packed),
+                                 _stream(dev)),
+           "polyq_pack_rows")
     return packed
 
 

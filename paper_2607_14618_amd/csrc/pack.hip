@@ -1,7 +1,9 @@
 // Pack / unpack of the clustered quantized weight (Sec. 4.1: the clustered
 // weight P W is materialized once, at compile time) and the explicit activation
 // shuffle of Eq. 9.  Memory-bound helper kernels; the packed layout is the one
-// declared in include/polyq.h.
+// declared in include/polyq.h.  Packing can also reorder the output rows
+// (Sec. 4.3, Eq. 10): packed row r then holds source row row_perm[r], so the
+// layer emits its output directly in a consumer's clustered channel basis.
 #include <hip/hip_runtime.h>
 
 #include "codec.h"
@@ -16,12 +18,20 @@ inline unsigned grid_for(int64_t items) {
   return static_cast<unsigned>((items + kThreads - 1) / kThreads);
 }
 
+// Source row of packed row R (R < n): R itself, or row_perm[R]; -1 (a zero
+// row) for an entry outside [0, n).
+__device__ __forceinline__ int source_row(const int32_t* __restrict__ row_perm, int R, int n) {
+  if (row_perm == nullptr) return R;
+  const int src = row_perm[R];
+  return static_cast<unsigned>(src) < static_cast<unsigned>(n) ? src : -1;
+}
+
 // One thread per (tile, chunk, lane slice): gathers the slice's 4 rows x 8
 // channels from the row-major codes and writes its 4*B bytes.
 template <int B>
 __global__ __launch_bounds__(kThreads) void pack_codes_kernel(
-    const uint16_t* __restrict__ codes, int n, int k, int k0, int nch, int n_tiles,
-    int64_t tile_bytes, int64_t record_bytes, uint8_t* __restrict__ region) {
+    const uint16_t* __restrict__ codes, const int32_t* __restrict__ row_perm, int n, int k, int k0,
+    int nch, int n_tiles, int64_t tile_bytes, int64_t record_bytes, uint8_t* __restrict__ region) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (idx >= static_cast<int64_t>(n_tiles) * nch * 64) return;
   const int lane = static_cast<int>(idx % 64);
@@ -31,8 +41,9 @@ __global__ __launch_bounds__(kThreads) void pack_codes_kernel(
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int R = t * 64 + 16 * r + (lane % 16);
-    if (R < n) {
-      const uint4 u = *reinterpret_cast<const uint4*>(codes + static_cast<int64_t>(R) * k + k0 +
+    const int src = R < n ? source_row(row_perm, R, n) : -1;
+    if (src >= 0) {
+      const uint4 u = *reinterpret_cast<const uint4*>(codes + static_cast<int64_t>(src) * k + k0 +
                                                       c * 32 + 8 * (lane / 16));
       const uint32_t wd[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
@@ -82,15 +93,17 @@ __global__ __launch_bounds__(kThreads) void unpack_codes_kernel(
 
 // One thread per (row, block-local group): scale and zero point into the group's metadata.
 __global__ __launch_bounds__(kThreads) void pack_meta_kernel(
-    const uint16_t* __restrict__ scales, const uint16_t* __restrict__ zeros, int n, int G, int g0,
-    int ng, int64_t tile_bytes, int64_t record_bytes, int rows_total, uint8_t* __restrict__ region) {
+    const uint16_t* __restrict__ scales, const uint16_t* __restrict__ zeros,
+    const int32_t* __restrict__ row_perm, int n, int G, int g0, int ng, int64_t tile_bytes,
+    int64_t record_bytes, int rows_total, uint8_t* __restrict__ region) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (idx >= static_cast<int64_t>(rows_total) * ng) return;
   const int R = static_cast<int>(idx % rows_total);
   const int g = static_cast<int>(idx / rows_total);
   uint16_t sv = 0, zv = 0;
-  if (R < n) {
-    const int64_t at = static_cast<int64_t>(R) * G + g0 + g;
+  const int src = R < n ? source_row(row_perm, R, n) : -1;
+  if (src >= 0) {
+    const int64_t at = static_cast<int64_t>(src) * G + g0 + g;
     sv = scales[at];
     zv = zeros[at];
   }
@@ -124,12 +137,12 @@ __global__ __launch_bounds__(kThreads) void permute_kernel(const int32_t* __rest
 }
 
 template <int B>
-void launch_pack(const polyq_layout& L, int i, const uint16_t* codes, uint8_t* region,
-                 hipStream_t st) {
+void launch_pack(const polyq_layout& L, int i, const uint16_t* codes, const int32_t* row_perm,
+                 uint8_t* region, hipStream_t st) {
   const int nch = L.block[i].len / kChunk;
   hipLaunchKernelGGL(pack_codes_kernel<B>,
                      dim3(grid_for(static_cast<int64_t>(L.n_tiles) * nch * 64)), dim3(kThreads), 0,
-                     st, codes, L.n, L.k, L.k_begin[i], nch, L.n_tiles, L.tile_bytes[i],
+                     st, codes, row_perm, L.n, L.k, L.k_begin[i], nch, L.n_tiles, L.tile_bytes[i],
                      L.record_bytes[i], region);
 }
 
@@ -148,9 +161,9 @@ void launch_unpack(const polyq_layout& L, int i, const uint8_t* region, uint16_t
 
 using namespace polyq;
 
-extern "C" polyq_status polyq_pack(const polyq_layout* layout, const uint16_t* codes,
-                                   const uint16_t* scales, const uint16_t* zeros, void* packed,
-                                   void* stream) {
+namespace {
+polyq_status pack_impl(const polyq_layout* layout, const uint16_t* codes, const uint16_t* scales,
+                       const uint16_t* zeros, const int32_t* row_perm, void* packed, void* stream) {
   if (!layout_is_valid(layout)) return POLYQ_ERR_ARG;
   const polyq_layout& L = *layout;
   if (codes == nullptr || packed == nullptr) return POLYQ_ERR_ARG;
@@ -163,21 +176,36 @@ extern "C" polyq_status polyq_pack(const polyq_layout* layout, const uint16_t* c
   for (int i = 0; i < L.nblocks; ++i) {
     uint8_t* region = base + L.block_offset[i];
     switch (L.block[i].bits) {
-      case 2: launch_pack<2>(L, i, codes, region, st); break;
-      case 3: launch_pack<3>(L, i, codes, region, st); break;
-      case 4: launch_pack<4>(L, i, codes, region, st); break;
-      case 8: launch_pack<8>(L, i, codes, region, st); break;
-      case 16: launch_pack<16>(L, i, codes, region, st); break;
+      case 2: launch_pack<2>(L, i, codes, row_perm, region, st); break;
+      case 3: launch_pack<3>(L, i, codes, row_perm, region, st); break;
+      case 4: launch_pack<4>(L, i, codes, row_perm, region, st); break;
+      case 8: launch_pack<8>(L, i, codes, row_perm, region, st); break;
+      case 16: launch_pack<16>(L, i, codes, row_perm, region, st); break;
       default: return POLYQ_ERR_BITS;
     }
     if (L.block[i].bits <= 8) {
       const int ng = (L.block[i].len + kGroup - 1) / kGroup;
       hipLaunchKernelGGL(pack_meta_kernel, dim3(grid_for(static_cast<int64_t>(rows_total) * ng)),
-                         dim3(kThreads), 0, st, scales, zeros, L.n, L.n_groups, L.group_begin[i],
+                         dim3(kThreads), 0, st, scales, zeros, row_perm, L.n, L.n_groups, L.group_begin[i],
                          ng, L.tile_bytes[i], L.record_bytes[i], rows_total, region);
     }
   }
   return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
+}
+
+}  // namespace
+
+extern "C" polyq_status polyq_pack(const polyq_layout* layout, const uint16_t* codes,
+                                   const uint16_t* scales, const uint16_t* zeros, void* packed,
+                                   void* stream) {
+  return pack_impl(layout, codes, scales, zeros, nullptr, packed, stream);
+}
+
+extern "C" polyq_status polyq_pack_rows(const polyq_layout* layout, const uint16_t* codes,
+                                        const uint16_t* scales, const uint16_t* zeros,
+                                        const int32_t* row_perm, void* packed, void* stream) {
+  if (row_perm == nullptr) return POLYQ_ERR_ARG;
+  return pack_impl(layout, codes, scales, zeros, row_perm, packed, stream);
 }
 
 extern "C" polyq_status polyq_unpack(const polyq_layout* layout, const void* packed,

@@ -14,17 +14,25 @@ class PackedLinear:
 
     Built once from logical codes (clustered order), fp16 scales and zeros and
     the permutation; ``decode`` runs polyq_gemv and ``prefill`` runs polyq_gemm.
+    ``out_perm`` (optional, [n]) stores the output rows in another basis
+    (polyq_pack_rows): the layer then emits y[:, out_perm], which is a
+    consumer's clustered input when out_perm is that consumer's permutation.
     """
 
     def __init__(self, blocks: Sequence[Tuple[int, int]], codes: torch.Tensor,
-                 scales: torch.Tensor, zeros: torch.Tensor, perm, device="cuda"):
+                 scales: torch.Tensor, zeros: torch.Tensor, perm, device="cuda", out_perm=None):
         n, k = codes.shape
         self.layout = _lib.plan(n, k, blocks)
         dev = torch.device(device)
         codes = codes.to(dev).contiguous()
         scales = scales.to(dev, torch.float16).contiguous()
         zeros = zeros.to(dev, torch.float16).contiguous()
-        self.packed = _lib.pack(self.layout, codes, scales, zeros)
+        if out_perm is None:
+            self.packed = _lib.pack(self.layout, codes, scales, zeros)
+        else:
+            # Eq. 10: output rows stored in a consumer's basis (y'[:, r] = y[:, out_perm[r]])
+            row_perm = torch.as_tensor(np.asarray(out_perm, dtype=np.int32)).to(dev).contiguous()
+            self.packed = _lib.pack_rows(self.layout, codes, scales, zeros, row_perm)
         self.perm = torch.as_tensor(np.asarray(perm, dtype=np.int32)).to(dev)
         self.n, self.k = n, k
 

@@ -108,3 +108,12 @@ def test_gemm_empty_token_count_is_refused_before_any_launch(m):
     L = pq.plan(64, 64, [(2, 64)])
     fake = ctypes.c_void_p(1 << 20)
     assert pq.lib().polyq_gemm(ctypes.byref(L), fake, None, fake, m, fake, None, 0, None) == 1
+
+
+def test_pack_rows_refuses_a_missing_row_perm_before_any_launch():
+    # host-side check: no device pointer is touched (the ones passed are never
+    # dereferenced), so this runs without a GPU
+    layout = pq.plan(64, 32, [(4, 32)])
+    fake = ctypes.c_void_p(256)
+    st = pq.lib().polyq_pack_rows(ctypes.byref(layout), fake, fake, fake, None, fake, None)
+    assert pq.lib().polyq_status_str(st).decode() != "" and st != 0

@@ -305,3 +305,52 @@ def test_check_tolerance_rules():
     assert not oracle.check_tolerance(np.array([[1.02, 0.0, 2.0]]), y_ref, bound)[0]
     assert not oracle.check_tolerance(np.array([[1.0, 1e-30, 2.0]]), y_ref, bound)[0]
     assert not oracle.check_tolerance(np.array([[np.nan, 0.0, 2.0]]), y_ref, bound)[0]
+
+
+def _emit_pair(seed):
+    prod = random_quant_linear(96, 160, [(2, 64), (4, 32), (8, 32), (16, 32)], seed=seed, mode="codes")
+    cons = random_quant_linear(64, 96, [(2, 32), (4, 32), (16, 32)], seed=seed + 1, mode="codes")
+    return prod, cons
+
+
+def test_eq10_emission_removes_the_consumer_shuffle():
+    # Eq. 10: A (W P^T)(P W') = (A W) W'.  The consumer fed the emitting
+    # producer's output as already-clustered input must equal the consumer
+    # applying its own Eq. 9 gather to the producer's plain output.  A wrong
+    # direction (P^-1 instead of P) breaks the identity.
+    prod, cons = _emit_pair(4100)
+    p2 = np.asarray(cons.perm, dtype=np.int64)
+    assert not np.array_equal(p2[p2], np.arange(p2.size))  # not an involution
+    x = np.random.default_rng(5).standard_normal((3, 160))
+    y1, _ = oracle.linear(prod.blocks, _codes(prod), _np(prod.scales), _np(prod.zeros), prod.perm, x)
+    y1e, _ = oracle.linear_emitting(prod.blocks, _codes(prod), _np(prod.scales), _np(prod.zeros),
+                                    prod.perm, x, p2)
+    assert np.array_equal(y1e, y1[:, p2])
+    c2 = (cons.blocks, _codes(cons), _np(cons.scales), _np(cons.zeros))
+    shuffled, _ = oracle.linear(*c2, cons.perm, y1)
+    merged, _ = oracle.linear(*c2, None, y1e)
+    np.testing.assert_allclose(merged, shuffled, rtol=1e-12, atol=1e-12)
+    inv = np.argsort(p2)
+    y1w, _ = oracle.linear_emitting(prod.blocks, _codes(prod), _np(prod.scales), _np(prod.zeros),
+                                    prod.perm, x, inv)
+    wrong, _ = oracle.linear(*c2, None, y1w)
+    assert not np.allclose(wrong, shuffled, rtol=1e-6)
+
+
+def test_eq10_emission_of_an_all_16bit_layer_is_the_fp16_product_of_reordered_rows():
+    # special case reducing to a library matmul: W16[out_perm] x' with fp16
+    # weights; entries outside [0, n) give zero rows, so zero outputs
+    n, k = 40, 64
+    lin = random_quant_linear(n, k, [(16, 64)], seed=4200, mode="gauss")
+    out = np.random.default_rng(7).permutation(n).astype(np.int64)
+    out[3], out[11] = -1, n
+    x = np.random.default_rng(8).standard_normal((2, k))
+    y, bound = oracle.linear_emitting(lin.blocks, _codes(lin), _np(lin.scales), _np(lin.zeros),
+                                      lin.perm, x, out)
+    w16 = torch.from_numpy(_codes(lin).view(np.float16).astype(np.float64))
+    xp = torch.from_numpy(x)[:, torch.as_tensor(np.asarray(lin.perm, dtype=np.int64))]
+    valid = torch.as_tensor((out >= 0) & (out < n))
+    rows = w16[torch.as_tensor(np.where((out >= 0) & (out < n), out, 0))] * valid[:, None]
+    want = (xp @ rows.T).numpy()
+    np.testing.assert_allclose(y, want, rtol=1e-13, atol=1e-13)
+    assert np.all(y[:, [3, 11]] == 0) and np.all(bound[:, [3, 11]] == 0)
