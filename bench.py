@@ -13,7 +13,9 @@ Infinity Cache cannot serve the weights.
 + fp16 scale/zero, Eq. 7 budget) / step time.  The same JSON line carries the
 roofline of the GEMV kernel (bytes per launch / average launch time from HIP
 events on the launch stream), the prefill GEMM at M=512 (4.0-bit mix, bf16) as
-a secondary figure, and the fp64 CPU oracle timed on a bounded sample.
+a secondary figure, the same decode step with the gate/up -> down edge merged
+(Eq. 10: gate and up packed to emit in down's basis, down reading clustered
+activations), and the fp64 CPU oracle timed on a bounded sample.
 
 Other modes (each prints its own single JSON line):
   --sweep        budget sweep 3/4/5/6 b x M in {1, 4, 16} on the Llama2-13B layer (M > 1 also
@@ -43,9 +45,10 @@ def _args():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--variant", choices=["G", "P", "S"], default="G",
+    p.add_argument("--variant", choices=["G", "P", "S", "M"], default="G",
                    help="G: permutation gathered in-kernel; P: activations pre-permuted; "
-                        "S: explicit polyq_permute inside every step, then clustered x")
+                        "S: explicit polyq_permute inside every step, then clustered x; "
+                        "M: G with gate/up emitting in down's basis (Eq. 10), down on clustered x")
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--no-prefill", action="store_true", help="skip the prefill GEMM figure")
@@ -88,6 +91,9 @@ def _log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+EMIT_TO_DOWN = ("gate_proj", "up_proj")   # producers merged into down's basis (variant M)
+
+
 def _clone(pl):
     import copy
     from paper_2607_14618_amd._lib import _aligned_empty
@@ -98,14 +104,19 @@ def _clone(pl):
 
 
 def build_layer(torch, pq, synth, config, layer=0, mix=None, target_bits=None, m=1,
-                x_dtype=None):
-    """[(name, PackedLinear, x on device)] for one synthetic layer."""
+                x_dtype=None, emit=False):
+    """[(name, PackedLinear, x on device)] for one synthetic layer.  emit: gate
+    and up are packed with their output rows in down's basis (Eq. 10), so the
+    elementwise SiLU(gate) * up hands down its clustered input."""
     dev = torch.device("cuda", 0)
     lins, groups = synth.make_layer(config, layer=layer, mix=mix, target_bits=target_bits, m=m,
                                     x_dtype=x_dtype or torch.float16, device=dev)
+    down_perm = {lin.name: lin.perm for lin in lins}.get("down_proj")
     out = []
     for lin in lins:
-        pl = pq.PackedLinear(lin.blocks, lin.codes, lin.scales, lin.zeros, lin.perm, device=dev)
+        out_perm = down_perm if emit and lin.name in EMIT_TO_DOWN else None
+        pl = pq.PackedLinear(lin.blocks, lin.codes, lin.scales, lin.zeros, lin.perm, device=dev,
+                             out_perm=out_perm)
         out.append((lin.name, pl, groups[lin.group].x.to(dev)))
         lin.codes = lin.scales = lin.zeros = None
     return out
@@ -181,10 +192,14 @@ def schedule(layer, grouped):
 def decode_launches(torch, pq, copies, variant, grouped=True):
     """Variants: G gathers x' in the GEMV; P reads x' permuted beforehand (outside
     the timed step); S permutes explicitly inside the step (one polyq_permute per
-    launch into a preallocated buffer, then the GEMV on clustered x')."""
+    launch into a preallocated buffer, then the GEMV on clustered x'); M is G
+    with the gate/up -> down edge merged (Eq. 10): gate and up emit in down's
+    basis, so down reads clustered x' (prepared outside the timed step, as the
+    elementwise SiLU(gate) * up would hand it over)."""
     dev = torch.device("cuda", 0)
     ys = [torch.empty((x.shape[0], pl.n), dtype=torch.float32, device=dev) for _, pl, x in copies[0]]
-    xs = [pl.permute(x) if variant in ("P", "S") else x for _, pl, x in copies[0]]
+    pres = [variant in ("P", "S") or (variant == "M" and nm == "down_proj") for nm, _, _ in copies[0]]
+    xs = [pl.permute(x) if p else x for (_, pl, x), p in zip(copies[0], pres)]
     pre = variant in ("P", "S")
     sched = schedule(copies[0], grouped)
 
@@ -203,7 +218,7 @@ def decode_launches(torch, pq, copies, variant, grouped=True):
             return run
         if len(idx) == 1:
             j = idx[0]
-            return lambda: copy[j][1].decode(xs[j], pre_permuted=pre, y=ys[j])
+            return lambda: copy[j][1].decode(xs[j], pre_permuted=pres[j], y=ys[j])
         return lambda: pq.decode_batch([copy[j][1] for j in idx], [xs[j] for j in idx],
                                        pre_permuted=pre, ys=[ys[j] for j in idx])
 
@@ -216,7 +231,8 @@ def decode_launches(torch, pq, copies, variant, grouped=True):
 
 def decode_figure(torch, pq, synth, steps, warmup, variant, config=1, mix=None, target_bits=None,
                   m=1, grouped=True):
-    layer = build_layer(torch, pq, synth, config, mix=mix, target_bits=target_bits, m=m)
+    layer = build_layer(torch, pq, synth, config, mix=mix, target_bits=target_bits, m=m,
+                        emit=variant == "M")
     step_bytes = sum(pl.weight_bytes for _, pl, _ in layer)
     copies = rotation(layer, step_bytes)
     launches, sched = decode_launches(torch, pq, copies, variant, grouped)
@@ -357,6 +373,16 @@ def main_default(a, torch, pq, synth):
                 "four-launch dependency chain of a real decode step (not the headline value)",
         "us_per_step": round(one["ms_step"] * 1e3, 2), "gbs": round(one["gbs"], 1),
         "pct_hbm_peak": round(100 * one["gbs"] / HBM_PEAK_GBS, 2)}
+    if a.variant == "G":
+        mg = decode_figure(torch, pq, synth, a.steps, a.warmup, "M", grouped=not a.per_linear)
+        _log(f"decode, gate/up -> down merged (Eq. 10): {mg['ms_step'] * 1e3:.1f} us/step, "
+             f"{mg['gbs']:.1f} GB/s")
+        extra["merged_gate_up_down"] = {
+            "note": "the same step with gate and up packed to emit in down's basis (Eq. 10, "
+                    "polyq_pack_rows), so down reads clustered activations without a gather",
+            "us_per_step": round(mg["ms_step"] * 1e3, 2), "gbs": round(mg["gbs"], 1),
+            "pct_hbm_peak": round(100 * mg["gbs"] / HBM_PEAK_GBS, 2),
+            "per_launch_evented": mg["per_launch"]}
     if not a.no_prefill:
         _log("prefill GEMM, M=512")
         extra["prefill"] = prefill_figure(torch, pq, synth, 10, 3, grouped=not a.per_linear)
