@@ -19,7 +19,8 @@ activations), and the fp64 CPU oracle timed on a bounded sample.
 
 Other modes (each prints its own single JSON line):
   --sweep        budget sweep 3/4/5/6 b x M in {1, 4, 16} on the Llama2-13B layer (M > 1 also
-                 with the explicit shuffle: polyq_permute + GEMV on clustered x)
+                 with the explicit shuffle: polyq_permute + GEMV on clustered x, and with the
+                 gate/up -> down edge merged by output-row emission)
   --qwen         Qwen3-32B-shaped stack of 64 layers, variants G and P
   --copy-probe   a plain device copy of known size (HBM counter calibration)
 """
@@ -419,6 +420,11 @@ def main_sweep(a, torch, pq, synth):
                                   mix=synth.SWEEP_MIXES[bits], target_bits=bits, m=m)
                 rows[-1]["us_per_step_shuffle"] = round(e["ms_step"] * 1e3, 2)
                 rows[-1]["gbs_shuffle"] = round(e["gbs"], 1)
+                # the gate/up -> down edge merged (Eq. 10): down reads clustered x' with
+                # neither a gather nor a shuffle
+                g = decode_figure(torch, pq, synth, a.steps, a.warmup, "M", config=2,
+                                  mix=synth.SWEEP_MIXES[bits], target_bits=bits, m=m)
+                rows[-1]["us_per_step_merged"] = round(g["ms_step"] * 1e3, 2)
             _log(json.dumps(rows[-1]))
     base = [r for r in rows if r["avg_bits"] == 3 and r["m"] == 1][0]
     for r in rows:
