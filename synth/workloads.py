@@ -42,7 +42,7 @@ __all__ = [
     "BITS", "QUANTUM", "GROUP", "MASTER_SEED", "MIX_3", "MIX_PREFILL_4", "SWEEP_MIXES",
     "LinearSpec", "QuantLinear", "InputGroup", "LLAMA2_13B_LAYER", "QWEN3_32B_LAYER",
     "child_seed", "snap_counts", "mix_average", "outlier_channels", "sample_activations",
-    "rank_channels", "blocks_and_perm", "quantize_weight", "make_group", "make_linear",
+    "rank_channels", "blocks_and_perm", "quantize_weight", "quantize_weight_symmetric", "make_group", "make_linear",
     "make_layer", "random_quant_linear", "random_perm", "config_layer_specs",
 ]
 
@@ -293,6 +293,46 @@ def quantize_weight(weight: torch.Tensor, blocks: Sequence[Tuple[int, int]], per
             codes[:, a:e] = q.to(torch.int16)
             scales[:, g] = s64.astype(np.float16)
             zeros[:, g] = z64.astype(np.float16)
+            g += 1
+        k0 += ln
+    return (codes, torch.as_tensor(scales).to(dev), torch.as_tensor(zeros).to(dev))
+
+
+def quantize_weight_symmetric(weight: torch.Tensor, blocks: Sequence[Tuple[int, int]],
+                              perm: np.ndarray) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Symmetric group quantization (the paper's Q_b of Sec. 3.1) in the stored form.
+
+    Per row and per group inside a block of b <= 8 bits: s = fp16_rne(max|w| /
+    (2^(b-1) - 1)) computed in fp64, signed code c = clamp(rint(w / s), -2^(b-1),
+    2^(b-1) - 1), stored as q = c + 2^(b-1) with the constant zero point
+    z = 2^(b-1), so that s (q - z) = s c.  A group with s == 0 gets s = 1, q = z.
+    16-bit channels store fp16_rne(w).  Same return layout as quantize_weight.
+    """
+    dev = weight.device
+    n, k = weight.shape
+    wp = weight.index_select(1, torch.as_tensor(perm, dtype=torch.long, device=dev))
+    n_groups = sum(-(-ln // GROUP) for b, ln in blocks if b != 16)
+    codes = torch.empty((n, k), dtype=torch.int16, device=dev)
+    scales = np.zeros((n, n_groups), dtype=np.float16)
+    zeros = np.zeros((n, n_groups), dtype=np.float16)
+    k0, g = 0, 0
+    for b, ln in blocks:
+        if b == 16:
+            codes[:, k0:k0 + ln] = wp[:, k0:k0 + ln].to(torch.float16).view(torch.int16)
+            k0 += ln
+            continue
+        half = 1 << (b - 1)
+        for a in range(k0, k0 + ln, GROUP):
+            e = min(a + GROUP, k0 + ln)
+            w = wp[:, a:e]
+            amax = w.abs().amax(dim=1).double().cpu().numpy()
+            s16 = _fp16_from_f64(amax / (half - 1)) if half > 1 else _fp16_from_f64(amax)
+            s64 = np.where(s16 == 0, 1.0, s16.astype(np.float64))
+            s_t = torch.as_tensor(s64, device=dev).unsqueeze(1)
+            c = torch.clamp(torch.round(w.double() / s_t), -half, half - 1)
+            codes[:, a:e] = (c + half).to(torch.int16)
+            scales[:, g] = s64.astype(np.float16)
+            zeros[:, g] = float(half)
             g += 1
         k0 += ln
     return (codes, torch.as_tensor(scales).to(dev), torch.as_tensor(zeros).to(dev))

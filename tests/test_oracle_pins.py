@@ -354,3 +354,36 @@ def test_eq10_emission_of_an_all_16bit_layer_is_the_fp16_product_of_reordered_ro
     want = (xp @ rows.T).numpy()
     np.testing.assert_allclose(y, want, rtol=1e-13, atol=1e-13)
     assert np.all(y[:, [3, 11]] == 0) and np.all(bound[:, [3, 11]] == 0)
+
+
+def test_symmetric_quantizer_is_the_zero_point_special_case():
+    # The paper's Q_b is symmetric (Sec. 3.1): w_hat = s * c with a signed code
+    # c in [-2^(b-1), 2^(b-1) - 1].  Stored as q = c + 2^(b-1) with the constant
+    # zero point 2^(b-1), the oracle's s (q - z) must give exactly s * c, and it
+    # must track the fp32 weights within half a quantization step (or the
+    # clamp at the negative end, which symmetric ranges never reach).
+    from synth import quantize_weight_symmetric, random_perm
+    blocks = [(2, 128), (3, 96), (4, 64), (8, 32), (16, 32)]
+    n, k = 24, sum(l for _, l in blocks)
+    w = torch.randn((n, k), generator=torch.Generator().manual_seed(61), dtype=torch.float32) * 0.02
+    perm = random_perm(k, 62)
+    codes, scales, zeros = quantize_weight_symmetric(w, blocks, perm)
+    c16, s, z = _np(codes).view(np.uint16), _np(scales), _np(zeros)
+    w_hat = oracle.dequantize(blocks, c16, s, z)
+    wp = _np(w).astype(np.float64)[:, perm]
+    k0, g = 0, 0
+    for b, ln in blocks:
+        if b == 16:
+            assert np.array_equal(w_hat[:, k0:k0 + ln], wp[:, k0:k0 + ln].astype(np.float16).astype(np.float64))
+            k0 += ln
+            continue
+        half = 1 << (b - 1)
+        for a in range(k0, k0 + ln, 128):
+            e = min(a + 128, k0 + ln)
+            sg = s[:, g].astype(np.float64)[:, None]
+            signed = c16[:, a:e].astype(np.int64) - half
+            assert np.all(z[:, g] == half)
+            assert np.array_equal(w_hat[:, a:e], sg * signed)
+            assert np.all(np.abs(w_hat[:, a:e] - wp[:, a:e]) <= 0.5 * sg * (1 + 1e-3) + 1e-12)
+            g += 1
+        k0 += ln
