@@ -167,12 +167,16 @@ polyq_status polyq_unpack(const polyq_layout* layout, const void* packed, uint16
  * polyq_permute -- the explicit activation shuffle of Sec. 4.1 / Eq. 9:
  * x_out[i][k'] = x[i][perm[k']] for i < m, k' < k, for any 2-byte element type
  * (fp16 or bf16).  perm: int32 [k] (device).  An entry outside [0, k) yields 0.
+ * m * k must not exceed 2^31 - 1 elements (else POLYQ_ERR_CAPACITY, before any
+ * launch).
  */
 polyq_status polyq_permute(const int32_t* perm, const uint16_t* x, uint16_t* x_out, int32_t m,
                            int32_t k, void* stream);
 
 /*
- * polyq_gemv -- decode / small-batch product, 1 <= m <= 16 tokens:
+ * polyq_gemv -- decode / small-batch product, 1 <= m <= 16 tokens: the
+ * clustered product of Eq. 9 (x P^T times P W), one kernel over all bit blocks
+ * accumulating into one output (Sec. 4.2), dequantized as in Sec. 3.4:
  *   y[i][n] = sum_k' w_hat[n][k'] * x[i][perm[k']]   (fp32 accumulation)
  *   packed  buffer written by polyq_pack for `layout`.
  *   perm    int32 [k] (device, 16-byte aligned), or NULL when x is already in
@@ -220,7 +224,9 @@ polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32
                               void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * polyq_gemm -- prefill product for any m >= 1 (bf16 activations):
+ * polyq_gemm -- prefill product for any m >= 1 (bf16 activations): the same
+ * clustered product (Eq. 9; all blocks into one output, Sec. 4.2) as a dense
+ * contraction on the matrix cores:
  *   y[i][n] = sum_k' w_hat[n][k'] * x[i][perm[k']]
  *   x bf16 [m][k] bits, original channel order if perm != NULL, else clustered
  *   (then 16-byte aligned); m * k * 2 < 2^31.
@@ -232,9 +238,12 @@ polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32
  *   entry are ignored.  The split sums are added in a fixed order, so results
  *   do not depend on scheduling.
  * Computed with bf16 MFMA and fp32 accumulation: (q - z) enters as one exact
- * bf16 value when z is an integer in [0, 255], else as the bf16 pair hi + lo
- * (relative error below 2^-16); the group scale is applied in fp32; a 16-bit
- * channel enters as the exact bf16 pair hi + lo of its fp16 weight.
+ * bf16 value when z is an integer in [0, 255]; for any other fp16 z, q - z is
+ * formed in fp32 from exact operands with one rounding (relative error at most
+ * 2^-24) and enters as the bf16 pair hi + lo (together within 2^-16 relative of
+ * q - z); the group scale is applied in fp32; a 16-bit channel enters as the
+ * exact bf16 pair hi + lo of its fp16 weight.  |y - y_ref| <= 1e-3 *
+ * sum |w_hat x| for any fp16 scale and zero point.
  */
 size_t polyq_gemm_workspace_bytes(const polyq_layout* layout, int32_t m, int perm_given);
 polyq_status polyq_gemm(const polyq_layout* layout, const void* packed, const int32_t* perm,
@@ -258,6 +267,20 @@ typedef polyq_gemv_item polyq_gemm_item;
 size_t polyq_gemm_batch_workspace_bytes(const polyq_gemm_item* items, int32_t count, int32_t m);
 polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t count, int32_t m,
                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * polyq_read_probe -- measurement utility, not part of the linear-layer
+ * computation: reads `bytes` bytes of device memory once and discards them
+ * (each of at most work_groups work-groups reads one contiguous share).  The
+ * time of this launch is the reference read rate of a launch of that size,
+ * against which the decode GEMV's weight stream is measured.
+ *   buf: device, 16-byte aligned; bytes: a positive multiple of 16.
+ *   sink: device array of work_groups uint32, written only when a checksum
+ *         takes one particular value (contents afterwards unspecified).
+ *   bytes / work_groups must stay below 2^30 (else POLYQ_ERR_CAPACITY).
+ */
+polyq_status polyq_read_probe(const void* buf, int64_t bytes, int32_t work_groups, uint32_t* sink,
+                              void* stream);
 
 /* Static description of a status code (never NULL). */
 const char* polyq_status_str(polyq_status status);

@@ -31,7 +31,7 @@ STATUS = {0: "POLYQ_OK", 1: "POLYQ_ERR_ARG", 2: "POLYQ_ERR_BITS", 3: "POLYQ_ERR_
 EXPORTS = ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq_permute", "polyq_gemv_workspace_bytes",
            "polyq_gemv", "polyq_gemv_batch_workspace_bytes", "polyq_gemv_batch",
            "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_gemm_batch_workspace_bytes",
-           "polyq_gemm_batch", "polyq_status_str")
+           "polyq_gemm_batch", "polyq_read_probe", "polyq_status_str")
 
 
 class Block(ctypes.Structure):
@@ -108,10 +108,12 @@ def lib() -> ctypes.CDLL:
             L.polyq_gemm_batch_workspace_bytes.argtypes = [ip, i32, i32]
             L.polyq_gemm_batch_workspace_bytes.restype = sz
             L.polyq_gemm_batch.argtypes = [ip, i32, i32, vp, sz, vp]
+            L.polyq_read_probe.argtypes = [vp, ctypes.c_int64, i32, vp, vp]
             L.polyq_status_str.argtypes = [ctypes.c_int]
             L.polyq_status_str.restype = ctypes.c_char_p
             for name in ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq_permute",
-                         "polyq_gemv", "polyq_gemv_batch", "polyq_gemm", "polyq_gemm_batch"):
+                         "polyq_gemv", "polyq_gemv_batch", "polyq_gemm", "polyq_gemm_batch",
+                         "polyq_read_probe"):
                 getattr(L, name).restype = ctypes.c_int
             _lib = L
     return _lib
@@ -373,3 +375,74 @@ def gemm_batch(items: Sequence[Tuple[Layout, torch.Tensor, Optional[torch.Tensor
                                   0 if ws is None else ws.numel() * ws.element_size(), _stream(dev)),
            "polyq_gemm_batch")
     return ys
+
+
+class PreparedBatch:
+    """One polyq_gemv_batch (kind "gemv") or polyq_gemm_batch (kind "gemm")
+    launch whose arguments are marshalled once: the item array, the token count,
+    the workspace (queried once and allocated once, zero-filled for the GEMV) and
+    the output tensors are kept, so ``run()`` is a single library call.  The
+    activations are read from the same tensors on every run (write new values
+    into them in place).  items: (layout, packed, perm or None, x, y or None)."""
+
+    def __init__(self, kind: str, items, workspace: Optional[torch.Tensor] = None):
+        if kind not in ("gemv", "gemm"):
+            raise ValueError(kind)
+        if not 1 <= len(items) <= MAX_BATCH:
+            raise ValueError(f"1..{MAX_BATCH} items per batch")
+        want = torch.float16 if kind == "gemv" else torch.bfloat16
+        self.kind = kind
+        self.arr = (GemvItem * len(items))()
+        self.keep, self.ys, self.layouts = [], [], []
+        m, dev = None, None
+        for i, (layout, packed, perm, x, y) in enumerate(items):
+            x2 = x if x.dim() == 2 else x.reshape(1, -1)
+            d = _need_cuda(packed, perm, x2, y, workspace)
+            dev = d if dev is None else dev
+            if d != dev:
+                raise ValueError("all tensors must be on the same device")
+            if x2.dtype != want or x2.shape[1] != layout.k:
+                raise ValueError(f"x must be {want} [m][k]")
+            if m is None:
+                m = x2.shape[0]
+            elif x2.shape[0] != m:
+                raise ValueError("every item of a batch has the same m")
+            if perm is not None and (perm.dtype != torch.int32 or perm.numel() != layout.k):
+                raise ValueError("perm must be int32 [k]")
+            if y is None:
+                y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
+            self.arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y))
+            self.keep += [layout, packed, perm, x2]
+            self.ys.append(y)
+        self.m, self.count, self.dev = m, len(items), dev
+        L = lib()
+        if kind == "gemv":
+            need = int(L.polyq_gemv_batch_workspace_bytes(self.arr, self.count, m)) if 1 <= m <= MAX_M_GEMV else 0
+        else:
+            need = int(L.polyq_gemm_batch_workspace_bytes(self.arr, self.count, m))
+        if workspace is None and need:
+            raw = (torch.zeros if kind == "gemv" else torch.empty)(need + 256, dtype=torch.uint8, device=dev)
+            off = (-raw.data_ptr()) % 256
+            workspace = raw[off:off + need]
+        self.workspace = workspace
+        self.ws_ptr = _ptr(workspace)
+        self.ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        self.fn = L.polyq_gemv_batch if kind == "gemv" else L.polyq_gemm_batch
+        self.name = "polyq_gemv_batch" if kind == "gemv" else "polyq_gemm_batch"
+
+    def run(self):
+        _check(self.fn(self.arr, self.count, self.m, self.ws_ptr, self.ws_bytes, _stream(self.dev)), self.name)
+        return self.ys
+
+
+def read_probe(buf: torch.Tensor, nbytes: int, work_groups: int, sink: torch.Tensor) -> None:
+    """Launch the streaming-read probe over the first nbytes of buf (a
+    measurement utility: the reference read rate of a launch of that size)."""
+    dev = _need_cuda(buf, sink)
+    if sink.dtype != torch.int32 or sink.numel() < work_groups:
+        raise ValueError("sink must be int32 with at least work_groups entries")
+    if nbytes > buf.numel() * buf.element_size():
+        raise ValueError("nbytes exceeds the buffer")
+    _check(lib().polyq_read_probe(_ptr(buf), int(nbytes), int(work_groups), _ptr(sink), _stream(dev)),
+           "polyq_read_probe")
+

@@ -21,9 +21,11 @@
 // hi + lo of bf16 values (two MFMAs); for 16-bit weights the pair is exact.
 //
 // Dequantization uses the fp16 exponent field: (1024 + q) is the fp16 with
-// exponent 10 and mantissa q, so one AND-OR forms two codes of a pair as fp16,
-// and one mixed-precision FMA per code gives q - z in fp32 exactly; the bf16
-// value is then the fp32 value's upper half (exact when its lower half is 0).
+// exponent 10 and mantissa q, so one AND-OR forms two codes of a pair as fp16.
+// For an integer z in [0, 255] one fp32 subtract of (1024 + z) gives q - z
+// exactly and the bf16 value is the fp32 value's upper half; for any other
+// fp16 z, (1024 + q) - 1024 = q exactly and q - z rounds once in fp32 before
+// the split into hi + lo.
 #include <hip/hip_runtime.h>
 
 #include <string.h>
@@ -302,19 +304,27 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
       case 4: sub_tile_pairs<4>(pr.w, dr, hp); break;
       default: sub_tile_pairs<8>(pr.w, dr, hp); break;
     }
-    // (1024 + q) - (1024 + z) = q - z, exact in fp32; exact in bf16 too when z
-    // is an integer in [0, 255] (then |q - z| <= 255)
-    const float zoff = 1024.f + zf;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const h2 h = __builtin_bit_cast(h2, hp[j]);
-      v[2 * j] = static_cast<float>(h.x) - zoff;
-      v[2 * j + 1] = static_cast<float>(h.y) - zoff;
-    }
     if (__all(zf == truncf(zf) && zf >= 0.f && zf <= 255.f)) {  // wave-uniform
+      // (1024 + q) - (1024 + z) = q - z: both sums are exact for such z, and
+      // so is the difference, in fp32 and in bf16 (|q - z| <= 255)
+      const float zoff = 1024.f + zf;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const h2 h = __builtin_bit_cast(h2, hp[j]);
+        v[2 * j] = static_cast<float>(h.x) - zoff;
+        v[2 * j + 1] = static_cast<float>(h.y) - zoff;
+      }
       store_exact(v, hi);
       *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
     } else {
+      // any other fp16 z: ((1024 + q) - 1024) is q exactly, and q - z rounds
+      // once in fp32 (1024 + z itself would round for small non-integer z)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const h2 h = __builtin_bit_cast(h2, hp[j]);
+        v[2 * j] = (static_cast<float>(h.x) - 1024.f) - zf;
+        v[2 * j + 1] = (static_cast<float>(h.y) - 1024.f) - zf;
+      }
       store_pair(v, hi, lo);
       lds_tag[st] = ci.c + 1;  // any thread; every writer stores the same value
     }
@@ -562,7 +572,7 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
   // group's other chunks: 1024 + z of both rows, rows whose scale is 0, and
   // whether every zero point of the wave is an integer in [0, 255].
   float sig_prev0 = 1.f, sig_prev1 = 1.f;
-  float gzo0 = 1024.f, gzo1 = 1024.f;
+  float gz0 = 0.f, gz1 = 0.f;
   bool gdead0 = false, gdead1 = false, gdead = false, gexact = true;
   auto store = [&](const ChunkCursor& ci, const PreW& pr, int st) {
 #pragma unroll
@@ -578,8 +588,8 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
         sg1 = gdead1 ? 1.f : s1;
         const h2 zz = __builtin_bit_cast(h2, pr.z2);
         const float z0 = static_cast<float>(zz.x), z1 = static_cast<float>(zz.y);
-        gzo0 = 1024.f + z0;
-        gzo1 = 1024.f + z1;
+        gz0 = z0;
+        gz1 = z1;
         const bool ok0 = z0 == truncf(z0) && z0 >= 0.f && z0 <= 255.f;
         const bool ok1 = z1 == truncf(z1) && z1 >= 0.f && z1 <= 255.f;
         gexact = __all(ok0 && ok1);  // wave-uniform
@@ -615,15 +625,28 @@ __global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
       case 4: pairs_at<4>(pr.w0, dr, 0, hp0); pairs_at<4>(pr.w0, dr + 1, 1, hp1); break;
       default: pairs_at<8>(pr.w0, dr, 0, hp0); pairs_at<8>(pr.w0, dr + 1, 1, hp1); break;
     }
-    // (1024 + q) - (1024 + z) = q - z, exact in fp32 (and in bf16 when z is an
-    // integer in [0, 255])
+    if (gexact) {
+      // (1024 + q) - (1024 + z) = q - z, all exact for an integer z in [0, 255]
+      // (in bf16 too)
+      const float zo0 = 1024.f + gz0, zo1 = 1024.f + gz1;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const h2 h = __builtin_bit_cast(h2, hp0[j]), g = __builtin_bit_cast(h2, hp1[j]);
-      v0[2 * j] = static_cast<float>(h.x) - gzo0;
-      v0[2 * j + 1] = static_cast<float>(h.y) - gzo0;
-      v1[2 * j] = static_cast<float>(g.x) - gzo1;
-      v1[2 * j + 1] = static_cast<float>(g.y) - gzo1;
+      for (int j = 0; j < 4; ++j) {
+        const h2 h = __builtin_bit_cast(h2, hp0[j]), g = __builtin_bit_cast(h2, hp1[j]);
+        v0[2 * j] = static_cast<float>(h.x) - zo0;
+        v0[2 * j + 1] = static_cast<float>(h.y) - zo0;
+        v1[2 * j] = static_cast<float>(g.x) - zo1;
+        v1[2 * j + 1] = static_cast<float>(g.y) - zo1;
+      }
+    } else {
+      // any other fp16 z: (1024 + q) - 1024 = q exactly, then q - z rounds once
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const h2 h = __builtin_bit_cast(h2, hp0[j]), g = __builtin_bit_cast(h2, hp1[j]);
+        v0[2 * j] = (static_cast<float>(h.x) - 1024.f) - gz0;
+        v0[2 * j + 1] = (static_cast<float>(h.y) - 1024.f) - gz0;
+        v1[2 * j] = (static_cast<float>(g.x) - 1024.f) - gz1;
+        v1[2 * j + 1] = (static_cast<float>(g.y) - 1024.f) - gz1;
+      }
     }
     if (gdead) {  // rows whose scale is 0 contribute nothing
 #pragma unroll
@@ -949,8 +972,27 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
     if (reinterpret_cast<uintptr_t>(itm.packed) % 256 != 0 || reinterpret_cast<uintptr_t>(itm.y) % 4 != 0)
       return POLYQ_ERR_ARG;
     if (L.packed_bytes > 0x7FFFFFFFll) return POLYQ_ERR_CAPACITY;
+    if (itm.perm == nullptr && reinterpret_cast<uintptr_t>(itm.x) % 16 != 0)
+      return POLYQ_ERR_ARG;  // clustered activations are read as 16-byte vectors
     tiles1 += L.n_tiles;
   }
+  // Every check above and here comes before the first launch.  Work-group
+  // shape by launch size: 4-wave work-groups of 256 tokens x 128
+  // rows with 128 x 64 wave tiles (gemm_wide_kernel) when there are enough of
+  // them for two per CU, or K is split; else 8-wave work-groups of the same tile
+  // (gemm_kernel<2>) when those fill most CUs; else one packed tile per
+  // 4-wave work-group (gemm_kernel<1>, two co-resident per CU).
+  const int64_t wg2 = (tiles1 + count) / 2 * a.m_tiles;
+  const int kind = splits > 1 || wg2 >= 400 ? 3 : wg2 >= 200 ? 2 : 1;
+  const bool wide = kind >= 2;
+  const int tn = wide ? 2 : 1;
+  int64_t wg = 0;
+  for (int i = 0; i < count; ++i) {
+    a.wg_begin[i] = static_cast<int32_t>(wg);
+    wg += static_cast<int64_t>((items[i].layout->n_tiles + tn - 1) / tn) * a.m_tiles * splits;
+    if (wg > 0x7FFFFFFF) return POLYQ_ERR_CAPACITY;
+  }
+  for (int i = count; i <= POLYQ_MAX_BATCH; ++i) a.wg_begin[i] = static_cast<int32_t>(wg);
   // Permuted copies (one per distinct (x, perm)), then the products.
   for (int i = 0; i < count; ++i) {
     const polyq_gemv_item& itm = items[i];
@@ -972,8 +1014,6 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
         }
       }
       xp = out;
-    } else if (reinterpret_cast<uintptr_t>(itm.x) % 16 != 0) {
-      return POLYQ_ERR_ARG;  // activations are read as 16-byte vectors
     }
     GemmItem& g = a.item[i];
     g.packed = static_cast<const uint8_t*>(itm.packed);
@@ -995,22 +1035,6 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
       g.rb[b] = used ? L.record_bytes[b] : 0;
     }
   }
-  // Work-group shape by launch size: 4-wave work-groups of 256 tokens x 128
-  // rows with 128 x 64 wave tiles (gemm_wide_kernel) when there are enough of
-  // them for two per CU, or K is split; else 8-wave work-groups of the same tile
-  // (gemm_kernel<2>) when those fill most CUs; else one packed tile per
-  // 4-wave work-group (gemm_kernel<1>, two co-resident per CU).
-  const int64_t wg2 = (tiles1 + count) / 2 * a.m_tiles;
-  const int kind = splits > 1 || wg2 >= 400 ? 3 : wg2 >= 200 ? 2 : 1;
-  const bool wide = kind >= 2;
-  const int tn = wide ? 2 : 1;
-  int64_t wg = 0;
-  for (int i = 0; i < count; ++i) {
-    a.wg_begin[i] = static_cast<int32_t>(wg);
-    wg += static_cast<int64_t>((items[i].layout->n_tiles + tn - 1) / tn) * a.m_tiles * splits;
-    if (wg > 0x7FFFFFFF) return POLYQ_ERR_CAPACITY;
-  }
-  for (int i = count; i <= POLYQ_MAX_BATCH; ++i) a.wg_begin[i] = static_cast<int32_t>(wg);
   // split s covers groups [G s / S, G (s + 1) / S) of the group sequence
   {
     const polyq_layout& L = *items[0].layout;

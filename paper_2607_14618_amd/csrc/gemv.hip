@@ -937,7 +937,39 @@ polyq_status plan_batch(const polyq_gemv_item* items, int32_t count, int32_t m, 
   return POLYQ_OK;
 }
 
+// Pointer and alignment checks of every item (the planner reads only the
+// layouts).
+polyq_status check_items(const polyq_gemv_item* items, int32_t count) {
+  for (int i = 0; i < count; ++i) {
+    const polyq_gemv_item& t = items[i];
+    if (t.packed == nullptr || t.x == nullptr || t.y == nullptr) return POLYQ_ERR_ARG;
+    if (reinterpret_cast<uintptr_t>(t.packed) % 256 != 0) return POLYQ_ERR_ARG;
+    if (reinterpret_cast<uintptr_t>(t.x) % 16 != 0 || reinterpret_cast<uintptr_t>(t.y) % 4 != 0 ||
+        reinterpret_cast<uintptr_t>(t.perm) % 16 != 0)
+      return POLYQ_ERR_ARG;  // activations and permutation are read as 16-byte vectors
+    for (int b = 0; b < t.layout->nblocks; ++b)
+      if (t.layout->tile_bytes[b] > INT32_MAX) return POLYQ_ERR_UNSUPPORTED;
+  }
+  return POLYQ_OK;
+}
+
 }  // namespace
+
+namespace polyq {
+
+polyq_status gemv_batch_workspace_status(const polyq_gemv_item* items, int32_t count, int32_t m,
+                                         size_t* need) {
+  GemvPlan plans[POLYQ_MAX_BATCH];
+  size_t offs[POLYQ_MAX_BATCH], total = 0, lds = 0;
+  const polyq_status st = plan_batch(items, count, m, plans, offs, &total, &lds);
+  if (st != POLYQ_OK) return st;
+  const polyq_status ct = check_items(items, count);
+  if (ct != POLYQ_OK) return ct;
+  *need = total;
+  return POLYQ_OK;
+}
+
+}  // namespace polyq
 
 extern "C" size_t polyq_gemv_batch_workspace_bytes(const polyq_gemv_item* items, int32_t count,
                                                    int32_t m) {
@@ -953,6 +985,8 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
   size_t offs[POLYQ_MAX_BATCH], total = 0, lds = 0;
   const polyq_status st = plan_batch(items, count, m, plans, offs, &total, &lds);
   if (st != POLYQ_OK) return st;
+  const polyq_status ct = check_items(items, count);
+  if (ct != POLYQ_OK) return ct;
   if (total > 0 && (workspace == nullptr || workspace_bytes < total)) return POLYQ_ERR_CAPACITY;
   if (total > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return POLYQ_ERR_ARG;
 
@@ -962,11 +996,6 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
   for (int i = 0; i < count; ++i) {
     const polyq_gemv_item& t = items[i];
     const polyq_layout& L = *t.layout;
-    if (t.packed == nullptr || t.x == nullptr || t.y == nullptr) return POLYQ_ERR_ARG;
-    if (reinterpret_cast<uintptr_t>(t.packed) % 256 != 0) return POLYQ_ERR_ARG;
-    if (reinterpret_cast<uintptr_t>(t.x) % 16 != 0 || reinterpret_cast<uintptr_t>(t.y) % 4 != 0 ||
-        reinterpret_cast<uintptr_t>(t.perm) % 16 != 0)
-      return POLYQ_ERR_ARG;  // activations and permutation are read as 16-byte vectors
     const GemvPlan& p = plans[i];
     GemvItem& g = a.item[i];
     g.packed = static_cast<const uint8_t*>(t.packed);
@@ -1001,7 +1030,6 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
       g.magic[b] = div_magic(static_cast<uint32_t>(g.waves[b]));
       w0 += g.waves[b];
       g.block_offset[b] = used ? L.block_offset[b] : 0;
-      if (used && L.tile_bytes[b] > INT32_MAX) return POLYQ_ERR_UNSUPPORTED;
       g.tile_bytes[b] = used ? static_cast<int32_t>(L.tile_bytes[b]) : 0;
     }
     wgs = std::max(wgs, L.n_tiles * p.S);

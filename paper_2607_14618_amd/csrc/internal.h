@@ -96,6 +96,11 @@ size_t gemv_wave_lds_bytes(const GemvPlan& p, int32_t m);
 size_t gemv_zero_offset(const GemvPlan& p, int32_t m);
 size_t gemv_lds_bytes(const GemvPlan& p, int32_t m);
 
+// Validation and workspace size of a polyq_gemv_batch request: every check
+// polyq_gemv_batch makes before it launches, except the workspace's own.
+polyq_status gemv_batch_workspace_status(const polyq_gemv_item* items, int32_t count, int32_t m,
+                                         size_t* need);
+
 // Block accessor of a layout for wave_range (host side).
 struct LayoutBlocks {
   const polyq_layout* L;

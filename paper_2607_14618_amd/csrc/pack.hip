@@ -14,6 +14,8 @@ namespace {
 
 constexpr int kThreads = 256;
 
+constexpr int64_t kMaxPermuteElems = (static_cast<int64_t>(1) << 31) - 1;  // m * k of polyq_permute
+
 inline unsigned grid_for(int64_t items) {
   return static_cast<unsigned>((items + kThreads - 1) / kThreads);
 }
@@ -243,7 +245,8 @@ extern "C" polyq_status polyq_permute(const int32_t* perm, const uint16_t* x, ui
                                       int32_t m, int32_t k, void* stream) {
   if (perm == nullptr || x == nullptr || x_out == nullptr) return POLYQ_ERR_ARG;
   if (m < 1 || k < 1 || k > POLYQ_MAX_K) return POLYQ_ERR_ARG;
-  if (static_cast<int64_t>(m) * k > (static_cast<int64_t>(1) << 40)) return POLYQ_ERR_CAPACITY;
+  // one thread per element: the grid's thread count must stay below 2^32
+  if (static_cast<int64_t>(m) * k > kMaxPermuteElems) return POLYQ_ERR_CAPACITY;
   hipLaunchKernelGGL(permute_kernel, dim3(grid_for(static_cast<int64_t>(m) * k)), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), perm, x, x_out, m, k);
   return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;

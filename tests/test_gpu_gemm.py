@@ -197,3 +197,57 @@ def test_gemm_and_gemv_beyond_the_lds_row_gather():
     assert_parity(y, y_ref, bound, "gemm k=40960")
     yv_ref, bv = oracle_ref(lin, xh)
     assert_parity(yv, yv_ref, bv, "gemv k=40960")
+
+
+SMALL_Z = [0.001, 0.03, -0.001, 2.0 ** -24, 0.0999]
+
+
+def _small_z_linear(n, k, blocks, seed):
+    """Codes-mode layer where rows 0..9 have all low-bit codes 0 and every zero
+    point of rows 0..19 is a small non-integer (fp16 of SMALL_Z, cycled): with
+    q = 0 the product is s * (0 - z) * x, so any rounding of z shows in full."""
+    lin = random_quant_linear(n, k, blocks, seed=seed, mode="codes")
+    codes = lin.codes.clone()
+    zeros = lin.zeros.clone()
+    k0 = 0
+    for b, ln in blocks:
+        if b != 16:
+            codes[:10, k0:k0 + ln] = 0
+        k0 += ln
+    for r in range(min(20, n)):
+        for g in range(zeros.shape[1]):
+            zeros[r, g] = SMALL_Z[(r + g) % len(SMALL_Z)]
+    lin.codes, lin.zeros = codes, zeros
+    return lin
+
+
+@pytest.mark.parametrize("case", ["split_k", "one_tile", "eight_wave", "wide"])
+def test_gemm_small_non_integer_zero_points(case):
+    """Zero points below 2^-3 that are not integers (1024 + z is not exact in
+    fp32): every prefill kernel form -- one tile per work-group, 8-wave
+    work-groups, the wide-wave kernel, and a single linear with K split -- meets
+    the bound on rows whose codes are all 0 and on random-code rows."""
+    mixed = [(2, 992), (3, 704), (4, 256), (8, 64), (16, 32)]
+    small = [(2, 160), (3, 96), (4, 128), (8, 96), (16, 32)]
+    if case == "split_k":
+        specs = [(100, mixed)]            # one linear, 2 tiles, 18 groups: K split
+    elif case == "one_tile":
+        specs = [(100, small), (70, small)]
+    elif case == "eight_wave":
+        specs = [(16384, small), (16384, small)]
+    else:
+        specs = [(25600, small), (25600, small)]
+    lins = [_small_z_linear(n, sum(l for _, l in bl), bl, seed=4100 + i) for i, (n, bl) in enumerate(specs)]
+    k = lins[0].k
+    for lin in lins[1:]:
+        lin.perm = lins[0].perm
+    pls = [packed_linear(lin) for lin in lins]
+    x = _xb(7, k, seed=41)
+    xd = x.to(dev())
+    ys = [pls[0].prefill(xd)] if len(pls) == 1 else pq.prefill_batch(pls, [xd] * len(pls))
+    torch.cuda.synchronize()
+    for lin, y in zip(lins, ys):
+        y_ref, bound = oracle_ref(lin, x)
+        assert_parity(y, y_ref, bound, f"gemm small z {case} n={lin.n}")
+        # the all-zero-code rows alone (their products are -s z x only)
+        assert_parity(np_(y)[:, :10], y_ref[:, :10], bound[:, :10], f"gemm small z rows {case}")
