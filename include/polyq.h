@@ -198,6 +198,9 @@ polyq_status polyq_gemv(const polyq_layout* layout, const void* packed, const in
                         const uint16_t* x, int32_t m, float* y, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/* Size of the device array behind polyq_gemv_batch_noalloc (per GPU). */
+#define POLYQ_NOALLOC_SCRATCH_BYTES (16u << 20)
+
 /*
  * polyq_gemv_batch -- up to POLYQ_MAX_BATCH independent decode products in one
  * launch (e.g. the q/k/v projections, or gate/up, which share x and perm):
@@ -222,6 +225,23 @@ typedef struct {
 size_t polyq_gemv_batch_workspace_bytes(const polyq_gemv_item* items, int32_t count, int32_t m);
 polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32_t m,
                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * polyq_gemv_batch_noalloc -- polyq_gemv_batch without a workspace argument,
+ * for callers that cannot allocate device memory (code under graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  The workspace is a
+ * fixed array of POLYQ_NOALLOC_SCRATCH_BYTES bytes inside this library, one
+ * copy per GPU, held until the process ends; the call allocates and frees
+ * nothing.  Arguments and results as for polyq_gemv_batch (same kernels).
+ *   - A request whose workspace (polyq_gemv_batch_workspace_bytes) exceeds
+ *     POLYQ_NOALLOC_SCRATCH_BYTES returns POLYQ_ERR_CAPACITY before any launch.
+ *   - The first call on a GPU clears that GPU's array on `stream` (one kernel)
+ *     before the product; every completed call leaves it zero-filled again.
+ *   - All calls on one GPU share its array: calls that may overlap (e.g. on
+ *     different streams without ordering) race and give undefined results.
+ */
+polyq_status polyq_gemv_batch_noalloc(const polyq_gemv_item* items, int32_t count, int32_t m,
+                                      void* stream);
 
 /*
  * polyq_gemm -- prefill product for any m >= 1 (bf16 activations): the same

@@ -31,7 +31,7 @@ STATUS = {0: "POLYQ_OK", 1: "POLYQ_ERR_ARG", 2: "POLYQ_ERR_BITS", 3: "POLYQ_ERR_
 EXPORTS = ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq_permute", "polyq_gemv_workspace_bytes",
            "polyq_gemv", "polyq_gemv_batch_workspace_bytes", "polyq_gemv_batch",
            "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_gemm_batch_workspace_bytes",
-           "polyq_gemm_batch", "polyq_read_probe", "polyq_status_str")
+           "polyq_gemm_batch", "polyq_read_probe", "polyq_gemv_batch_noalloc", "polyq_status_str")
 
 
 class Block(ctypes.Structure):
@@ -109,11 +109,12 @@ def lib() -> ctypes.CDLL:
             L.polyq_gemm_batch_workspace_bytes.restype = sz
             L.polyq_gemm_batch.argtypes = [ip, i32, i32, vp, sz, vp]
             L.polyq_read_probe.argtypes = [vp, ctypes.c_int64, i32, vp, vp]
+            L.polyq_gemv_batch_noalloc.argtypes = [ip, i32, i32, vp]
             L.polyq_status_str.argtypes = [ctypes.c_int]
             L.polyq_status_str.restype = ctypes.c_char_p
             for name in ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq_permute",
                          "polyq_gemv", "polyq_gemv_batch", "polyq_gemm", "polyq_gemm_batch",
-                         "polyq_read_probe"):
+                         "polyq_read_probe", "polyq_gemv_batch_noalloc"):
                 getattr(L, name).restype = ctypes.c_int
             _lib = L
     return _lib
@@ -446,3 +447,35 @@ def read_probe(buf: torch.Tensor, nbytes: int, work_groups: int, sink: torch.Ten
     _check(lib().polyq_read_probe(_ptr(buf), int(nbytes), int(work_groups), _ptr(sink), _stream(dev)),
            "polyq_read_probe")
 
+
+NOALLOC_SCRATCH_BYTES = 16 << 20
+
+
+def gemv_batch_noalloc(items):
+    """polyq_gemv_batch_noalloc: the decode launch of gemv_batch with the
+    library's own device scratch array as workspace (no allocation by the
+    library; outputs must be given or are allocated here by torch).  items:
+    (layout, packed, perm or None, x fp16 [m][k], y or None)."""
+    if not 1 <= len(items) <= MAX_BATCH:
+        raise ValueError(f"1..{MAX_BATCH} items per batch")
+    arr = (GemvItem * len(items))()
+    keep, ys, m, dev = [], [], None, None
+    for i, (layout, packed, perm, x, y) in enumerate(items):
+        x2 = x if x.dim() == 2 else x.reshape(1, -1)
+        d = _need_cuda(packed, perm, x2, y)
+        dev = d if dev is None else dev
+        if d != dev:
+            raise ValueError("all tensors must be on the same device")
+        if x2.dtype != torch.float16 or x2.shape[1] != layout.k:
+            raise ValueError("x must be fp16 [m][k]")
+        if m is None:
+            m = x2.shape[0]
+        elif x2.shape[0] != m:
+            raise ValueError("every item of a batch has the same m")
+        if y is None:
+            y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
+        arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y))
+        keep.append(x2)
+        ys.append(y)
+    _check(lib().polyq_gemv_batch_noalloc(arr, len(items), m, _stream(dev)), "polyq_gemv_batch_noalloc")
+    return ys
