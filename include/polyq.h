@@ -182,11 +182,16 @@ polyq_status polyq_permute(const int32_t* perm, const uint16_t* x, uint16_t* x_o
  *   perm    int32 [k] (device, 16-byte aligned), or NULL when x is already in
  *           clustered order.
  *   x       fp16 [m][k] bits (16-byte aligned).   y fp32 [m][n], fully overwritten.
- *   workspace / workspace_bytes: device scratch of at least
- *           polyq_gemv_workspace_bytes(layout, m) bytes (may be NULL when that
- *           is 0).  It must be zero-filled before its first use and is left
- *           zero-filled by every completed call; calls that share a workspace
- *           must be ordered (same stream).
+ *   workspace / workspace_bytes: device memory of at least
+ *           polyq_gemv_workspace_bytes(layout, m) bytes (enough with or
+ *           without a permutation; may be NULL when that is 0), 256-byte
+ *           aligned, laid out as for polyq_gemv_batch with one item: its
+ *           first polyq_gemv_batch_workspace_zero_bytes bytes (the split-K
+ *           state) must be zero on entry and are zero again when the call
+ *           completes; the bytes after them are scratch that the call
+ *           overwrites (a clustered copy of x for several tokens, or for a row
+ *           too long for the kernel's LDS).  Calls that share a workspace must
+ *           be ordered (same stream).
  * Precision: for zero points that are integers of magnitude <= 1023 every
  * w_hat * x product is exact in fp32 (q - z is an exact integer, s is applied
  * once per group) and only fp32 accumulation rounds.  Any other z is applied
@@ -210,9 +215,18 @@ polyq_status polyq_gemv(const polyq_layout* layout, const void* packed, const in
  * input or another y.  The work split of every item is sized for the whole
  * launch, so the workspace is queried for the batch:
  *   workspace of at least polyq_gemv_batch_workspace_bytes(items, count, m)
- *   bytes (only the layout field of each item is read by the query; 0 on an
- *   invalid request), zero-filled before first use and left zero-filled by
- *   every completed call, as for polyq_gemv.
+ *   bytes, 256-byte aligned (the queries read the layout, perm and x fields of
+ *   each item and return 0 on an invalid request).  It holds two parts:
+ *     [0, Z)  Z = polyq_gemv_batch_workspace_zero_bytes(items, count, m): the
+ *             split-K counters and partial sums.  Must be zero on entry; every
+ *             completed call leaves them zero.
+ *     [Z, ..) scratch: one clustered copy x' = x[:, perm] per distinct (x,
+ *             perm) of the items with a permutation and several tokens (or a
+ *             row too long for LDS); overwritten by the call (Eq. 9's explicit
+ *             shuffle, made once per launch).
+ *   A workspace reused for requests of different shapes must therefore be
+ *   zeroed again up to the new request's Z wherever an earlier call left
+ *   scratch there.
  */
 typedef struct {
   const polyq_layout* layout;
@@ -223,6 +237,7 @@ typedef struct {
 } polyq_gemv_item;
 
 size_t polyq_gemv_batch_workspace_bytes(const polyq_gemv_item* items, int32_t count, int32_t m);
+size_t polyq_gemv_batch_workspace_zero_bytes(const polyq_gemv_item* items, int32_t count, int32_t m);
 polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32_t m,
                               void* workspace, size_t workspace_bytes, void* stream);
 
@@ -235,8 +250,10 @@ polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32
  * nothing.  Arguments and results as for polyq_gemv_batch (same kernels).
  *   - A request whose workspace (polyq_gemv_batch_workspace_bytes) exceeds
  *     POLYQ_NOALLOC_SCRATCH_BYTES returns POLYQ_ERR_CAPACITY before any launch.
- *   - The first call on a GPU clears that GPU's array on `stream` (one kernel)
- *     before the product; every completed call leaves it zero-filled again.
+ *   - The library keeps, per GPU, how much of the array is known to be zero;
+ *     a call whose split-K state reaches past that clears the difference on
+ *     `stream` (one kernel) before the product (the first call on a GPU
+ *     always does).
  *   - All calls on one GPU share its array: calls that may overlap (e.g. on
  *     different streams without ordering) race and give undefined results.
  */

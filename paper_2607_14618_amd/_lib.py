@@ -29,7 +29,8 @@ STATUS = {0: "POLYQ_OK", 1: "POLYQ_ERR_ARG", 2: "POLYQ_ERR_BITS", 3: "POLYQ_ERR_
 
 # every symbol include/polyq.h declares
 EXPORTS = ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq_permute", "polyq_gemv_workspace_bytes",
-           "polyq_gemv", "polyq_gemv_batch_workspace_bytes", "polyq_gemv_batch",
+           "polyq_gemv", "polyq_gemv_batch_workspace_bytes", "polyq_gemv_batch_workspace_zero_bytes",
+           "polyq_gemv_batch",
            "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_gemm_batch_workspace_bytes",
            "polyq_gemm_batch", "polyq_read_probe", "polyq_gemv_batch_noalloc", "polyq_status_str")
 
@@ -101,6 +102,8 @@ def lib() -> ctypes.CDLL:
             ip = ctypes.POINTER(GemvItem)
             L.polyq_gemv_batch_workspace_bytes.argtypes = [ip, i32, i32]
             L.polyq_gemv_batch_workspace_bytes.restype = sz
+            L.polyq_gemv_batch_workspace_zero_bytes.argtypes = [ip, i32, i32]
+            L.polyq_gemv_batch_workspace_zero_bytes.restype = sz
             L.polyq_gemv_batch.argtypes = [ip, i32, i32, vp, sz, vp]
             L.polyq_gemm_workspace_bytes.argtypes = [lp, i32, ctypes.c_int]
             L.polyq_gemm_workspace_bytes.restype = sz
@@ -242,21 +245,30 @@ def permute(perm: torch.Tensor, x: torch.Tensor, out: Optional[torch.Tensor] = N
     return out if x.dim() == 2 else out.reshape(x.shape)
 
 
-_ws: Dict[Tuple[str, int, int], torch.Tensor] = {}
+_ws: Dict[Tuple[str, int, int], list] = {}
 
 
-def _workspace(kind: str, nbytes: int, dev: torch.device, zero: bool) -> Optional[torch.Tensor]:
+def _workspace(kind: str, nbytes: int, dev: torch.device, zero_bytes: int = 0) -> Optional[torch.Tensor]:
+    """A cached 256-byte aligned workspace per (kind, device, stream) whose first
+    zero_bytes bytes are zero (the GEMV's split-K state; the bytes after it are
+    the call's scratch, which the call leaves non-zero).  The cache remembers
+    how long a prefix is known to be zero and clears only the difference."""
     if nbytes == 0:
         return None
     key = (kind, dev.index if dev.index is not None else torch.cuda.current_device(), _stream(dev))
-    buf = _ws.get(key)
-    if buf is None or buf.numel() < nbytes:
-        size = max(nbytes, 2 * (buf.numel() if buf is not None else 0))
-        raw = torch.zeros(size + 256, dtype=torch.uint8, device=dev) if zero else \
-            torch.empty(size + 256, dtype=torch.uint8, device=dev)
+    ent = _ws.get(key)
+    if ent is None or ent[0].numel() < nbytes:
+        size = max(nbytes, 2 * (ent[0].numel() if ent is not None else 0))
+        raw = torch.zeros(size + 256, dtype=torch.uint8, device=dev)
         off = (-raw.data_ptr()) % 256
-        buf = raw[off:off + size]
-        _ws[key] = buf
+        ent = [raw[off:off + size], size]   # buffer, known-zero prefix
+        _ws[key] = ent
+    buf, clean = ent
+    if zero_bytes > clean:
+        buf[clean:zero_bytes].zero_()
+        clean = zero_bytes
+    # after the call [0, zero_bytes) is zero again; scratch after it is not
+    ent[1] = zero_bytes if nbytes > zero_bytes else clean
     return buf
 
 
@@ -280,8 +292,13 @@ def gemv(layout: Layout, packed: torch.Tensor, perm: Optional[torch.Tensor], x: 
         raise ValueError("perm must be int32 [k]")
     if y is None:
         y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
-    need = gemv_workspace_bytes(layout, m) if 1 <= m <= MAX_M_GEMV else 0
-    ws = workspace if workspace is not None else _workspace("gemv", need, dev, zero=True)
+    if 1 <= m <= MAX_M_GEMV:
+        one = (GemvItem * 1)(GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y)))
+        need = int(lib().polyq_gemv_batch_workspace_bytes(one, 1, m))
+        zero = int(lib().polyq_gemv_batch_workspace_zero_bytes(one, 1, m))
+    else:
+        need = zero = 0
+    ws = workspace if workspace is not None else _workspace("gemv", need, dev, zero)
     _check(lib().polyq_gemv(ctypes.byref(layout), _ptr(packed), _ptr(perm), _ptr(x2), m, _ptr(y),
                             _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                             _stream(dev)), "polyq_gemv")
@@ -316,8 +333,12 @@ def gemv_batch(items: Sequence[Tuple[Layout, torch.Tensor, Optional[torch.Tensor
         arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y))
         keep.append(x2)
         ys.append(y)
-    need = int(lib().polyq_gemv_batch_workspace_bytes(arr, len(items), m)) if 1 <= m <= MAX_M_GEMV else 0
-    ws = workspace if workspace is not None else _workspace("gemv", need, dev, zero=True)
+    if 1 <= m <= MAX_M_GEMV:
+        need = int(lib().polyq_gemv_batch_workspace_bytes(arr, len(items), m))
+        zero = int(lib().polyq_gemv_batch_workspace_zero_bytes(arr, len(items), m))
+    else:
+        need = zero = 0
+    ws = workspace if workspace is not None else _workspace("gemv", need, dev, zero)
     _check(lib().polyq_gemv_batch(arr, len(items), m, _ptr(ws),
                                   0 if ws is None else ws.numel() * ws.element_size(), _stream(dev)),
            "polyq_gemv_batch")
@@ -335,7 +356,7 @@ def gemm(layout: Layout, packed: torch.Tensor, perm: Optional[torch.Tensor], x: 
     if y is None:
         y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
     need = gemm_workspace_bytes(layout, m, perm is not None)
-    ws = workspace if workspace is not None else _workspace("gemm", need, dev, zero=False)
+    ws = workspace if workspace is not None else _workspace("gemm", need, dev)
     _check(lib().polyq_gemm(ctypes.byref(layout), _ptr(packed), _ptr(perm), _ptr(x2), m, _ptr(y),
                             _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                             _stream(dev)), "polyq_gemm")
@@ -371,7 +392,7 @@ def gemm_batch(items: Sequence[Tuple[Layout, torch.Tensor, Optional[torch.Tensor
         keep.append(x2)
         ys.append(y)
     need = int(lib().polyq_gemm_batch_workspace_bytes(arr, len(items), m))
-    ws = workspace if workspace is not None else _workspace("gemm", need, dev, zero=False)
+    ws = workspace if workspace is not None else _workspace("gemm", need, dev)
     _check(lib().polyq_gemm_batch(arr, len(items), m, _ptr(ws),
                                   0 if ws is None else ws.numel() * ws.element_size(), _stream(dev)),
            "polyq_gemm_batch")
@@ -421,6 +442,9 @@ class PreparedBatch:
             need = int(L.polyq_gemv_batch_workspace_bytes(self.arr, self.count, m)) if 1 <= m <= MAX_M_GEMV else 0
         else:
             need = int(L.polyq_gemm_batch_workspace_bytes(self.arr, self.count, m))
+        # A workspace of its own (or one shared by prepared launches of the
+        # same plan, which all leave the split-K state zero and write their
+        # scratch after it): allocated zero-filled.
         if workspace is None and need:
             raw = (torch.zeros if kind == "gemv" else torch.empty)(need + 256, dtype=torch.uint8, device=dev)
             off = (-raw.data_ptr()) % 256

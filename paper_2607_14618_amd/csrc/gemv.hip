@@ -913,8 +913,21 @@ using namespace polyq;
 namespace {
 
 // Plans of a batch: every linear's splits are sized for the whole launch.
-polyq_status plan_batch(const polyq_gemv_item* items, int32_t count, int32_t m, GemvPlan* plans,
-                        size_t* ws_offset, size_t* ws_total, size_t* lds) {
+// Workspace: per item its split-K region (counters, partials; the part that
+// must be zero on entry and is zero again on return), then one clustered copy
+// x' = x[:, perm] per distinct (x, perm) of the items that take Eq. 9's
+// explicit shuffle (several tokens with a permutation: each wave then stages
+// its tokens' activations with 16-byte loads instead of one 2-byte gather per
+// channel and token).
+struct BatchPlan {
+  GemvPlan plans[POLYQ_MAX_BATCH];
+  size_t split_off[POLYQ_MAX_BATCH];
+  int64_t xp_off[POLYQ_MAX_BATCH];  // -1: the item reads x as given
+  bool xp_first[POLYQ_MAX_BATCH];   // this item's copy is made here (not shared with an earlier item)
+  size_t zero, total, lds;
+};
+
+polyq_status plan_batch(const polyq_gemv_item* items, int32_t count, int32_t m, BatchPlan* bp) {
   if (items == nullptr || count < 1) return POLYQ_ERR_ARG;
   if (count > POLYQ_MAX_BATCH) return POLYQ_ERR_CAPACITY;
   if (m < 1) return POLYQ_ERR_ARG;
@@ -927,18 +940,35 @@ polyq_status plan_batch(const polyq_gemv_item* items, int32_t count, int32_t m, 
   size_t off = 0, l = 0;
   for (int i = 0; i < count; ++i) {
     const polyq_layout& L = *items[i].layout;
-    if (plan_gemv(L, m, tiles, &plans[i]) != 0 || plans[i].W != kWaves) return POLYQ_ERR_CAPACITY;
-    ws_offset[i] = off;
-    off += static_cast<size_t>(align_up(static_cast<int64_t>(gemv_workspace_for(L, m, plans[i])), 256));
-    l = std::max(l, gemv_lds_bytes(plans[i], m));
+    if (plan_gemv(L, m, tiles, &bp->plans[i]) != 0 || bp->plans[i].W != kWaves) return POLYQ_ERR_CAPACITY;
+    bp->split_off[i] = off;
+    off += static_cast<size_t>(align_up(static_cast<int64_t>(gemv_workspace_for(L, m, bp->plans[i])), 256));
+    l = std::max(l, gemv_lds_bytes(bp->plans[i], m));
   }
-  *ws_total = off;
-  *lds = l;
+  bp->zero = off;
+  for (int i = 0; i < count; ++i) {
+    bp->xp_off[i] = -1;
+    bp->xp_first[i] = false;
+    if (m == 1 || items[i].perm == nullptr) continue;
+    for (int j = 0; j < i; ++j)
+      if (bp->xp_off[j] >= 0 && items[j].perm == items[i].perm && items[j].x == items[i].x &&
+          items[j].layout->k == items[i].layout->k) {
+        bp->xp_off[i] = bp->xp_off[j];
+        break;
+      }
+    if (bp->xp_off[i] < 0) {
+      bp->xp_off[i] = static_cast<int64_t>(off);
+      bp->xp_first[i] = true;
+      off += static_cast<size_t>(align_up(static_cast<int64_t>(m) * items[i].layout->k * 2, 256));
+    }
+  }
+  bp->total = off;
+  bp->lds = l;
   return POLYQ_OK;
 }
 
 // Pointer and alignment checks of every item (the planner reads only the
-// layouts).
+// layouts, permutations and activation pointers).
 polyq_status check_items(const polyq_gemv_item* items, int32_t count) {
   for (int i = 0; i < count; ++i) {
     const polyq_gemv_item& t = items[i];
@@ -958,14 +988,14 @@ polyq_status check_items(const polyq_gemv_item* items, int32_t count) {
 namespace polyq {
 
 polyq_status gemv_batch_workspace_status(const polyq_gemv_item* items, int32_t count, int32_t m,
-                                         size_t* need) {
-  GemvPlan plans[POLYQ_MAX_BATCH];
-  size_t offs[POLYQ_MAX_BATCH], total = 0, lds = 0;
-  const polyq_status st = plan_batch(items, count, m, plans, offs, &total, &lds);
+                                         size_t* need, size_t* zero) {
+  BatchPlan bp;
+  const polyq_status st = plan_batch(items, count, m, &bp);
   if (st != POLYQ_OK) return st;
   const polyq_status ct = check_items(items, count);
   if (ct != POLYQ_OK) return ct;
-  *need = total;
+  *need = bp.total;
+  *zero = bp.zero;
   return POLYQ_OK;
 }
 
@@ -973,41 +1003,48 @@ polyq_status gemv_batch_workspace_status(const polyq_gemv_item* items, int32_t c
 
 extern "C" size_t polyq_gemv_batch_workspace_bytes(const polyq_gemv_item* items, int32_t count,
                                                    int32_t m) {
-  GemvPlan plans[POLYQ_MAX_BATCH];
-  size_t offs[POLYQ_MAX_BATCH], total = 0, lds = 0;
-  if (plan_batch(items, count, m, plans, offs, &total, &lds) != POLYQ_OK) return 0;
-  return total;
+  BatchPlan bp;
+  if (plan_batch(items, count, m, &bp) != POLYQ_OK) return 0;
+  return bp.total;
+}
+
+extern "C" size_t polyq_gemv_batch_workspace_zero_bytes(const polyq_gemv_item* items, int32_t count,
+                                                        int32_t m) {
+  BatchPlan bp;
+  if (plan_batch(items, count, m, &bp) != POLYQ_OK) return 0;
+  return bp.zero;
 }
 
 extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t count, int32_t m,
                                          void* workspace, size_t workspace_bytes, void* stream) {
-  GemvPlan plans[POLYQ_MAX_BATCH];
-  size_t offs[POLYQ_MAX_BATCH], total = 0, lds = 0;
-  const polyq_status st = plan_batch(items, count, m, plans, offs, &total, &lds);
+  BatchPlan bp;
+  const polyq_status st = plan_batch(items, count, m, &bp);
   if (st != POLYQ_OK) return st;
   const polyq_status ct = check_items(items, count);
   if (ct != POLYQ_OK) return ct;
-  if (total > 0 && (workspace == nullptr || workspace_bytes < total)) return POLYQ_ERR_CAPACITY;
-  if (total > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return POLYQ_ERR_ARG;
+  if (bp.total > 0 && (workspace == nullptr || workspace_bytes < bp.total)) return POLYQ_ERR_CAPACITY;
+  if (bp.total > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return POLYQ_ERR_ARG;
 
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
   GemvBatchArgs a;
   memset(&a, 0, sizeof(a));
   int wgs = 0;
   for (int i = 0; i < count; ++i) {
     const polyq_gemv_item& t = items[i];
     const polyq_layout& L = *t.layout;
-    const GemvPlan& p = plans[i];
+    const GemvPlan& p = bp.plans[i];
     GemvItem& g = a.item[i];
+    const bool shuffled = bp.xp_off[i] >= 0;
     g.packed = static_cast<const uint8_t*>(t.packed);
-    g.perm = t.perm;
-    g.x = t.x;
+    g.perm = shuffled ? nullptr : t.perm;
+    g.x = shuffled ? reinterpret_cast<const uint16_t*>(ws + bp.xp_off[i]) : t.x;
     g.y = t.y;
     g.partial = nullptr;
     g.counter = nullptr;
     if (p.S > 1) {  // [counters: n_tiles x u32, 256-aligned][partials: S x m x rows_pad fp32]
-      uint8_t* ws = static_cast<uint8_t*>(workspace) + offs[i];
-      g.counter = reinterpret_cast<uint32_t*>(ws);
-      g.partial = reinterpret_cast<float*>(ws + align_up(static_cast<int64_t>(L.n_tiles) * 4, 256));
+      uint8_t* w = ws + bp.split_off[i];
+      g.counter = reinterpret_cast<uint32_t*>(w);
+      g.partial = reinterpret_cast<float*>(w + align_up(static_cast<int64_t>(L.n_tiles) * 4, 256));
     }
     g.n = L.n;
     g.k = L.k;
@@ -1034,9 +1071,13 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
     }
     wgs = std::max(wgs, L.n_tiles * p.S);
   }
-
-  hipLaunchKernelGGL(gemv_kernel, dim3(wgs, count), dim3(kWaves * 64), lds,
-                     static_cast<hipStream_t>(stream), a);
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  // Eq. 9's explicit shuffle first, once per distinct (x, perm) of several tokens
+  for (int i = 0; i < count; ++i)
+    if (bp.xp_first[i])
+      launch_permute_rows(items[i].perm, items[i].x, reinterpret_cast<uint16_t*>(ws + bp.xp_off[i]), m,
+                          items[i].layout->k, hs);
+  hipLaunchKernelGGL(gemv_kernel, dim3(wgs, count), dim3(kWaves * 64), bp.lds, hs, a);
   return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
 }
 

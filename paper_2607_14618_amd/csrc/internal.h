@@ -98,8 +98,16 @@ size_t gemv_lds_bytes(const GemvPlan& p, int32_t m);
 
 // Validation and workspace size of a polyq_gemv_batch request: every check
 // polyq_gemv_batch makes before it launches, except the workspace's own.
+// need: total bytes; zero: the leading bytes that must be zero on entry.
 polyq_status gemv_batch_workspace_status(const polyq_gemv_item* items, int32_t count, int32_t m,
-                                         size_t* need);
+                                         size_t* need, size_t* zero);
+
+// Explicit activation shuffle out[i][j] = x[i][perm[j]] (Eq. 9) for m rows of
+// k 2-byte values on `stream` (an entry outside [0, k) yields 0); rows are
+// staged in LDS when k and the alignments allow.  Launch only: the caller has
+// validated the arguments.
+void launch_permute_rows(const int32_t* perm, const uint16_t* x, uint16_t* out, int32_t m, int32_t k,
+                         hipStream_t stream);
 
 // Block accessor of a layout for wave_range (host side).
 struct LayoutBlocks {

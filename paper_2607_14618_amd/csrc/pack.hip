@@ -138,6 +138,60 @@ __global__ __launch_bounds__(kThreads) void permute_kernel(const int32_t* __rest
   out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
 }
 
+// x'[i][j] = x[i][perm[j]] for one token row per work-group: the row is staged
+// in LDS with 16-byte loads, then gathered there and written with 16-byte
+// stores (k <= kPermLdsK, rows 16-byte aligned).
+constexpr int kPermLdsK = 32768;
+
+__global__ __launch_bounds__(256) void permute_rows_lds_kernel(const int32_t* __restrict__ perm,
+                                                               const uint16_t* __restrict__ x,
+                                                               uint16_t* __restrict__ out, int k) {
+  extern __shared__ uint4 row4[];
+  const uint16_t* row = reinterpret_cast<const uint16_t*>(row4);
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * k;
+  const uint4* src = reinterpret_cast<const uint4*>(x + base);
+  const int4* p4 = reinterpret_cast<const int4*>(perm);
+  // The indices of the first kPre passes are loaded together with the row (one
+  // memory round trip for both).
+  constexpr int kPre = 4;
+  int4 pp[kPre][2];
+#pragma unroll
+  for (int u = 0; u < kPre; ++u) {
+    const int j = threadIdx.x + u * 256;
+    if (j < k / 8) {
+      pp[u][0] = p4[2 * j];
+      pp[u][1] = p4[2 * j + 1];
+    }
+  }
+  for (int j = threadIdx.x; j < k / 8; j += 256) row4[j] = src[j];
+  __syncthreads();
+  uint4* dst = reinterpret_cast<uint4*>(out + base);
+  auto gather = [&](int j, int4 p0, int4 p1) {
+    const int p[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+    uint32_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = static_cast<unsigned>(p[e]) < static_cast<unsigned>(k) ? row[p[e]] : 0u;
+    dst[j] = uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+  };
+#pragma unroll
+  for (int u = 0; u < kPre; ++u) {
+    const int j = threadIdx.x + u * 256;
+    if (j < k / 8) gather(j, pp[u][0], pp[u][1]);
+  }
+  for (int j = threadIdx.x + kPre * 256; j < k / 8; j += 256) gather(j, p4[2 * j], p4[2 * j + 1]);
+}
+
+// Fallback gather, one element per thread (any k, any alignment).
+__global__ __launch_bounds__(256) void permute_rows_kernel(const int32_t* __restrict__ perm,
+                                                           const uint16_t* __restrict__ x,
+                                                           uint16_t* __restrict__ out, int m, int k) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(m) * k) return;
+  const int i = static_cast<int>(idx / k), kp = static_cast<int>(idx % k);
+  const int p = perm[kp];
+  out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
+}
+
 template <int B>
 void launch_pack(const polyq_layout& L, int i, const uint16_t* codes, const int32_t* row_perm,
                  uint8_t* region, hipStream_t st) {
@@ -159,6 +213,20 @@ void launch_unpack(const polyq_layout& L, int i, const uint8_t* region, uint16_t
 }
 
 }  // namespace
+
+void launch_permute_rows(const int32_t* perm, const uint16_t* x, uint16_t* out, int32_t m, int32_t k,
+                         hipStream_t st) {
+  if (k <= kPermLdsK && k % 8 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+      reinterpret_cast<uintptr_t>(perm) % 16 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) {
+    hipLaunchKernelGGL(permute_rows_lds_kernel, dim3(static_cast<unsigned>(m)), dim3(256),
+                       static_cast<size_t>(k) * 2, st, perm, x, out, k);
+  } else {
+    const int64_t n_el = static_cast<int64_t>(m) * k;
+    hipLaunchKernelGGL(permute_rows_kernel, dim3(static_cast<unsigned>((n_el + 255) / 256)), dim3(256), 0,
+                       st, perm, x, out, m, k);
+  }
+}
+
 }  // namespace polyq
 
 using namespace polyq;

@@ -210,8 +210,12 @@ size_t gemv_workspace_for(const polyq_layout& L, int32_t m, const GemvPlan& p) {
 }  // namespace polyq
 
 extern "C" size_t polyq_gemv_workspace_bytes(const polyq_layout* layout, int32_t m) {
+  // enough with or without a permutation: the split-K state, and for several
+  // tokens the clustered copy of x that a call with a permutation makes first
   if (!polyq::layout_is_valid(layout) || m < 1 || m > POLYQ_MAX_M_GEMV) return 0;
   polyq::GemvPlan p;
   if (polyq::plan_gemv(*layout, m, layout->n_tiles, &p) != 0) return 0;
-  return polyq::gemv_workspace_for(*layout, m, p);
+  size_t need = static_cast<size_t>(polyq::align_up(static_cast<int64_t>(polyq::gemv_workspace_for(*layout, m, p)), 256));
+  if (m > 1) need += static_cast<size_t>(polyq::align_up(static_cast<int64_t>(m) * layout->k * 2, 256));
+  return need;
 }
