@@ -21,7 +21,9 @@
 // accumulation rounds.  16-bit channels enter the MFMA as their fp16 weights.
 //
 // Each wave stages its own channel range of the permuted activations
-// x'[k'] = x[perm[k']] (Eq. 9) and of the group metadata into LDS; the waves of
+// x'[k'] = x[perm[k']] (Eq. 9) and of the group metadata into LDS (one token
+// gathers through the permutation in-kernel; for several, the host launch
+// shuffles x once beforehand and the kernel reads x' as given); the waves of
 // a work-group (tile, split) reduce through LDS, and the splits of a tile
 // across work-groups are combined by the last-arriving work-group (fixed
 // order).
@@ -546,7 +548,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   // a step is issued before the first of them is used.
   constexpr int kRound = 64 * 8;
   constexpr int kFastRounds = 4;
-  constexpr int kTokBatch = 8;  // tokens gathered per memory round trip (m > 1)
+  constexpr int kTokBatch = 8;  // tokens staged per memory round trip (m > 1)
   const int fast_end = min(range, kFastRounds * kRound);
   const int rounds = max((fast_end + kRound - 1) / kRound, 1);
   const bool use_perm = perm != nullptr;
@@ -645,37 +647,6 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
         store_x(u, uint4{h[u][0] | (h[u][1] << 16), h[u][2] | (h[u][3] << 16),
                          h[u][4] | (h[u][5] << 16), h[u][6] | (h[u][7] << 16)});
       store_meta(rounds_tag);
-      // (2') Tokens 1..m-1 through the same permutation slices (still in
-      // registers): per round, one 2-byte gather per channel and token through
-      // the token row's bounded buffer, kTokBatch tokens per memory round trip.
-      if (m > 1) {
-#pragma unroll
-        for (int u = 0; u < R; ++u) {
-          const uint32_t p8[8] = {pv[u][0].x, pv[u][0].y, pv[u][0].z, pv[u][0].w,
-                                  pv[u][1].x, pv[u][1].y, pv[u][1].z, pv[u][1].w};
-          uint32_t off[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) off[e] = min(p8[e], static_cast<uint32_t>(kdim)) << 1;
-          const int kk = u * kRound + lane * 8;
-          for (int t0 = 1; t0 < m; t0 += kTokBatch) {
-            uint32_t g[kTokBatch][8];
-#pragma unroll
-            for (int j = 0; j < kTokBatch; ++j) {
-              const __amdgpu_buffer_rsrc_t rrow = tile_rsrc(
-                  reinterpret_cast<const uint8_t*>(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim),
-                  2 * static_cast<int64_t>(kdim));
-#pragma unroll
-              for (int e = 0; e < 8; ++e) g[j][e] = __builtin_amdgcn_raw_buffer_load_b16(rrow, off[e], 0, 0);
-            }
-#pragma unroll
-            for (int j = 0; j < kTokBatch; ++j)
-              if (t0 + j < m && kk < fast_end)
-                *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) =
-                    uint4{g[j][0] | (g[j][1] << 16), g[j][2] | (g[j][3] << 16), g[j][4] | (g[j][5] << 16),
-                          g[j][6] | (g[j][7] << 16)};
-          }
-        }
-      }
     }
   };
   using I1 = std::integral_constant<int, 1>;
@@ -703,11 +674,11 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       }
     }
     // (6) More tokens, or channels past the fast rounds (these loads wait behind
-    // the weight slots).  Tokens go in batches of kTokBatch, every load of a
-    // batch issued before the first of them is used (one memory round trip per
-    // batch): a 16-byte load per token for clustered x, else one 2-byte gather
-    // per channel and token through the token row's bounded buffer (indices
-    // outside [0, k) read 0).
+    // the weight slots).  Clustered x: tokens go in batches of kTokBatch, every
+    // load of a batch issued before the first of them is used (one memory
+    // round trip per batch), a 16-byte load per token.  With a permutation
+    // (one token): one 2-byte gather per channel through token 0's bounded
+    // buffer (indices outside [0, k) read 0).
     auto stage_slow = [&](int k_lo, int k_hi, int t_lo, bool zero_row) {
       for (int kk = k_lo + lane * 8; kk < k_hi; kk += kRound) {
         if (!use_perm) {
@@ -721,28 +692,16 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
               if (t0 + j < m) *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) = v[j];
           }
         } else {
+          // a permutation comes with one token (several take the explicit
+          // shuffle first): one 2-byte gather per channel
           const uint4 p0 = ldg16(perm + kbase + kk), p1 = ldg16(perm + kbase + kk + 4);
           const uint32_t p8[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-          uint32_t off[8];
+          uint32_t h[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) off[e] = min(p8[e], static_cast<uint32_t>(kdim)) << 1;
-          for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
-            uint32_t h[kTokBatch][8];
-#pragma unroll
-            for (int j = 0; j < kTokBatch; ++j) {
-              const __amdgpu_buffer_rsrc_t rrow = tile_rsrc(
-                  reinterpret_cast<const uint8_t*>(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim),
-                  2 * static_cast<int64_t>(kdim));
-#pragma unroll
-              for (int e = 0; e < 8; ++e) h[j][e] = __builtin_amdgcn_raw_buffer_load_b16(rrow, off[e], 0, 0);
-            }
-#pragma unroll
-            for (int j = 0; j < kTokBatch; ++j)
-              if (t0 + j < m)
-                *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) =
-                    uint4{h[j][0] | (h[j][1] << 16), h[j][2] | (h[j][3] << 16), h[j][4] | (h[j][5] << 16),
-                          h[j][6] | (h[j][7] << 16)};
-          }
+          for (int e = 0; e < 8; ++e)
+            h[e] = __builtin_amdgcn_raw_buffer_load_b16(xrs, min(p8[e], static_cast<uint32_t>(kdim)) << 1, 0, 0);
+          *reinterpret_cast<uint4*>(xs16 + kk) =
+              uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
         }
         if (zero_row) *reinterpret_cast<uint4*>(zs16 + kk) = uint4{0u, 0u, 0u, 0u};
       }
