@@ -23,11 +23,15 @@ CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", f"-I{INCLUDE}"
           "-Wno-unused-function"]
 # Per-source additions.  The decode GEMV keeps its small MFMA accumulators in
 # VGPRs (they feed VALU folds every group; the AGPR form costs a copy each way).
-# The prefill GEMM keeps its accumulators in VGPRs too (the group fold reads
-# them every 128 channels) and its private arrays out of LDS (with one
-# work-group per CU the compiler would otherwise move one there).
+# The prefill GEMM keeps its accumulators in VGPRs too (the group rescale
+# reads them every 128 channels), its private arrays out of LDS (with one
+# work-group per CU the compiler would otherwise move one there), and its
+# loop invariants in the loops that use them (hoisted to the kernel entry they
+# would stay live across every bit-width's store and overflow the 256
+# registers a wave of an 8-wave work-group can have).
 EXTRA = {"gemv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-         "gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-disable-promote-alloca-to-lds"]}
+         "gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-disable-promote-alloca-to-lds",
+                      "-mllvm", "-disable-machine-licm"]}
 
 
 def _compile(src: str) -> str:

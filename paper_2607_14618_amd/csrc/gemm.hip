@@ -2,30 +2,35 @@
 //   y[m][n] = sum_k' w_hat[n][k'] x'[m][k'],  x' = x[:, perm] (Eq. 9)
 //
 // Prefill is a dense contraction, so it runs on the bf16 matrix cores
-// (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  A work-group owns 256 tokens
-// x 64*TN weight rows (TN packed tiles) and walks K one 32-channel chunk at a
-// time through a two-stage LDS ring:
-//   * every thread prefetches, two chunks ahead, 32 or 64 bytes of activations
-//     and its share of the packed chunk (one row sub-tile of one lane slice,
-//     4*b/4 .. 4*b bytes) plus that row's zero point;
+// (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  A work-group of 8 waves owns
+// 256 tokens x 128 weight rows (two packed tiles) and walks K one 32-channel
+// chunk at a time through a two-stage LDS ring:
+//   * every thread prefetches, two chunks ahead, 32 bytes of activations and
+//     its share of the packed chunk (8 codes of one row: one row sub-tile of
+//     one lane slice) plus that row's zero point and scale;
 //   * the packed share is dequantized once per work-group into a bf16 tile in
-//     LDS that all waves of the work-group multiply (weights are the MFMA A
-//     operand, activations the B operand);
-//   * wave (tq, rt) multiplies rows 64*rt.. by tokens 64*tq..: 16 MFMAs per
+//     LDS that all waves multiply (weights are the MFMA A operand, activations
+//     the B operand);
+//   * wave (tq, rt) multiplies rows 64 rt.. by tokens 64 tq..: 16 MFMAs per
 //     chunk; one barrier per chunk.
-// Group-fold numerics: the dequantized operand is (q - z), an integer of
-// magnitude <= 255 that bf16 holds exactly when z is an integer; each
-// 128-channel group accumulates into its own fp32 tile, which is then scaled
-// by the row's fp16 scale s (fp32 FMA) into the output accumulator.  A 16-bit
-// channel, or a group whose zero point is not an integer, enters as the pair
-// hi + lo of bf16 values (two MFMAs); for 16-bit weights the pair is exact.
+// The loop is specialized per bit-width: a block's chunks run through the
+// copy of the loop compiled for its bit-width, one 128-channel group per
+// iteration, so the unpack, the group start and the group fold are fixed at
+// compile time and a step's common path has no branch.  The blocks (whose
+// bit-widths ascend) are visited by straight-line code, one copy per
+// bit-width, so that no loop carries the accumulators through every copy.
 //
-// Dequantization uses the fp16 exponent field: (1024 + q) is the fp16 with
-// exponent 10 and mantissa q, so one AND-OR forms two codes of a pair as fp16.
-// For an integer z in [0, 255] one fp32 subtract of (1024 + z) gives q - z
-// exactly and the bf16 value is the fp32 value's upper half; for any other
-// fp16 z, (1024 + q) - 1024 = q exactly and q - z rounds once in fp32 before
-// the split into hi + lo.
+// Numerics.  The dequantized operand is (q - z), an integer of magnitude
+// <= 255 that bf16 holds exactly when z is an integer in [0, 255]; each
+// 128-channel group accumulates into its own fp32 tile, which is then scaled
+// by the row's fp16 scale s (fp32 FMA) into the output accumulator.  A code
+// field at bit f of a half-word, OR-ed with the fp16 exponent field 25 - f,
+// reads as the fp16 value 2^(10-f) + q (exact), and one packed fp16 add of
+// -(2^(10-f) + z) leaves q - z exactly for such z; the bf16 value is the upper
+// half of its fp32 conversion.  A 16-bit channel, or a group whose zero point
+// is not such an integer, enters as the pair hi + lo of bf16 values (two
+// MFMAs): for fp16 weights the pair is exact; for any other z, q is recovered
+// exactly in fp32 and q - z rounds once before the split.
 #include <hip/hip_runtime.h>
 
 #include <string.h>
@@ -42,10 +47,14 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
-constexpr int kTokWG = 256;   // tokens per work-group: 4 waves of 64 along M
-constexpr int kLdsRow = 40;   // bf16 per LDS row: 32 channels + 8 pad against bank conflicts
-constexpr uint32_t kMagic2 = 0x64006400u;  // two fp16 1024.0
+constexpr int kTokWG = 256;                 // tokens per work-group
+constexpr int kRowsWG = 2 * kTileRows;      // weight rows per work-group (two packed tiles)
+constexpr int kThreads = 512;               // 8 waves
+constexpr int kLdsRow = 40;                 // bf16 per LDS row: 32 channels + 8 pad against bank conflicts
+constexpr int kStageA = kTokWG * kLdsRow;   // bf16 of one activation stage
+constexpr int kStageB = kRowsWG * kLdsRow;  // bf16 of one weight tile (hi or lo) of a stage
 
 // One linear of a launch.
 struct GemmItem {
@@ -78,64 +87,98 @@ struct GemmBatchArgs {
   float* partial;
 };
 
-// Position of a pipeline stage in the chunk sequence: chunk c, chunk cl of
-// block bi (bit-width bits, ending at chunk ce).  Advanced one chunk at a
-// time; the block table is read (from the kernel arguments) only when a block
-// ends.
-struct ChunkCursor {
-  int c, bi, bits, cl, ce;
-  __device__ __forceinline__ bool first() const { return (cl & 3) == 0; }
-  __device__ __forceinline__ bool last() const { return (cl & 3) == 3 || c + 1 == ce; }
-};
-
-typedef uint32_t u4v __attribute__((ext_vector_type(4)));
-
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
                                            static_cast<int>(bytes), 0x00020000);
 }
 
 // Prefetched data of one chunk for one thread.
-template <int TN>
 struct Pre {
-  u4v av[4 / TN];  // activation pieces (16 bytes each)
-  u4v w;           // 16 bytes from this thread's packed sub-tile (the first 4*b/4 .. 16 used)
-  uint32_t z, s;   // its row's fp16 zero point and scale (bits), b <= 8
+  u4v av[2];     // two 16-byte activation pieces
+  u4v w;         // 16 bytes at this thread's row sub-tile of its lane slice (b bytes used, 12 for 3 bits)
+  uint32_t z, s; // fp16 zero point and scale of the thread's row (loaded at a group's first chunk)
 };
 
-// Two codes of a pair as fp16 (1024 + q): the fields sit at bit offsets o and
-// 16 + o of w.
-__device__ __forceinline__ uint32_t pair_magic(uint32_t w, int o, uint32_t mask2) {
-  return ((w >> o) & mask2) | kMagic2;
+__host__ __device__ constexpr uint32_t exp_field(int e) { return (static_cast<uint32_t>(e) << 10) * 0x00010001u; }
+
+// The fields at bits f and 16 + f of w (mask m2 covers both, already shifted
+// to f) as the fp16 pair (2^(10-f) + q_even, 2^(10-f) + q_odd).
+__device__ __forceinline__ uint32_t field_pair(uint32_t w, uint32_t m2, int f) {
+  return (w & m2) | exp_field(25 - f);
 }
 
 // The 4 code pairs (channels 2j, 2j+1) of row sub-tile r of a lane slice, in
-// the slice arrangement of codec.h, as fp16 pairs (1024 + q).
+// the arrangement of codec.h, as fp16 pairs (off[j] + q) with off[j] =
+// 2^(10 - f) for the field position f each pair is read at.  `w` holds the
+// 16 bytes loaded at the sub-tile's offset (sub_offset); r is wave-uniform.
 template <int B>
-__device__ __forceinline__ void sub_tile_pairs(const u4v w, int r, uint32_t* hp) {
-  if constexpr (B == 2) {  // word r/2 (loaded as w.x) holds sub-tiles r & ~1 and r | 1
-    const int sh = 8 * (r & 1);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) hp[j] = pair_magic(w.x, sh + 2 * j, 0x00030003u);
-  } else if constexpr (B == 4) {  // word r
-#pragma unroll
-    for (int j = 0; j < 4; ++j) hp[j] = pair_magic(w.x, 4 * j, 0x000F000Fu);
-  } else if constexpr (B == 8) {  // words 2r, 2r+1
-#pragma unroll
-    for (int j = 0; j < 4; ++j) hp[j] = pair_magic((j >> 1) ? w.y : w.x, 8 * (j & 1), 0x00FF00FFu);
-  } else {  // B == 3: all three words; pair P = 4r + j sits in word P/5 at f3(P%5)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int P = 4 * r + j;
-      if (P < 15) {
-        const int d = P / 5, p = P - 5 * d;
-        const uint32_t wd = d == 0 ? w.x : (d == 1 ? w.y : w.z);
-        hp[j] = pair_magic(wd, 3 * p + (p >= 3 ? 1 : 0), 0x00070007u);
-      } else {  // codes 30, 31: bit d of each in bits 9 and 25 of word d
-        const uint32_t t = ((w.x >> 9) & 0x00010001u) | ((w.y >> 8) & 0x00020002u) |
-                           ((w.z >> 7) & 0x00040004u);
-        hp[j] = t | kMagic2;
-      }
+__device__ __forceinline__ void unpack_sub_tile(const u4v w, int r, uint32_t* hp) {
+  if constexpr (B == 2) {  // word r/2 holds sub-tiles r & ~1 (bits 0..7) and r | 1 (8..15)
+    const uint32_t u = w.x >> (8 * (r & 1));
+    hp[0] = field_pair(u, 0x00030003u, 0);
+    hp[1] = field_pair(u, 0x000C000Cu, 2);
+    hp[2] = field_pair(u, 0x00300030u, 4);
+    hp[3] = field_pair(u, 0x00C000C0u, 6);
+  } else if constexpr (B == 4) {  // word r, pairs at 0, 4, 8, 12
+    const uint32_t t = w.x >> 8;
+    hp[0] = field_pair(w.x, 0x000F000Fu, 0);
+    hp[1] = field_pair(w.x, 0x00F000F0u, 4);
+    hp[2] = field_pair(t, 0x000F000Fu, 0);
+    hp[3] = field_pair(t, 0x00F000F0u, 4);
+  } else if constexpr (B == 8) {  // words 2r, 2r+1, pairs at bytes (0, 2) and (1, 3); 0x64 = exponent 25
+    hp[0] = __builtin_amdgcn_perm(w.x, 0x64646464u, 0x00060004u);
+    hp[1] = __builtin_amdgcn_perm(w.x, 0x64646464u, 0x00070005u);
+    hp[2] = __builtin_amdgcn_perm(w.y, 0x64646464u, 0x00060004u);
+    hp[3] = __builtin_amdgcn_perm(w.y, 0x64646464u, 0x00070005u);
+  } else {  // B == 3: pair P = 4r + j in word P/5 at f3(P%5); fields at 10, 13 read after >> 10
+    const uint32_t t0 = w.x >> 10, t1 = w.y >> 10, t2 = w.z >> 10;
+    switch (r) {
+      case 0:
+        hp[0] = field_pair(w.x, 0x00070007u, 0);
+        hp[1] = field_pair(w.x, 0x00380038u, 3);
+        hp[2] = field_pair(w.x, 0x01C001C0u, 6);
+        hp[3] = field_pair(t0, 0x00070007u, 0);
+        break;
+      case 1:
+        hp[0] = field_pair(t0, 0x00380038u, 3);
+        hp[1] = field_pair(w.y, 0x00070007u, 0);
+        hp[2] = field_pair(w.y, 0x00380038u, 3);
+        hp[3] = field_pair(w.y, 0x01C001C0u, 6);
+        break;
+      case 2:
+        hp[0] = field_pair(t1, 0x00070007u, 0);
+        hp[1] = field_pair(t1, 0x00380038u, 3);
+        hp[2] = field_pair(w.z, 0x00070007u, 0);
+        hp[3] = field_pair(w.z, 0x00380038u, 3);
+        break;
+      default:  // codes 30, 31: bit d of each in bits 9 and 25 of word d
+        hp[0] = field_pair(w.z, 0x01C001C0u, 6);
+        hp[1] = field_pair(t2, 0x00070007u, 0);
+        hp[2] = field_pair(t2, 0x00380038u, 3);
+        hp[3] = ((w.x >> 9) & 0x00010001u) | ((w.y >> 8) & 0x00020002u) | ((w.z >> 7) & 0x00040004u) |
+                exp_field(25);
+        break;
+    }
+  }
+}
+
+// off[j] of unpack_sub_tile for sub-tile r.
+template <int B>
+__device__ __forceinline__ void pair_offsets(int r, float* off) {
+  if constexpr (B == 2) {
+    off[0] = 1024.f; off[1] = 256.f; off[2] = 64.f; off[3] = 16.f;
+  } else if constexpr (B == 4) {
+    off[0] = 1024.f; off[1] = 64.f; off[2] = 1024.f; off[3] = 64.f;
+  } else if constexpr (B == 8) {
+    off[0] = off[1] = off[2] = off[3] = 1024.f;
+  } else {
+    const float t[4][4] = {{1024.f, 128.f, 16.f, 1024.f}, {128.f, 1024.f, 128.f, 16.f},
+                           {1024.f, 128.f, 1024.f, 128.f}, {16.f, 1024.f, 128.f, 1024.f}};
+    switch (r) {
+      case 0: for (int j = 0; j < 4; ++j) off[j] = t[0][j]; break;
+      case 1: for (int j = 0; j < 4; ++j) off[j] = t[1][j]; break;
+      case 2: for (int j = 0; j < 4; ++j) off[j] = t[2][j]; break;
+      default: for (int j = 0; j < 4; ++j) off[j] = t[3][j]; break;
     }
   }
 }
@@ -149,16 +192,6 @@ __device__ __forceinline__ uint32_t hi_half_pair(float lo, float hi) {
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
   const uint32_t u = __builtin_bit_cast(uint32_t, f);
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
-
-// Eight values of one row, each exact in bf16, into the hi tile.
-__device__ __forceinline__ void store_exact(const float* v, uint16_t* hi_dst) {
-  uint4 o;
-  o.x = hi_half_pair(v[0], v[1]);
-  o.y = hi_half_pair(v[2], v[3]);
-  o.z = hi_half_pair(v[4], v[5]);
-  o.w = hi_half_pair(v[6], v[7]);
-  *reinterpret_cast<uint4*>(hi_dst) = o;
 }
 
 // Eight values of one row as the bf16 pair hi (nearest) + lo (nearest to the
@@ -182,13 +215,13 @@ __device__ __forceinline__ int sub_offset(int b, int r) {
   return b == 2 ? (r >> 1) * 4 : b == 4 ? r * 4 : b == 8 ? r * 8 : b == 16 ? r * 16 : 0;
 }
 
-template <int TN>
-__global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
-  constexpr int kThreads = 256 * TN, kRows = 64 * TN;
-  constexpr int kAPieces = 4 / TN;  // 16-byte activation pieces per thread per chunk
-  __shared__ __attribute__((aligned(16))) uint16_t lds_a[2][kTokWG * kLdsRow];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_b[2][2][kRows * kLdsRow];  // [stage][hi, lo]
-  __shared__ __attribute__((aligned(16))) float lds_s[2][kRows];                 // row scales of the stage's group
+template <int V>
+using Int = std::integral_constant<int, V>;
+
+__global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds_a[2 * kStageA];      // [stage][token][channel]
+  __shared__ __attribute__((aligned(16))) uint16_t lds_b[2 * 2 * kStageB];  // [stage][hi, lo][row][channel]
+  __shared__ __attribute__((aligned(16))) float lds_r[2 * kRowsWG];         // [stage][row] group scale
   __shared__ int lds_tag[2];  // chunk index + 1 when the stage holds a nonzero lo tile
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -204,51 +237,46 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
   const int mt = local % a.m_tiles, rest = local / a.m_tiles;
   const int ks = rest % a.splits, rp = rest / a.splits;
   const int m0 = mt * kTokWG;
-  // this work-group's chunks [c0, C)
+  // this work-group's chunks [c0, C), c0 at a group boundary
   const int c0 = a.splits > 1 ? a.split_chunk[ks] : 0;
   const int C = a.splits > 1 ? a.split_chunk[ks + 1] : it.n_chunks;
   int b0 = 0;
 #pragma unroll
   for (int j = 0; j < POLYQ_MAX_BLOCKS - 1; ++j) b0 += (j + 1 < it.nblocks && c0 >= it.ce[j]) ? 1 : 0;
-  auto cursor_at0 = [&]() { return ChunkCursor{c0, b0, it.bits[b0], c0 - it.cb[b0], it.ce[b0]}; };
-  auto advance = [&](ChunkCursor& u) {
-    ++u.c;
-    ++u.cl;
-    if (u.c == u.ce && u.c < C) {
-      ++u.bi;
-      u.bits = it.bits[u.bi];
-      u.ce = it.ce[u.bi];
-      u.cl = 0;
-    }
-  };
 
-  // Dequantization role: packed tile dt, row sub-tile dr (wave-uniform), lane
-  // slice lane; row drow of the tile.
+  // Dequantization role: packed tile dp, row sub-tile dr (wave-uniform), lane
+  // slice `lane`: row drow of the tile, channels 8 (lane / 16) .. + 7.
   const int dp = wv >> 2, dr = wv & 3;
-  const int dt = rp * TN + dp;
+  const int dt = rp * 2 + dp;
   const bool dtile_ok = dt < it.n_tiles;
   const int drow = 16 * dr + (lane & 15);
-  const int bofs = (dp * 64 + drow) * kLdsRow + 8 * (lane >> 4);
-  constexpr int kHalfB = kRows * kLdsRow;
+  const int bst = (dp * 64 + drow) * kLdsRow + 8 * (lane >> 4);  // LDS slot of its 8 weights
+  const int sst = dp * 64 + drow;                                  // LDS slot of its row's scale
 
   // Activations: buffer over rows m0 .. m0 + 255 of x' (reads past row m - 1
   // return zero); piece j of this thread is token piece/4, 16-byte segment piece%4.
   const __amdgpu_buffer_rsrc_t xrs =
       make_rsrc(it.x + static_cast<int64_t>(m0) * it.k, static_cast<uint32_t>(min(a.m - m0, kTokWG)) * it.k * 2u);
-  uint32_t avoff[kAPieces];
+  uint32_t avoff[2];
+  int ast[2];
 #pragma unroll
-  for (int j = 0; j < kAPieces; ++j) {
+  for (int j = 0; j < 2; ++j) {
     const int piece = tid + j * kThreads;
     avoff[j] = (static_cast<uint32_t>(piece >> 2) * it.k + (piece & 3) * 8) * 2u;
+    ast[j] = (piece >> 2) * kLdsRow + (piece & 3) * 8;
   }
+  // MFMA fragment reads: tokens 64 tq + 16 j + lane%16 (B), rows 64 rt + 16 i + lane%16 (A)
+  const int ard = (tq * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
+  const int brd = (rt * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
 
   // Load cursor: the next chunk to fetch, its block and a buffer over this
   // thread's packed tile of that block (no records for a tile past the end,
-  // so its reads return zero).
+  // so its reads return zero).  Block-generic: it runs ahead of the
+  // bit-width-specialized loop across block boundaries.
   int lc = c0, lb = 0, lcl = 0, lbits = 0, lce = 0, lrb = 0;
   uint32_t lvoff = 0;
   __amdgpu_buffer_rsrc_t wrs;
-  auto set_block = [&](int b) {
+  auto set_block = [&](int b) __attribute__((always_inline)) {
     lb = b;
     lbits = it.bits[b];
     lce = it.ce[b];
@@ -260,13 +288,16 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
     lcl = 0;
   };
   const uint32_t zvoff = 2 * meta_z_half(drow), svoff = 2 * meta_s_half(drow);
-  auto load = [&](Pre<TN>& pr) {
+  auto load = [&](Pre& pr) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < kAPieces; ++j)
+    for (int j = 0; j < 2; ++j)
       pr.av[j] = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, avoff[j], lc * 64, 0));
     const int rec = (lcl >> 2) * lrb;
     const int soff = rec + (lbits <= 8 ? kMetaBytes : 0) + (lcl & 3) * 256 * lbits;
     pr.w = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(wrs, lvoff, soff, 0));
+    // the row's z and s of the chunk's group (used at a group's first chunk;
+    // loaded for every chunk, so that every slot has the same loads in flight
+    // and each wait can leave the younger slot's loads outstanding)
     pr.z = __builtin_amdgcn_raw_buffer_load_b16(wrs, zvoff, rec, 0);
     pr.s = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff, rec, 0);
     ++lc;
@@ -274,516 +305,247 @@ __global__ __launch_bounds__(256 * TN) void gemm_kernel(const GemmBatchArgs a) {
     if (lc == lce && lc < C) set_block(lb + 1);
   };
 
-  auto store = [&](const ChunkCursor& ci, const Pre<TN>& pr, int st) {
+  // Group state of the thread's row while its group is being stored: scale,
+  // zero point, whether every zero point of the wave is an integer in
+  // [0, 255] (wave-uniform), and the pair constants -(off[j] + z).
+  float gs = 0.f, gz = 0.f;
+  bool gexact = true;
+  h2 gc[4];
+  // bit st: this thread's lo slot of stage st may hold nonzero values (a
+  // 16-bit chunk or a pair-stored group used it); cleared before an exact
+  // store into the stage, since a stage's second MFMA pass reads every row.
+  uint32_t lo_dirty = 0;
+
+  // Dequantize one chunk (prefetched in pr) into stage st, with its rows'
+  // group scales.  first: the chunk starts a group (its z and s are in pr).
+  // The exact form (integer zero points) is always written, without
+  // branches; store_fix then rewrites the chunk as hi + lo pairs in a wave
+  // whose zero points are not all such integers.
+  auto store_main = [&](auto b_tag, const Pre& pr, int c, int st, bool first) __attribute__((always_inline)) {
+    constexpr int B = decltype(b_tag)::value;
+    uint16_t* sa = lds_a + st * kStageA;
 #pragma unroll
-    for (int j = 0; j < kAPieces; ++j) {
-      const int piece = tid + j * kThreads;
-      *reinterpret_cast<u4v*>(&lds_a[st][(piece >> 2) * kLdsRow + (piece & 3) * 8]) = pr.av[j];
-    }
-    uint16_t* hi = &lds_b[st][0][bofs];
-    uint16_t* lo = hi + kHalfB;
-    float v[8];
-    if (ci.bits == 16) {
+    for (int j = 0; j < 2; ++j) *reinterpret_cast<u4v*>(sa + ast[j]) = pr.av[j];
+    uint16_t* hi = lds_b + st * 2 * kStageB + bst;
+    uint16_t* lo = hi + kStageB;
+    if constexpr (B == 16) {
+      lds_r[st * kRowsWG + sst] = 1.f;  // the four threads of a row store the same value
       const uint32_t ww[4] = {pr.w.x, pr.w.y, pr.w.z, pr.w.w};
+      float v[8];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const h2 h = __builtin_bit_cast(h2, ww[i]);
         v[2 * i] = static_cast<float>(h.x);
         v[2 * i + 1] = static_cast<float>(h.y);
       }
-      lds_s[st][dp * 64 + drow] = 1.f;  // the four threads of a row store the same value
       store_pair(v, hi, lo);
+      lo_dirty |= 1u << st;
       return;
     }
-    const float zf = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.z)));
-    lds_s[st][dp * 64 + drow] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s)));
+    if (first) {
+      float off[4];
+      pair_offsets<B>(dr, off);
+      gz = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.z)));
+      gs = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s)));
+      gexact = __all(gz == truncf(gz) && gz >= 0.f && gz <= 255.f);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const _Float16 cz = static_cast<_Float16>(-(off[j] + gz));  // exact when gexact
+        gc[j] = h2{cz, cz};
+      }
+    }
+    lds_r[st * kRowsWG + sst] = gs;
     uint32_t hp[4];
-    switch (ci.bits) {
-      case 2: sub_tile_pairs<2>(pr.w, dr, hp); break;
-      case 3: sub_tile_pairs<3>(pr.w, dr, hp); break;
-      case 4: sub_tile_pairs<4>(pr.w, dr, hp); break;
-      default: sub_tile_pairs<8>(pr.w, dr, hp); break;
-    }
-    if (__all(zf == truncf(zf) && zf >= 0.f && zf <= 255.f)) {  // wave-uniform
-      // (1024 + q) - (1024 + z) = q - z: both sums are exact for such z, and
-      // so is the difference, in fp32 and in bf16 (|q - z| <= 255)
-      const float zoff = 1024.f + zf;
+    unpack_sub_tile<B>(pr.w, dr, hp);
+    // (off + q) - (off + z) = q - z exactly in fp16 (|q - z| <= 255), and
+    // exactly again in fp32 and in its upper half (bf16)
+    uint32_t o[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const h2 h = __builtin_bit_cast(h2, hp[j]);
-        v[2 * j] = static_cast<float>(h.x) - zoff;
-        v[2 * j + 1] = static_cast<float>(h.y) - zoff;
-      }
-      store_exact(v, hi);
-      *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
-    } else {
-      // any other fp16 z: ((1024 + q) - 1024) is q exactly, and q - z rounds
-      // once in fp32 (1024 + z itself would round for small non-integer z)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const h2 h = __builtin_bit_cast(h2, hp[j]);
-        v[2 * j] = (static_cast<float>(h.x) - 1024.f) - zf;
-        v[2 * j + 1] = (static_cast<float>(h.y) - 1024.f) - zf;
-      }
-      store_pair(v, hi, lo);
-      lds_tag[st] = ci.c + 1;  // any thread; every writer stores the same value
+    for (int j = 0; j < 4; ++j) {
+      const h2 d = __builtin_bit_cast(h2, hp[j]) + gc[j];
+      o[j] = hi_half_pair(static_cast<float>(d.x), static_cast<float>(d.y));
     }
+    *reinterpret_cast<uint4*>(hi) = uint4{o[0], o[1], o[2], o[3]};
+  };
+  auto store_fix = [&](auto b_tag, const Pre& pr, int c, int st) __attribute__((always_inline)) {
+    constexpr int B = decltype(b_tag)::value;
+    uint16_t* hi = lds_b + st * 2 * kStageB + bst;
+    uint16_t* lo = hi + kStageB;
+    if constexpr (B == 16) {
+      if (tid == 0) lds_tag[st] = c + 1;
+      return;
+    }
+    if (__builtin_expect(gexact, 1)) {
+      if (__builtin_expect(lo_dirty & (1u << st), 0)) {
+        *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
+        lo_dirty &= ~(1u << st);
+      }
+      return;
+    }
+    // any other fp16 z: (off + q) - off = q exactly, then q - z rounds once
+    float off[4];
+    pair_offsets<B>(dr, off);
+    uint32_t hp[4];
+    unpack_sub_tile<B>(pr.w, dr, hp);
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const h2 h = __builtin_bit_cast(h2, hp[j]);
+      v[2 * j] = (static_cast<float>(h.x) - off[j]) - gz;
+      v[2 * j + 1] = (static_cast<float>(h.y) - off[j]) - gz;
+    }
+    store_pair(v, hi, lo);
+    lo_dirty |= 1u << st;
+    lds_tag[st] = c + 1;  // any thread; every writer stores the same value
   };
 
-  f4 total[4][4], part[4][4];
+  f4 T[4][4], P[4][4];  // output accumulators, the group's partial sums
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) total[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) T[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-  const int aofs = (tq * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
-  const int bofs_m = (rt * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
-  // Chunk mc.c: multiply stage c&1, dequantize chunk c+1 (cursor sc) from
-  // `slot` into the other stage, fetch chunk c+3 into `slot`, fold a finished
-  // group.
-  ChunkCursor mc = cursor_at0(), sc = cursor_at0();
-  auto step = [&](Pre<TN>& slot, auto st_tag) {  // st = (c - c0) & 1, known at each call
-    constexpr int st = decltype(st_tag)::value;
-    const int c = mc.c;
-    const bool two = mc.bits == 16 || lds_tag[st] == c + 1;
+  // MFMA pass over stage st: the hi tile (first: fresh partial sums) or the
+  // lo tile.
+  auto mfma_pass = [&](int st, bool first, int tile) __attribute__((always_inline)) {
+    const uint16_t* sa = lds_a + st * kStageA;
+    const uint16_t* sb = lds_b + st * 2 * kStageB + tile * kStageB;
     bf16x8 af[4], bfr[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      af[i] = *reinterpret_cast<const bf16x8*>(&lds_b[st][0][bofs_m + i * 16 * kLdsRow]);
-      bfr[i] = *reinterpret_cast<const bf16x8*>(&lds_a[st][aofs + i * 16 * kLdsRow]);
+      af[i] = *reinterpret_cast<const bf16x8*>(sb + brd + i * 16 * kLdsRow);
+      bfr[i] = *reinterpret_cast<const bf16x8*>(sa + ard + i * 16 * kLdsRow);
     }
-    if (mc.first()) {  // first chunk of a group: fresh partial sums
+    if (first) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          part[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+          P[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], f4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
     } else {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) part[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], part[i][j], 0, 0, 0);
+        for (int j = 0; j < 4; ++j) P[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], P[i][j], 0, 0, 0);
     }
-    if (two) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(&lds_b[st][1][bofs_m + i * 16 * kLdsRow]);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) part[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], part[i][j], 0, 0, 0);
-    }
-    if (c + 1 < C) {
-      advance(sc);
-      store(sc, slot, st ^ 1);
-    }
-    if (c + 3 < C) load(slot);
-    if (mc.last()) {  // group fold: total += s * part, s of rows 16 i + 4 (lane/16) + e
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const f4 sv = *reinterpret_cast<const f4*>(&lds_s[st][rt * 64 + 16 * i + 4 * (lane >> 4)]);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) total[i][j][e] = fmaf(sv[e], part[i][j][e], total[i][j][e]);
-      }
-    }
-    advance(mc);
-    __syncthreads();
   };
-
-  Pre<TN> s0, s1;
-  if (tid < 2) lds_tag[tid] = 0;
-  set_block(b0);
-  lcl = c0 - it.cb[b0];
-  load(s0);
-  if (C - c0 > 1) load(s1);
-  __syncthreads();
-  store(sc, s0, 0);
-  if (C - c0 > 2) load(s0);
-  __syncthreads();
-  int c = c0;
-  for (; c + 1 < C; c += 2) {
-    step(s1, std::integral_constant<int, 0>{});
-    step(s0, std::integral_constant<int, 1>{});
-  }
-  if (c < C) step(s1, std::integral_constant<int, 0>{});
-
-  // D layout: lane holds weight rows 16 i + 4 (lane/16) + e of token 16 j + lane%16.
-  const int row0 = (rp * TN + rt) * kTileRows + 4 * (lane >> 4);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int tok = m0 + tq * 64 + 16 * j + (lane & 15);
-    if (tok >= a.m) continue;
-    float* yr = a.splits > 1 ? a.partial + (static_cast<int64_t>(ks) * a.m + tok) * it.n
-                             : it.y + static_cast<int64_t>(tok) * it.n;
-    const bool vec = a.splits > 1 ? (it.n & 3) == 0 : it.y_vec != 0;
+  // Group fold: total += s * part, s of rows 16 i + 4 (lane/16) + e
+  // (stage st holds the group's last chunk and its scales).
+  auto fold = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = row0 + 16 * i;
-      if (vec && row + 3 < it.n) {
-        *reinterpret_cast<f4*>(yr + row) = total[i][j];
-      } else {
+      const f4 sv = *reinterpret_cast<const f4*>(&lds_r[st * kRowsWG + rt * 64 + 16 * i + 4 * (lane >> 4)]);
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (row + e < it.n) yr[row + e] = total[i][j][e];
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Wide-wave variant: a work-group of 4 waves owns 256 tokens x 128 rows (two
-// packed tiles) and each wave 128 tokens x 64 rows, so a chunk costs a wave 32
-// MFMAs against the same per-chunk bookkeeping.  To fit 128 accumulators per
-// lane the group fold is replaced by a running rescale: the accumulator T of
-// a row is kept in units of the current group's scale s_g (T = sum over
-// earlier groups of s_g' P_g' / s_g); at a group's first chunk T is multiplied
-// by s_{g-1} / s_g, the group's integer products (q - z) x are added by the
-// MFMAs, and the output is T * s_last.  Each rescale rounds once (relative
-// error below 2^-23 per group); a scale of 0 is treated as 1 with the row's
-// dequantized values set to 0, so its products vanish exactly.  The activation
-// tile is stored without padding, its 16-byte segments permuted per token
-// (seg ^ swz(token)) so that both the stores and the fragment reads are free
-// of bank conflicts.
-
-__device__ __forceinline__ int swz(int t) { return ((t >> 1) ^ (t >> 3)) & 3; }
-
-// Prefetched data of one chunk for one thread of the wide kernel.
-struct PreW {
-  u4v av[4];    // activation pieces
-  u4v w0, w1;   // packed words of the thread's two row sub-tiles (w1: 16-bit only)
-  uint32_t z2;  // fp16 zero points of the two rows (low, high half)
-  uint32_t s0, s1;  // fp16 scales of the two rows
-};
-
-// The 4 code pairs of row sub-tile r from the 16 bytes `w` that hold it (the
-// word(s) loaded at sub_offset(b, r) of the slice, or the whole 3-bit slice).
-template <int B>
-__device__ __forceinline__ void pairs_at(const u4v w, int r, int second, uint32_t* hp) {
-  if constexpr (B == 2) {  // sub-tiles 2k and 2k+1 share word k (w.x)
-    const int sh = 8 * second;
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) hp[j] = pair_magic(w.x, sh + 2 * j, 0x00030003u);
-  } else if constexpr (B == 4) {  // word r (w.x for the first, w.y for the second)
-    const uint32_t wd = second ? w.y : w.x;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) hp[j] = pair_magic(wd, 4 * j, 0x000F000Fu);
-  } else if constexpr (B == 8) {  // words 2r, 2r+1
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      hp[j] = pair_magic(second ? ((j >> 1) ? w.w : w.z) : ((j >> 1) ? w.y : w.x), 8 * (j & 1), 0x00FF00FFu);
-  } else {
-    sub_tile_pairs<3>(w, r, hp);
-  }
-}
-
-__global__ __launch_bounds__(256) void gemm_wide_kernel(const GemmBatchArgs a) {
-  constexpr int kRows = 128;
-  __shared__ __attribute__((aligned(16))) uint16_t lds_a[2][kTokWG * kChunk];     // swizzled, no padding
-  __shared__ __attribute__((aligned(16))) uint16_t lds_b[2][2][kRows * kLdsRow];  // [stage][hi, lo]
-  __shared__ __attribute__((aligned(16))) float lds_r[2][kRows];  // rescale s_{g-1}/s_g at a group's first chunk
-  __shared__ int lds_tag[2];
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int th = wv & 1, rt = wv >> 1;  // MFMA role: token half, packed tile
-  int idx = 0;
-#pragma unroll
-  for (int i = 1; i < POLYQ_MAX_BATCH; ++i) idx += (i < a.count && static_cast<int>(blockIdx.x) >= a.wg_begin[i]) ? 1 : 0;
-  const GemmItem& it = a.item[idx];
-  const int local = static_cast<int>(blockIdx.x) - a.wg_begin[idx];
-  const int mt = local % a.m_tiles, rest = local / a.m_tiles;
-  const int ks = rest % a.splits, rp = rest / a.splits;
-  const int m0 = mt * kTokWG;
-  const int c0 = a.splits > 1 ? a.split_chunk[ks] : 0;
-  const int C = a.splits > 1 ? a.split_chunk[ks + 1] : it.n_chunks;
-  int b0 = 0;
-#pragma unroll
-  for (int j = 0; j < POLYQ_MAX_BLOCKS - 1; ++j) b0 += (j + 1 < it.nblocks && c0 >= it.ce[j]) ? 1 : 0;
-  auto cursor_at0 = [&]() { return ChunkCursor{c0, b0, it.bits[b0], c0 - it.cb[b0], it.ce[b0]}; };
-  auto advance = [&](ChunkCursor& u) {
-    ++u.c;
-    ++u.cl;
-    if (u.c == u.ce && u.c < C) {
-      ++u.bi;
-      u.bits = it.bits[u.bi];
-      u.ce = it.ce[u.bi];
-      u.cl = 0;
+        for (int e = 0; e < 4; ++e) T[i][j][e] = fmaf(sv[e], P[i][j][e], T[i][j][e]);
     }
   };
 
-  // Dequantization role: packed tile dp, row sub-tiles dr and dr + 1, lane
-  // slice `lane`; rows R0 = 16 dr + lane % 16 and R0 + 16.
-  const int dp = wv >> 1, dr = 2 * (wv & 1);
-  const int dt = rp * 2 + dp;
-  const bool dtile_ok = dt < it.n_tiles;
-  const int R0 = 16 * dr + (lane & 15);
-  const int bofs = (dp * 64 + R0) * kLdsRow + 8 * (lane >> 4);
-  constexpr int kHalfB = kRows * kLdsRow;
-
-  const __amdgpu_buffer_rsrc_t xrs =
-      make_rsrc(it.x + static_cast<int64_t>(m0) * it.k, static_cast<uint32_t>(min(a.m - m0, kTokWG)) * it.k * 2u);
-  uint32_t avoff[4];
-  int aofs_st[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int piece = tid + j * 256, t = piece >> 2, sg = piece & 3;
-    avoff[j] = (static_cast<uint32_t>(t) * it.k + sg * 8) * 2u;
-    aofs_st[j] = t * kChunk + 8 * (sg ^ swz(t));
-  }
-
-  int lc = c0, lb = 0, lcl = 0, lbits = 0, lce = 0, lrb = 0;
-  uint32_t lvoff = 0;
-  __amdgpu_buffer_rsrc_t wrs;
-  auto set_block = [&](int b) {
-    lb = b;
-    lbits = it.bits[b];
-    lce = it.ce[b];
-    lrb = static_cast<int>(it.rb[b]);
-    const int64_t tb = it.tb[b];
-    wrs = make_rsrc(it.packed + it.off[b] + static_cast<int64_t>(dtile_ok ? dt : 0) * tb,
-                    dtile_ok ? static_cast<uint32_t>(tb) : 0u);
-    lvoff = static_cast<uint32_t>(lane * 4 * lbits + sub_offset(lbits, dr));
-    lcl = 0;
-  };
-  const uint32_t zvoff = 2 * meta_z_half(R0);  // both rows' z (halves 4 (lane%16) + dr, + 1)
-  const uint32_t svoff0 = 2 * meta_s_half(R0), svoff1 = 2 * meta_s_half(R0 + 16);
-  auto load = [&](PreW& pr) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      pr.av[j] = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, avoff[j], lc * 64, 0));
-    const int rec = (lcl >> 2) * lrb;
-    const int soff = rec + (lbits <= 8 ? kMetaBytes : 0) + (lcl & 3) * 256 * lbits;
-    pr.w0 = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(wrs, lvoff, soff, 0));
-    pr.w1 = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(wrs, lvoff + 16, soff, 0));
-    if ((lcl & 3) == 0) {  // z and s are read at a group's first chunk only
-      pr.z2 = __builtin_amdgcn_raw_buffer_load_b32(wrs, zvoff, rec, 0);
-      pr.s0 = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff0, rec, 0);
-      pr.s1 = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff1, rec, 0);
-    }
-    ++lc;
-    ++lcl;
-    if (lc == lce && lc < C) set_block(lb + 1);
-  };
-
-  // Group scale of the two rows (0 read as 1), kept from the previous group,
-  // and the values a group's first chunk derives from its metadata for the
-  // group's other chunks: 1024 + z of both rows, rows whose scale is 0, and
-  // whether every zero point of the wave is an integer in [0, 255].
-  float sig_prev0 = 1.f, sig_prev1 = 1.f;
-  float gz0 = 0.f, gz1 = 0.f;
-  bool gdead0 = false, gdead1 = false, gdead = false, gexact = true;
-  auto store = [&](const ChunkCursor& ci, const PreW& pr, int st) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) *reinterpret_cast<u4v*>(&lds_a[st][aofs_st[j]]) = pr.av[j];
-    if ((ci.cl & 3) == 0) {  // first chunk of a group: its rows' scales and zero points
-      float sg0 = 1.f, sg1 = 1.f;
-      if (ci.bits <= 8) {
-        const float s0 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s0)));
-        const float s1 = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(pr.s1)));
-        gdead0 = s0 == 0.f;
-        gdead1 = s1 == 0.f;
-        sg0 = gdead0 ? 1.f : s0;
-        sg1 = gdead1 ? 1.f : s1;
-        const h2 zz = __builtin_bit_cast(h2, pr.z2);
-        const float z0 = static_cast<float>(zz.x), z1 = static_cast<float>(zz.y);
-        gz0 = z0;
-        gz1 = z1;
-        const bool ok0 = z0 == truncf(z0) && z0 >= 0.f && z0 <= 255.f;
-        const bool ok1 = z1 == truncf(z1) && z1 >= 0.f && z1 <= 255.f;
-        gexact = __all(ok0 && ok1);  // wave-uniform
-        gdead = __any(gdead0 || gdead1);
-      }
-      lds_r[st][dp * 64 + R0] = sig_prev0 / sg0;  // rescale factors (the four threads of a row store the same value)
-      lds_r[st][dp * 64 + R0 + 16] = sig_prev1 / sg1;
-      sig_prev0 = sg0;
-      sig_prev1 = sg1;
-    }
-    uint16_t* hi = &lds_b[st][0][bofs];
-    uint16_t* lo = hi + kHalfB;
-    constexpr int kRowStep = 16 * kLdsRow;  // row R0 + 16
-    float v0[8], v1[8];
-    if (ci.bits == 16) {
-      const uint32_t ww[8] = {pr.w0.x, pr.w0.y, pr.w0.z, pr.w0.w, pr.w1.x, pr.w1.y, pr.w1.z, pr.w1.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const h2 h = __builtin_bit_cast(h2, ww[i]), g = __builtin_bit_cast(h2, ww[4 + i]);
-        v0[2 * i] = static_cast<float>(h.x);
-        v0[2 * i + 1] = static_cast<float>(h.y);
-        v1[2 * i] = static_cast<float>(g.x);
-        v1[2 * i + 1] = static_cast<float>(g.y);
-      }
-      store_pair(v0, hi, lo);
-      store_pair(v1, hi + kRowStep, lo + kRowStep);
-      return;
-    }
-    uint32_t hp0[4], hp1[4];
-    switch (ci.bits) {
-      case 2: pairs_at<2>(pr.w0, dr, 0, hp0); pairs_at<2>(pr.w0, dr + 1, 1, hp1); break;
-      case 3: pairs_at<3>(pr.w0, dr, 0, hp0); pairs_at<3>(pr.w0, dr + 1, 1, hp1); break;
-      case 4: pairs_at<4>(pr.w0, dr, 0, hp0); pairs_at<4>(pr.w0, dr + 1, 1, hp1); break;
-      default: pairs_at<8>(pr.w0, dr, 0, hp0); pairs_at<8>(pr.w0, dr + 1, 1, hp1); break;
-    }
-    if (gexact) {
-      // (1024 + q) - (1024 + z) = q - z, all exact for an integer z in [0, 255]
-      // (in bf16 too)
-      const float zo0 = 1024.f + gz0, zo1 = 1024.f + gz1;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const h2 h = __builtin_bit_cast(h2, hp0[j]), g = __builtin_bit_cast(h2, hp1[j]);
-        v0[2 * j] = static_cast<float>(h.x) - zo0;
-        v0[2 * j + 1] = static_cast<float>(h.y) - zo0;
-        v1[2 * j] = static_cast<float>(g.x) - zo1;
-        v1[2 * j + 1] = static_cast<float>(g.y) - zo1;
-      }
-    } else {
-      // any other fp16 z: (1024 + q) - 1024 = q exactly, then q - z rounds once
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const h2 h = __builtin_bit_cast(h2, hp0[j]), g = __builtin_bit_cast(h2, hp1[j]);
-        v0[2 * j] = (static_cast<float>(h.x) - 1024.f) - gz0;
-        v0[2 * j + 1] = (static_cast<float>(h.y) - 1024.f) - gz0;
-        v1[2 * j] = (static_cast<float>(g.x) - 1024.f) - gz1;
-        v1[2 * j + 1] = (static_cast<float>(g.y) - 1024.f) - gz1;
-      }
-    }
-    if (gdead) {  // rows whose scale is 0 contribute nothing
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        v0[e] = gdead0 ? 0.f : v0[e];
-        v1[e] = gdead1 ? 0.f : v1[e];
-      }
-    }
-    if (gexact) {
-      // lo is left as it is: zero, unless a chunk stored as pairs used this
-      // stage last, and then the owner of each slot clears it before the
-      // stage is stored again (clear_lo), because another wave may store its
-      // rows of this chunk as pairs and the second MFMA pass reads all rows
-      store_exact(v0, hi);
-      store_exact(v1, hi + kRowStep);
-    } else {
-      store_pair(v0, hi, lo);
-      store_pair(v1, hi + kRowStep, lo + kRowStep);
-      lds_tag[st] = ci.c + 1;
-    }
-  };
-
-  f4 T[4][8];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) T[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-
-  const int bofs_m = (rt * 64 + (lane & 15)) * kLdsRow + 8 * (lane >> 4);
-  auto bfrag = [&](int st, int j) {
-    const int t = th * 128 + 16 * j + (lane & 15);
-    return *reinterpret_cast<const bf16x8*>(&lds_a[st][t * kChunk + 8 * ((lane >> 4) ^ swz(t))]);
-  };
-  ChunkCursor mc = cursor_at0(), sc = cursor_at0();
-  // The lo tile of a stage is zero except where a chunk stored as pairs wrote
-  // it; each thread clears its own two lo slots of a stage whose chunk used
-  // the second pass, before it stores into that stage again.
-  bool lo_dirty[2] = {false, false};
-  auto clear_lo = [&](int st) {
-    uint16_t* lo = &lds_b[st][1][bofs];
-    *reinterpret_cast<uint4*>(lo) = uint4{0u, 0u, 0u, 0u};
-    *reinterpret_cast<uint4*>(lo + 16 * kLdsRow) = uint4{0u, 0u, 0u, 0u};
-  };
-  // st: the LDS stage of chunk c (chunks alternate, starting with stage 0 at
-  // c0), a compile-time constant in the loop below, which runs two chunks per
-  // iteration.
-  auto step = [&](PreW& slot, auto st_tag) {
-    constexpr int st = decltype(st_tag)::value;
-    const int c = mc.c;
-    const bool two = mc.bits == 16 || lds_tag[st] == c + 1;
-    if ((mc.cl & 3) == 0 && c != c0) {  // a new group: T to the new scale's units
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const f4 r = *reinterpret_cast<const f4*>(&lds_r[st][rt * 64 + 16 * i + 4 * (lane >> 4)]);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) T[i][j][e] *= r[e];
-      }
-    }
-    bf16x8 af[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(&lds_b[st][0][bofs_m + i * 16 * kLdsRow]);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const bf16x8 b = bfrag(st, j);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) T[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], b, T[i][j], 0, 0, 0);
-    }
-    if (two) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(&lds_b[st][1][bofs_m + i * 16 * kLdsRow]);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const bf16x8 b = bfrag(st, j);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) T[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], b, T[i][j], 0, 0, 0);
-      }
-    }
-    lo_dirty[st] = two;  // this chunk's pairs sit in stage st until cleared
-    if (c + 1 < C) {
-      advance(sc);
-      if (lo_dirty[st ^ 1]) {  // read by the previous step, before this step's barrier
-        clear_lo(st ^ 1);
-        lo_dirty[st ^ 1] = false;
-      }
-      store(sc, slot, st ^ 1);
-    }
-    if (c + 2 < C) load(slot);
-    advance(mc);
-    __syncthreads();
-  };
-
-  PreW pre;
+  // A chunk sits in a register slot from its load (two chunks ahead) to its
+  // store (one chunk ahead), and in an LDS stage from its store to its
+  // multiply; both alternate chunk by chunk.  `sc` is the slot the next step
+  // stores from, `sn` the other (it holds the chunk after that); a step that
+  // ends a block leaves its slot, holding the next block's first chunk, for
+  // that block's entry.  The slots are named, not indexed, so that they stay
+  // in registers: after an odd number of steps their contents trade places.
+  Pre sc, sn;
   if (tid < 2) lds_tag[tid] = 0;
-  clear_lo(0);
-  clear_lo(1);
+  *reinterpret_cast<uint4*>(lds_b + kStageB + bst) = uint4{0u, 0u, 0u, 0u};  // lo slots of both stages
+  *reinterpret_cast<uint4*>(lds_b + 3 * kStageB + bst) = uint4{0u, 0u, 0u, 0u};
   set_block(b0);
   lcl = c0 - it.cb[b0];
-  load(pre);
-  __syncthreads();
-  store(sc, pre, 0);
-  if (C - c0 > 1) load(pre);
-  __syncthreads();
-  {
-    int c = c0;
-    for (; c + 1 < C; c += 2) {
-      step(pre, std::integral_constant<int, 0>{});
-      step(pre, std::integral_constant<int, 1>{});
-    }
-    if (c < C) step(pre, std::integral_constant<int, 0>{});
-  }
+  load(sn);
+  if (C - c0 > 1) load(sc);
+  __syncthreads();  // the tags and cleared lo slots before the first store
+  int c = c0, par = 0;  // next chunk to multiply, its stage
 
-  // Output: T in units of the last group's scale; that scale goes through LDS.
-  lds_r[0][dp * 64 + R0] = sig_prev0;
-  lds_r[0][dp * 64 + R0 + 16] = sig_prev1;
-  __syncthreads();
+  // Chunks [c, cend) of one block of bit-width B, from a group boundary.  The
+  // loop is compiled per bit-width, one group of four chunks per iteration:
+  // the unpack, the group start and the group end are fixed at compile time
+  // and the common path of a step has no branch.
+  auto run_block = [&](auto b_tag, int cend) __attribute__((always_inline)) {
+    constexpr int B = decltype(b_tag)::value;
+    // entry: the block's first chunk, still in sn, into stage par
+    store_main(b_tag, sn, c, par, true);
+    store_fix(b_tag, sn, c, par);
+    if (c + 2 < C) load(sn);
+    __syncthreads();
+    // One step: multiply chunk c (stage st); if `more` (chunk c + 1 is in the
+    // block) store chunk c + 1 (`nf`: it starts a group) from `slot` into the
+    // other stage and fetch chunk c + 3 into it (`inner`: known to be in the
+    // split); fold a group that ends with chunk c.
+    auto step = [&](Pre& slot, int st, bool first, bool last, bool nf, bool more, bool inner) __attribute__((always_inline)) {
+      const bool two = B == 16 || __builtin_expect(lds_tag[st] == c + 1, 0);
+      mfma_pass(st, first, 0);
+      if (more) store_main(b_tag, slot, c + 1, st ^ 1, nf);
+      if (two) mfma_pass(st, false, 1);
+      if (last) fold(st);
+      if (more) {
+        store_fix(b_tag, slot, c + 1, st ^ 1);
+        if (inner || c + 3 < C) load(slot);
+      }
+      ++c;
+      __syncthreads();
+    };
+    // Every group but the block's last: all four steps have their next chunk
+    // in the block and (three chunks ahead) in the split, so every step
+    // issues the same loads and each wait leaves the younger slot in flight.
+    const int nch = cend - c;
+    for (int g = (nch - 1) / 4; g > 0; --g) {
+      step(sc, par, true, false, false, true, true);
+      step(sn, par ^ 1, false, false, false, true, true);
+      step(sc, par, false, false, false, true, true);
+      step(sn, par ^ 1, false, true, true, true, true);
+    }
+    // The block's last group: 1 .. 4 chunks.
+    const int r = cend - c;
+    step(sc, par, true, r == 1, false, r > 1, false);
+    if (r >= 2) step(sn, par ^ 1, false, r == 2, false, r > 2, false);
+    if (r >= 3) step(sc, par, false, r == 3, false, r > 3, false);
+    if (r >= 4) step(sn, par ^ 1, false, true, false, false, false);
+    if (r & 1) {
+      const Pre t = sc;
+      sc = sn;
+      sn = t;
+      par ^= 1;
+    }
+  };
+  // Blocks have strictly ascending bit-widths, so the work-group's blocks are
+  // visited by one pass over the palette: straight-line code, no loop whose
+  // registers every bit-width's copy would have to share.
+  int bi = b0;
+  auto visit = [&](auto b_tag) __attribute__((always_inline)) {
+    constexpr int B = decltype(b_tag)::value;
+    if (c < C && it.bits[bi] == B) {
+      run_block(b_tag, min(it.ce[bi], C));
+      ++bi;
+    }
+  };
+  visit(Int<2>{});
+  visit(Int<3>{});
+  visit(Int<4>{});
+  visit(Int<8>{});
+  visit(Int<16>{});
+
+  // D layout: lane holds weight rows 16 i + 4 (lane/16) + e of token 16 j + lane%16.
   const int row0 = (rp * 2 + rt) * kTileRows + 4 * (lane >> 4);
   float* ybase = a.splits > 1 ? a.partial + static_cast<int64_t>(ks) * a.m * it.n : it.y;
   const bool vec = a.splits > 1 ? (it.n & 3) == 0 : it.y_vec != 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const f4 sl = *reinterpret_cast<const f4*>(&lds_r[0][rt * 64 + 16 * i + 4 * (lane >> 4)]);
-    const int row = row0 + 16 * i;
+  for (int j = 0; j < 4; ++j) {
+    const int tok = m0 + tq * 64 + 16 * j + (lane & 15);
+    if (tok >= a.m) continue;
+    float* yr = ybase + static_cast<int64_t>(tok) * it.n;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int tok = m0 + th * 128 + 16 * j + (lane & 15);
-      if (tok >= a.m) continue;
-      float* yr = ybase + static_cast<int64_t>(tok) * it.n;
-      const f4 v = T[i][j] * sl;
+    for (int i = 0; i < 4; ++i) {
+      const int row = row0 + 16 * i;
       if (vec && row + 3 < it.n) {
-        *reinterpret_cast<f4*>(yr + row) = v;
+        *reinterpret_cast<f4*>(yr + row) = T[i][j];
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (row + e < it.n) yr[row + e] = v[e];
+          if (row + e < it.n) yr[row + e] = T[i][j][e];
       }
     }
   }
@@ -827,21 +589,20 @@ size_t permuted_bytes(const polyq_layout& L, int32_t m) {
   return static_cast<size_t>(align_up(static_cast<int64_t>(m) * L.k * 2, 256));
 }
 
-// Work-groups of one linear with TN packed tiles per work-group.
-int64_t tile_groups(const polyq_layout& L, int32_t m, int tn) {
-  return static_cast<int64_t>((L.n_tiles + tn - 1) / tn) * ((m + kTokWG - 1) / kTokWG);
+// Work-groups of one linear (two packed tiles each) per K split.
+int64_t tile_groups(const polyq_layout& L, int32_t m) {
+  return static_cast<int64_t>((L.n_tiles + 1) / 2) * ((m + kTokWG - 1) / kTokWG);
 }
 
-// K splits of a single-linear launch whose one-tile work-groups would leave
-// CUs idle: enough wide-wave work-groups for two per CU (about 480), at least
-// four groups per split, at most kMaxSplits.
+// K splits of a single-linear launch whose work-groups would leave CUs idle:
+// as many as keep the launch within one round of one work-group per CU (256),
+// at least four groups per split, at most kMaxSplits.
 int plan_splits(const polyq_layout& L, int32_t m, int32_t count) {
-  if (count != 1 || tile_groups(L, m, 1) >= 240) return 1;
-  const int64_t wg = tile_groups(L, m, 2);  // split launches run the wide-wave kernel
+  const int64_t wg = tile_groups(L, m);
+  if (count != 1 || wg >= 200) return 1;
   int groups = 0;
   for (int i = 0; i < L.nblocks; ++i) groups += (L.block[i].len / kChunk + kChunksPerGroup - 1) / kChunksPerGroup;
-  const int64_t want = (480 + wg - 1) / wg;
-  return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({want, kMaxSplits, groups / 4})));
+  return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({256 / wg, kMaxSplits, groups / 4})));
 }
 
 // Workspace of a batch: one permuted copy per distinct (x, perm) pair with
@@ -910,7 +671,6 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
   a.m = m;
   a.splits = splits;
   a.m_tiles = (m + kTokWG - 1) / kTokWG;
-  int64_t tiles1 = 0;
   for (int i = 0; i < count; ++i) {
     const polyq_gemv_item& itm = items[i];
     const polyq_layout& L = *itm.layout;
@@ -920,22 +680,12 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
     if (L.packed_bytes > 0x7FFFFFFFll) return POLYQ_ERR_CAPACITY;
     if (itm.perm == nullptr && reinterpret_cast<uintptr_t>(itm.x) % 16 != 0)
       return POLYQ_ERR_ARG;  // clustered activations are read as 16-byte vectors
-    tiles1 += L.n_tiles;
   }
-  // Every check above and here comes before the first launch.  Work-group
-  // shape by launch size: 4-wave work-groups of 256 tokens x 128
-  // rows with 128 x 64 wave tiles (gemm_wide_kernel) when there are enough of
-  // them for two per CU, or K is split; else 8-wave work-groups of the same tile
-  // (gemm_kernel<2>) when those fill most CUs; else one packed tile per
-  // 4-wave work-group (gemm_kernel<1>, two co-resident per CU).
-  const int64_t wg2 = (tiles1 + count) / 2 * a.m_tiles;
-  const int kind = splits > 1 || wg2 >= 400 ? 3 : wg2 >= 200 ? 2 : 1;
-  const bool wide = kind >= 2;
-  const int tn = wide ? 2 : 1;
+  // Every check above and here comes before the first launch.
   int64_t wg = 0;
   for (int i = 0; i < count; ++i) {
     a.wg_begin[i] = static_cast<int32_t>(wg);
-    wg += static_cast<int64_t>((items[i].layout->n_tiles + tn - 1) / tn) * a.m_tiles * splits;
+    wg += tile_groups(*items[i].layout, m) * splits;
     if (wg > 0x7FFFFFFF) return POLYQ_ERR_CAPACITY;
   }
   for (int i = count; i <= POLYQ_MAX_BATCH; ++i) a.wg_begin[i] = static_cast<int32_t>(wg);
@@ -985,12 +735,7 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
                                       : (sp >= splits ? L.n_chunks : gstart[static_cast<int64_t>(G) * sp / splits]);
     a.partial = splits > 1 ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + partial_off) : nullptr;
   }
-  if (kind == 3)
-    hipLaunchKernelGGL(gemm_wide_kernel, dim3(static_cast<unsigned>(wg)), dim3(256), 0, st, a);
-  else if (kind == 2)
-    hipLaunchKernelGGL(gemm_kernel<2>, dim3(static_cast<unsigned>(wg)), dim3(512), 0, st, a);
-  else
-    hipLaunchKernelGGL(gemm_kernel<1>, dim3(static_cast<unsigned>(wg)), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(gemm_kernel, dim3(static_cast<unsigned>(wg)), dim3(kThreads), 0, st, a);
   if (splits > 1) {
     const int64_t n_el = static_cast<int64_t>(m) * items[0].layout->n;
     hipLaunchKernelGGL(sum_splits_kernel, dim3(static_cast<unsigned>((n_el + 1023) / 1024)), dim3(256), 0, st,
