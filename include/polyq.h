@@ -319,6 +319,81 @@ polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t count, int32
 polyq_status polyq_read_probe(const void* buf, int64_t bytes, int32_t work_groups, uint32_t* sink,
                               void* stream);
 
+/*
+ * ---- Compile-time bit allocation (Sec. 3.1-3.3) --------------------------
+ * Host functions on host memory: synchronous, no device work, no global
+ * state (thread-safe).  Arrays indexed by bit-width use the palette order
+ * {2, 3, 4, 8, 16} (index 0 .. 4).  Channels are input channels in their
+ * original order.  Every error is detected before any output is written.
+ */
+#define POLYQ_NUM_BITS 5
+
+/*
+ * polyq_channel_error -- the activation-aware error proxy of Eq. 2 for every
+ * input channel and bit-width, E_b[j] = ||w~_j - w_j||^2 * E[x_j^2], with the
+ * scaled-and-quantized weight of Eq. 1, W~ = diag(s)^-1 Q_b(diag(s) W).
+ *   w:     fp32 [n][k] row-major (output rows x input channels);
+ *   x2:    fp64 [k], E[x_j^2] (finite, >= 0);
+ *   scale: fp32 [k] per-channel scales s_j (finite, > 0), or NULL for all 1;
+ *   err:   fp64 [POLYQ_NUM_BITS][k] out.
+ * Q_b is this library's asymmetric min-max quantizer applied per output row
+ * to groups of 128 consecutive input channels (the last group partial):
+ * s16 = fp16_rne((max - min) / (2^b - 1)), z = clamp(rint(-min / s16), 0,
+ * 2^b - 1), q = clamp(rint(w / s16) + z, 0, 2^b - 1), value s16 (q - z), all in
+ * fp64 with rint rounding half to even; a group whose s16 is 0 quantizes to 0.
+ * E_16 = 0 (16-bit channels are unquantized).
+ * Errors: POLYQ_ERR_ARG (null pointer, n or k < 1, an x2 or scale value out of
+ * range); POLYQ_ERR_SHAPE (n * k above 2^31).
+ */
+polyq_status polyq_channel_error(const float* w, int32_t n, int32_t k, const double* x2,
+                                 const float* scale, double* err);
+
+/*
+ * polyq_waterfill -- per-layer greedy waterfilling under the fractional
+ * budget B (Sec. 3.2, Eq. 3-5).  Every channel starts at 2 bits; the budget
+ * left is round(B k) - 2 k (round half to even; nothing happens when it is
+ * <= 0).  Each channel's next upgrade b -> b' (the next palette value) waits
+ * in a max-heap keyed by the gain (E_b[j] - E_b'[j]) / (b' - b), ties to the
+ * lower channel index; the top upgrade is applied if it fits the budget left
+ * (else dropped: the budget only shrinks) and the channel's next upgrade is
+ * pushed, until the budget is spent or the heap is empty.
+ *   err: fp64 [POLYQ_NUM_BITS][k] (polyq_channel_error's layout); bits: [k] out.
+ * Errors: POLYQ_ERR_ARG (null pointer, k < 1, B not finite or above 16).
+ */
+polyq_status polyq_waterfill(const double* err, int32_t k, double budget, int32_t* bits);
+
+/*
+ * polyq_quanta_match -- ISA-aware quanta matching (Sec. 3.3, Eq. 6-7): the
+ * per-bit channel counts of `bits` are rounded to multiples of `quantum`
+ * (floors in units of the quantum, the units left to the largest remainders,
+ * ties to the higher bit-width); whole-quantum moves between neighbouring
+ * levels then bring sum_b b c_b closer to round(B k) while one is strictly
+ * better (largest improvement first, ties to the lower pair, promotion
+ * first); finally single channels move between neighbouring levels until the
+ * counts match: across the lowest boundary whose flow is nonzero and whose
+ * source level is not empty, the channel with the largest gain is promoted
+ * (or the smallest loss demoted), ties to the lower channel index.
+ *   bits: [k] in (palette values) and out; counts: [POLYQ_NUM_BITS] out, or
+ *   NULL; B_real = sum_b bits b counts[b] / k (Eq. 7).
+ * Errors: POLYQ_ERR_ARG (null pointer, k < 1, quantum < 1, B not finite, a
+ * bit-width outside the palette); POLYQ_ERR_QUANTUM (k not a multiple of
+ * quantum).
+ */
+polyq_status polyq_quanta_match(const double* err, int32_t k, int32_t quantum, double budget,
+                                int32_t* bits, int32_t* counts);
+
+/*
+ * polyq_cluster -- channel clustering (Sec. 4.1, Eq. 9): blocks in ascending
+ * bit-width, ascending original index inside a block.
+ *   bits: [k] palette values; perm: [k] out, perm[k'] = original channel at
+ *   clustered position k'; blocks: [POLYQ_MAX_BLOCKS] out (bits, len) and
+ *   *nblocks: the number of nonempty blocks.  The block list is what
+ *   polyq_plan takes once every length is a multiple of POLYQ_QUANTUM.
+ * Errors: POLYQ_ERR_ARG (null pointer, k < 1, a bit-width outside the palette).
+ */
+polyq_status polyq_cluster(const int32_t* bits, int32_t k, int32_t* perm, polyq_block* blocks,
+                           int32_t* nblocks);
+
 /* Static description of a status code (never NULL). */
 const char* polyq_status_str(polyq_status status);
 

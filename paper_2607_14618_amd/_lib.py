@@ -32,7 +32,8 @@ EXPORTS = ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq
            "polyq_gemv", "polyq_gemv_batch_workspace_bytes", "polyq_gemv_batch_workspace_zero_bytes",
            "polyq_gemv_batch",
            "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_gemm_batch_workspace_bytes",
-           "polyq_gemm_batch", "polyq_read_probe", "polyq_gemv_batch_noalloc", "polyq_status_str")
+           "polyq_gemm_batch", "polyq_read_probe", "polyq_gemv_batch_noalloc", "polyq_channel_error",
+           "polyq_waterfill", "polyq_quanta_match", "polyq_cluster", "polyq_status_str")
 
 
 class Block(ctypes.Structure):
@@ -113,11 +114,16 @@ def lib() -> ctypes.CDLL:
             L.polyq_gemm_batch.argtypes = [ip, i32, i32, vp, sz, vp]
             L.polyq_read_probe.argtypes = [vp, ctypes.c_int64, i32, vp, vp]
             L.polyq_gemv_batch_noalloc.argtypes = [ip, i32, i32, vp]
+            L.polyq_channel_error.argtypes = [vp, i32, i32, vp, vp, vp]
+            L.polyq_waterfill.argtypes = [vp, i32, ctypes.c_double, vp]
+            L.polyq_quanta_match.argtypes = [vp, i32, i32, ctypes.c_double, vp, vp]
+            L.polyq_cluster.argtypes = [vp, i32, vp, ctypes.POINTER(Block), ctypes.POINTER(i32)]
             L.polyq_status_str.argtypes = [ctypes.c_int]
             L.polyq_status_str.restype = ctypes.c_char_p
             for name in ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq_permute",
                          "polyq_gemv", "polyq_gemv_batch", "polyq_gemm", "polyq_gemm_batch",
-                         "polyq_read_probe", "polyq_gemv_batch_noalloc"):
+                         "polyq_read_probe", "polyq_gemv_batch_noalloc", "polyq_channel_error",
+                         "polyq_waterfill", "polyq_quanta_match", "polyq_cluster"):
                 getattr(L, name).restype = ctypes.c_int
             _lib = L
     return _lib
@@ -503,3 +509,66 @@ def gemv_batch_noalloc(items):
         ys.append(y)
     _check(lib().polyq_gemv_batch_noalloc(arr, len(items), m, _stream(dev)), "polyq_gemv_batch_noalloc")
     return ys
+
+
+# ---------------------------------------------------------------- bit allocation (host)
+BITS = (2, 3, 4, 8, 16)
+
+
+def _host(a, dtype):
+    import numpy as np
+    a = np.ascontiguousarray(a.detach().cpu().numpy() if isinstance(a, torch.Tensor) else a, dtype=dtype)
+    return a, a.ctypes.data
+
+
+def channel_error(w, x2, scale=None):
+    """Eq. 2 error proxy (polyq_channel_error): w fp32 [n][k], x2 = E[x^2] [k],
+    optional per-channel scales [k]; returns fp64 [5][k] (bits 2, 3, 4, 8, 16)."""
+    import numpy as np
+    wa, wp = _host(w, np.float32)
+    n, k = wa.shape
+    xa, xp = _host(x2, np.float64)
+    sa, sp = (None, None) if scale is None else _host(scale, np.float32)
+    err = np.empty((len(BITS), k), dtype=np.float64)
+    _check(lib().polyq_channel_error(wp, n, k, xp, sp, err.ctypes.data), "polyq_channel_error")
+    return err
+
+
+def waterfill(err, budget: float):
+    """Eq. 3-5 (polyq_waterfill): bits per channel."""
+    import numpy as np
+    ea, ep = _host(err, np.float64)
+    k = ea.shape[1]
+    bits = np.empty(k, dtype=np.int32)
+    _check(lib().polyq_waterfill(ep, k, float(budget), bits.ctypes.data), "polyq_waterfill")
+    return bits
+
+
+def quanta_match(err, bits, quantum: int, budget: float):
+    """Eq. 6 (polyq_quanta_match): snapped bits per channel and the per-bit counts."""
+    import numpy as np
+    ea, ep = _host(err, np.float64)
+    out = np.array(bits, dtype=np.int32, copy=True)
+    counts = np.empty(len(BITS), dtype=np.int32)
+    _check(lib().polyq_quanta_match(ep, out.size, int(quantum), float(budget), out.ctypes.data,
+                                    counts.ctypes.data), "polyq_quanta_match")
+    return out, {b: int(c) for b, c in zip(BITS, counts)}
+
+
+def cluster(bits):
+    """Sec. 4.1 (polyq_cluster): perm (clustered position -> original channel) and blocks."""
+    import numpy as np
+    ba, bp = _host(bits, np.int32)
+    perm = np.empty(ba.size, dtype=np.int32)
+    blocks = (Block * MAX_BLOCKS)()
+    nb = ctypes.c_int32(0)
+    _check(lib().polyq_cluster(bp, ba.size, perm.ctypes.data, blocks, ctypes.byref(nb)), "polyq_cluster")
+    return perm, [(blocks[i].bits, blocks[i].len) for i in range(nb.value)]
+
+
+def allocate(w, x2, budget: float, quantum: int = QUANTUM, scale=None):
+    """Sec. 3.1-3.3 end to end on the host: (bits, perm, blocks, counts)."""
+    err = channel_error(w, x2, scale)
+    bits, counts = quanta_match(err, waterfill(err, budget), quantum, budget)
+    perm, blocks = cluster(bits)
+    return bits, perm, blocks, counts

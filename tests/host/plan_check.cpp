@@ -1,10 +1,14 @@
-// Host-only property check of the planner (plan.cpp): packed layouts of
-// random valid block lists, the statuses of invalid ones, and the decode-GEMV
-// work split (every chunk of a layer covered by exactly one wave, each wave
-// inside one block and starting on one of its group boundaries, LDS within the
-// work-group budget).  Built with g++ and the address and undefined-behaviour
-// sanitizers by tests/test_host_sanitizer.py; exits non-zero on the first
-// violated property.
+// Host-only property check of the planner (plan.cpp) and the bit allocation
+// (alloc.cpp): packed layouts of random valid block lists, the statuses of
+// invalid ones, the decode-GEMV work split (every chunk of a layer covered by
+// exactly one wave, each wave inside one block and starting on one of its
+// group boundaries, LDS within the work-group budget), and the allocation's
+// outputs (palette bit-widths, the budget never exceeded by waterfilling,
+// counts on the quantum after matching, a permutation from clustering).
+// Built with g++ and the address and undefined-behaviour sanitizers by
+// tests/test_host_sanitizer.py; exits non-zero on the first violated
+// property.
+#include <math.h>
 #include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
@@ -141,6 +145,45 @@ void check_invalid() {
         "m out of range");
 }
 
+void check_alloc(Rng& r, int iter) {
+  const int n = r.uniform(1, 40), k = 32 * r.uniform(1, 40);
+  std::vector<float> w(static_cast<size_t>(n) * k), s(k);
+  std::vector<double> x2(k), err(static_cast<size_t>(POLYQ_NUM_BITS) * k);
+  for (auto& v : w) v = static_cast<float>((static_cast<int64_t>(r.next() % 2001) - 1000) * 2e-5);
+  for (int j = 0; j < k; ++j) {
+    x2[j] = 1.0 + static_cast<double>(r.next() % 1000);
+    s[j] = 0.5f + static_cast<float>(r.next() % 100) / 50.0f;
+  }
+  CHECK(polyq_channel_error(w.data(), n, k, x2.data(), iter % 2 ? s.data() : nullptr, err.data()) == POLYQ_OK,
+        "channel_error");
+  for (int j = 0; j < k; ++j) CHECK(err[4 * static_cast<size_t>(k) + j] == 0.0 && err[j] >= 0.0, "E_16 = 0, E >= 0");
+  const double budget = 2.0 + static_cast<double>(r.next() % 1400) / 100.0;
+  std::vector<int32_t> bits(k), perm(k);
+  CHECK(polyq_waterfill(err.data(), k, budget, bits.data()) == POLYQ_OK, "waterfill");
+  int64_t sum = 0;
+  for (int j = 0; j < k; ++j) sum += bits[j];
+  CHECK(sum <= static_cast<int64_t>(nearbyint(budget * k)) || sum == 2 * k, "budget exceeded: %lld", (long long)sum);
+  int32_t counts[POLYQ_NUM_BITS];
+  CHECK(polyq_quanta_match(err.data(), k, 32, budget, bits.data(), counts) == POLYQ_OK, "quanta_match");
+  int32_t total = 0;
+  for (int i = 0; i < POLYQ_NUM_BITS; ++i) {
+    CHECK(counts[i] % 32 == 0, "count %d off the quantum", counts[i]);
+    total += counts[i];
+  }
+  CHECK(total == k, "counts sum to %d, k %d", total, k);
+  polyq_block blocks[POLYQ_MAX_BLOCKS];
+  int32_t nb = 0;
+  CHECK(polyq_cluster(bits.data(), k, perm.data(), blocks, &nb) == POLYQ_OK, "cluster");
+  std::vector<int> seen(k, 0);
+  for (int j = 0; j < k; ++j) ++seen[perm[j]];
+  for (int j = 0; j < k; ++j) CHECK(seen[j] == 1, "perm is not a permutation");
+  polyq_layout L;
+  CHECK(polyq_plan(n, k, blocks, nb, &L) == POLYQ_OK, "clustered blocks plan");
+  CHECK(polyq_waterfill(err.data(), k, NAN, bits.data()) == POLYQ_ERR_ARG, "NaN budget refused");
+  CHECK(polyq_quanta_match(err.data(), k, 7, budget, bits.data(), counts) ==
+            (k % 7 ? POLYQ_ERR_QUANTUM : POLYQ_OK), "quantum check");
+}
+
 }  // namespace
 
 int main(int argc, char** argv) {
@@ -170,6 +213,7 @@ int main(int argc, char** argv) {
       check_gemv_plan(L, ms[j], L.n_tiles * r.uniform(1, 40));
     }
   }
+  for (int it = 0; it < iters / 10 + 1 && !g_fail; ++it) check_alloc(r, it);
   if (g_fail) return 1;
   printf("plan_check ok: seed %llu, %d layouts\n", static_cast<unsigned long long>(seed), iters);
   return 0;

@@ -1,8 +1,9 @@
-"""The host planner (plan.cpp) built with g++ under AddressSanitizer and
-UndefinedBehaviorSanitizer, driven by tests/host/plan_check.cpp: random valid
-block lists up to the largest k, the statuses of invalid ones, and the decode
-work split's coverage and alignment properties.  Host code only: no HIP
-compiler and no GPU are involved."""
+"""The host planner (plan.cpp) and bit allocation (alloc.cpp) built with g++
+under AddressSanitizer and UndefinedBehaviorSanitizer, driven by
+tests/host/plan_check.cpp: random valid block lists up to the largest k, the
+statuses of invalid ones, the decode work split's coverage and alignment
+properties, and the allocation's outputs on random layers.  Host code only: no
+HIP compiler and no GPU are involved."""
 import os
 import shutil
 import subprocess
@@ -24,7 +25,8 @@ def plan_check(tmp_path_factory):
     cmd = [gxx, "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer",
            "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
            "-D__HIP_PLATFORM_AMD__", f"-I{ROCM_INCLUDE}", f"-I{ROOT / 'include'}", f"-I{CSRC}",
-           str(CSRC / "plan.cpp"), str(ROOT / "tests" / "host" / "plan_check.cpp"), "-o", str(exe)]
+           str(CSRC / "plan.cpp"), str(CSRC / "alloc.cpp"), str(ROOT / "tests" / "host" / "plan_check.cpp"),
+           "-o", str(exe)]
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     return exe
 
