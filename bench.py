@@ -22,6 +22,8 @@ eager launches are reported beside it.
                   durations and a streaming-read probe of the same byte count
                   (the highest read rate a launch of that size reaches here);
   small_batch     the same step at M = 4 and 16;
+  scaled_activations  the same step (M = 1 and 4) and prefill with Eq. 8's
+                  per-channel factors 1/s applied to x' in the kernels;
   qwen3_32b       the 64-layer Qwen3-32B-shaped stack, variants G (gather) and
                   P (pre-permuted), one graph of 256 launches per variant;
   prefill         the prefill GEMM at M = 512 (4.0-bit mix, bf16);
@@ -57,10 +59,11 @@ def _args():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--variant", choices=["G", "P", "S", "M"], default="G",
+    p.add_argument("--variant", choices=["G", "P", "S", "M", "X"], default="G",
                    help="G: permutation gathered in-kernel; P: activations pre-permuted; "
                         "S: explicit polyq_permute inside every step, then clustered x; "
-                        "M: G with gate/up emitting in down's basis (Eq. 10), down on clustered x")
+                        "M: G with gate/up emitting in down's basis (Eq. 10), down on clustered x; "
+                        "X: G with per-channel factors 1/s (Eq. 8) applied to x'")
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--no-prefill", action="store_true", help="skip the prefill GEMM figure")
@@ -227,6 +230,15 @@ def schedule(layer, grouped):
     return out
 
 
+def channel_factors(torch, k, seed):
+    """Seeded per-channel factors 2^e, e uniform in {-2, ..., 1}: the form Eq. 8's
+    power-of-two scales give the kernels (the timing does not depend on which
+    channel gets which factor, so the weights are not re-quantized for them)."""
+    g = torch.Generator().manual_seed(7001 + seed)
+    e = torch.randint(-2, 2, (k,), generator=g)
+    return torch.exp2(e.to(torch.float32)).to(torch.float16).to("cuda:0")
+
+
 def decode_launches(torch, pq, copies, variant, grouped=True):
     """Prepared launches of every rotation copy.  Variants: G gathers x' in the
     GEMV; P reads x' permuted beforehand (outside the timed step); S permutes
@@ -234,19 +246,21 @@ def decode_launches(torch, pq, copies, variant, grouped=True):
     preallocated buffer, then the GEMV on clustered x'); M is G with the
     gate/up -> down edge merged (Eq. 10): gate and up emit in down's basis, so
     down reads clustered x' (prepared outside the timed step, as the elementwise
-    SiLU(gate) * up would hand it over).  All copies share one workspace per
+    SiLU(gate) * up would hand it over); X is G with per-channel factors 1/s
+    (Eq. 8) applied to x' in the kernel.  All copies share one workspace per
     launch position (calls on one stream are ordered)."""
     dev = torch.device("cuda", 0)
     ys = [torch.empty((x.shape[0], pl.n), dtype=torch.float32, device=dev) for _, pl, x in copies[0]]
     pres = [variant in ("P", "S") or (variant == "M" and nm == "down_proj") for nm, _, _ in copies[0]]
+    xsc = [channel_factors(torch, pl.k, j) if variant == "X" else None for j, (_, pl, _) in enumerate(copies[0])]
     xs = [pl.permute(x) if p else x for (_, pl, x), p in zip(copies[0], pres)]
     torch.cuda.synchronize()
     sched = schedule(copies[0], grouped)
     workspaces = [None] * len(sched)
 
     def launch(copy, pos, idx):
-        items = [(copy[j][1].layout, copy[j][1].packed, None if pres[j] else copy[j][1].perm, xs[j], ys[j])
-                 for j in idx]
+        items = [(copy[j][1].layout, copy[j][1].packed, None if pres[j] else copy[j][1].perm, xs[j], ys[j],
+                  xsc[j]) for j in idx]
         prep = pq.PreparedBatch("gemv", items, workspace=workspaces[pos])
         if workspaces[pos] is None:
             workspaces[pos] = prep.workspace
@@ -330,18 +344,20 @@ def probe_figure(torch, pq, sizes, steps):
     return out
 
 
-def prefill_figure(torch, pq, synth, steps, warmup, m=512, grouped=True):
+def prefill_figure(torch, pq, synth, steps, warmup, m=512, grouped=True, scaled=False):
     """Config: Llama2-13B layer, 4.0-bit prefill mix, bf16 activations, M=512,
     permutation applied by the library (gather kernel + GEMM); one launch per
     group of linears that share an input (one permuted copy per group).  Timed
-    as one graph of `steps` steps (and eagerly)."""
+    as one graph of `steps` steps (and eagerly).  scaled: every linear carries
+    Eq. 8's factors 1/s, applied while the library permutes x."""
     dev = torch.device("cuda", 0)
     layer = build_layer(torch, pq, synth, 3, m=m, x_dtype=torch.bfloat16)
     flops = sum(2.0 * m * pl.n * pl.k for _, pl, _ in layer)
     ys = [torch.empty((m, pl.n), dtype=torch.float32, device=dev) for _, pl, _ in layer]
     sched = schedule(layer, grouped)
+    xsc = [channel_factors(torch, pl.k, j) if scaled else None for j, (_, pl, _) in enumerate(layer)]
     preps = [pq.PreparedBatch("gemm", [(layer[j][1].layout, layer[j][1].packed, layer[j][1].perm,
-                                        layer[j][2], ys[j]) for j in idx]) for idx in sched]
+                                        layer[j][2], ys[j], xsc[j]) for j in idx]) for idx in sched]
     calls = [p.run for p in preps]
     ms, reps = graph_region(torch, steps, warmup, lambda i: calls, replays=3)
     ms_eager = eager_region(torch, steps, 1, lambda i: calls)
@@ -532,6 +548,20 @@ def main_default(a, torch, pq, synth):
                            "ratio_vs_m1": round(r["ms_step"] / d["ms_step"], 3)}
             _log(f"decode M={m}: {sb[f'm{m}']}")
         extra["small_batch"] = sb
+    if a.variant == "G" and not a.no_small_batch:
+        sc = {"note": "the same steps with per-channel power-of-two factors 1/s (Eq. 8) applied to "
+                      "the clustered activations inside the library"}
+        for m in (1, 4):
+            r = decode_figure(torch, pq, synth, a.steps, a.warmup, "X", m=m, eager=False)
+            base = d["ms_step"] if m == 1 else sb["m4"]["us_per_step"] * 1e-3
+            sc[f"decode_m{m}"] = {"us_per_step": round(r["ms_step"] * 1e3, 2), "gbs": round(r["gbs"], 1),
+                                  "ratio_vs_unscaled": round(r["ms_step"] / base, 3)}
+            _log(f"decode M={m} with factors: {sc[f'decode_m{m}']}")
+        if not a.no_prefill:
+            p = prefill_figure(torch, pq, synth, 10, 3, grouped=not a.per_linear, scaled=True)
+            sc["prefill_m512"] = {"ms_per_step": p["ms_per_step"], "tflops": p["tflops"]}
+            _log(f"prefill with factors: {sc['prefill_m512']}")
+        extra["scaled_activations"] = sc
     if a.variant == "G":
         mg = decode_figure(torch, pq, synth, a.steps, a.warmup, "M", grouped=not a.per_linear, eager=False)
         _log(f"decode, gate/up -> down merged (Eq. 10): {mg['ms_step'] * 1e3:.2f} us/step")
@@ -550,8 +580,11 @@ def main_default(a, torch, pq, synth):
     if not a.no_cpu:
         _log("timing the CPU oracle")
         extra["cpu_baseline"] = cpu_baseline(synth, a.cpu_seconds)
-    wl = DECODE_WORKLOAD + ("channel permutation gathered in-kernel" if a.variant == "G"
-                            else "activations pre-permuted")
+    wl = DECODE_WORKLOAD + {"G": "channel permutation gathered in-kernel",
+                            "X": "channel permutation gathered in-kernel, per-channel factors 1/s (Eq. 8)",
+                            "M": "gate/up emitting in down's basis (Eq. 10)",
+                            "S": "explicit permutation kernel in the step"}.get(a.variant,
+                                                                              "activations pre-permuted")
     line(d["gbs"], "GB/s", a.steps, a.warmup, d["ms_step"], "f16",
          {"workload": wl, "m": 1, "avg_bits": 3.0, "variant": a.variant, "linears": 7,
           "launches": ("one per linear" if a.per_linear else

@@ -220,10 +220,10 @@ polyq_status polyq_gemv(const polyq_layout* layout, const void* packed, const in
  *     [0, Z)  Z = polyq_gemv_batch_workspace_zero_bytes(items, count, m): the
  *             split-K counters and partial sums.  Must be zero on entry; every
  *             completed call leaves them zero.
- *     [Z, ..) scratch: one clustered copy x' = x[:, perm] per distinct (x,
- *             perm) of the items with a permutation and several tokens (or a
- *             row too long for LDS); overwritten by the call (Eq. 9's explicit
- *             shuffle, made once per launch).
+ *     [Z, ..) scratch: one clustered copy x' = x[:, perm] (times xscale)
+ *             per distinct (x, perm, xscale) of the items with several tokens
+ *             and a permutation or a scale; overwritten by the call (Eq. 9's
+ *             explicit shuffle, made once per launch).
  *   A workspace reused for requests of different shapes must therefore be
  *   zeroed again up to the new request's Z wherever an earlier call left
  *   scratch there.
@@ -234,6 +234,15 @@ typedef struct {
   const int32_t* perm; /* may be NULL (x already clustered) */
   const uint16_t* x;   /* fp16 [m][k] */
   float* y;            /* fp32 [m][n] */
+  /* Bit-specific activation-aware scaling (Sec. 3.4, Eq. 8): fp16 [k] per
+   * clustered channel, the factor 1/s_j folded into the activations,
+   * x'[m][k'] = x[m][perm[k']] * xscale[k'], for weights packed from
+   * Q_b(diag(s) W); NULL (the default of a zero-initialized item) for none.
+   * The product is formed in fp32 and rounded to the activation type, so a
+   * power of two (what polyq_bit_scaling produces) is applied exactly.  For
+   * several tokens, and in the prefill GEMM, the scaled x' is written to the
+   * workspace's scratch part first (also without a permutation). */
+  const uint16_t* xscale;
 } polyq_gemv_item;
 
 size_t polyq_gemv_batch_workspace_bytes(const polyq_gemv_item* items, int32_t count, int32_t m);
@@ -393,6 +402,29 @@ polyq_status polyq_quanta_match(const double* err, int32_t k, int32_t quantum, d
  */
 polyq_status polyq_cluster(const int32_t* bits, int32_t k, int32_t* perm, polyq_block* blocks,
                            int32_t* nblocks);
+
+/*
+ * polyq_bit_scaling -- bit-specific activation-aware scaling (Sec. 3.4,
+ * Eq. 8), run after the bit map is fixed: for every bit-width b <= 8 present,
+ * one exponent alpha_b from `grid` (values in [0, 1]) for all its channels,
+ * s_j = 2^rint(alpha_b log2 m_j) (Eq. 8's power law kept to powers of two,
+ * so that the runtime fold of 1/s_j into x' is exact), chosen to minimize the
+ * block's proxy error sum_j E_b[j] (Eq. 2, x2 weights) with W~ =
+ * diag(s)^-1 Q_b(diag(s) W) and Q_b applied as deployed: to the block's
+ * channels in ascending index order, groups of 128 per row.  Ties keep the
+ * earlier grid point; 16-bit channels get s = 1.
+ *   w: fp32 [n][k]; x2: fp64 [k] >= 0; saliency: fp64 [k] m_j > 0 (e.g. mean
+ *   |x_j| normalized by its mean); bits: [k] palette values; grid: [ngrid];
+ *   scale: fp32 [k] out (powers of two); alpha: [POLYQ_NUM_BITS] out or NULL
+ *   (0 for absent bit-widths and for 16 bits).
+ * The weights to pack are then Q_b(diag(s) W), and the channel factors passed
+ * with them (polyq_gemv_item.xscale) are 1/s in clustered order.
+ * Errors: POLYQ_ERR_ARG (null pointer, n, k or ngrid < 1, a value out of
+ * range); POLYQ_ERR_SHAPE (n * k above 2^31).
+ */
+polyq_status polyq_bit_scaling(const float* w, int32_t n, int32_t k, const double* x2,
+                               const double* saliency, const int32_t* bits, const float* grid,
+                               int32_t ngrid, float* scale, float* alpha);
 
 /* Static description of a status code (never NULL). */
 const char* polyq_status_str(polyq_status status);

@@ -31,12 +31,20 @@ What it computes (fp64, NumPy; Sec. 3.1-3.4 of the paper):
 * Eq. 7: B_real = (1/k) sum_j b_j.
 * Sec. 4.1: clustering: blocks in ascending bits, ascending original index
   inside a block; perm[k'] = original channel at clustered position k'.
+* Eq. 8 (Sec. 3.4): bit-specific activation-aware scaling, after the bit map
+  is fixed: one exponent alpha_b per bit-width b <= 8 from a grid in [0, 1],
+  s_j = 2^rint(alpha_b log2 m_j) for the channels of bit-width b (the power
+  law m_j^alpha_b kept to powers of two), alpha_b minimizing the block's
+  summed proxy error sum_j E_b[j] with Q_b applied as the block is stored: to
+  the block's channels in ascending index order, 128 per group; ties keep the
+  earlier grid point; 16-bit channels keep s = 1.
 
 Readings where the paper is silent (listed in the design doc): the proxy's groups
 run along the input channels in original order; ties in the heap go to the
 lower channel index; a candidate that does not fit the remaining budget is
 dropped (the budget only shrinks); the rounding and repair rules of the
-count snap; the order of the single-channel moves.
+count snap; the order of the single-channel moves; the scales of Eq. 8 are
+rounded to powers of two, and their error is measured on the stored grouping.
 """
 from __future__ import annotations
 
@@ -234,3 +242,39 @@ def allocate(w: np.ndarray, x2: np.ndarray, budget: float, quantum: int,
     bits = quanta_match(err, waterfill(err, budget), quantum, budget)
     perm, blocks = cluster(bits)
     return bits, perm, blocks
+
+
+# --------------------------------------------------------------------------- Eq. 8
+SCALE_GRID = tuple(i / 10 for i in range(11))
+
+
+def block_scale_error(w: np.ndarray, x2: np.ndarray, idx: np.ndarray, s: np.ndarray, b: int) -> float:
+    """sum over j in idx of E_b[j] (Eq. 2) with W~ = diag(s)^-1 Q_b(diag(s) W)
+    restricted to the columns idx (in that order, 128 per group)."""
+    wb = w[:, idx]
+    wt = quantize_group_rows(wb * s[None, :], b) / s[None, :]
+    return float((((wt - wb) ** 2).sum(axis=0) * x2[idx]).sum())
+
+
+def bit_scaling(w: np.ndarray, x2: np.ndarray, saliency: np.ndarray, bits: np.ndarray,
+                grid: Sequence[float] = SCALE_GRID) -> Tuple[np.ndarray, Dict[int, float]]:
+    """Eq. 8: per-channel scales s [k] and alpha_b per bit-width.  Grid values
+    are taken at fp32 precision."""
+    w = np.asarray(w, dtype=np.float64)
+    x2 = np.asarray(x2, dtype=np.float64)
+    m = np.asarray(saliency, dtype=np.float64)
+    bits = np.asarray(bits)
+    s = np.ones(w.shape[1])
+    alpha = {b: 0.0 for b in BITS}
+    for b in BITS:
+        idx = np.nonzero(bits == b)[0]
+        if b == 16 or idx.size == 0:
+            continue
+        best = math.inf
+        for a in grid:
+            a = float(np.float32(a))
+            sb = np.exp2(np.rint(a * np.log2(m[idx])))
+            e = block_scale_error(w, x2, idx, sb, b)
+            if e < best:
+                best, alpha[b], s[idx] = e, a, sb
+    return s, alpha

@@ -117,18 +117,24 @@ def permute_activations(x: np.ndarray, perm: Optional[np.ndarray]) -> np.ndarray
 
 
 def linear(blocks: Blocks, codes, scales, zeros, perm, x, rows: Optional[np.ndarray] = None,
-           chunk: int = 2048) -> Tuple[np.ndarray, np.ndarray]:
+           chunk: int = 2048, xscale: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
     """y[m, n] = sum_k' w_hat[n, k'] x'[m, k'] and bound[m, n] = sum_k' |w_hat x'| (fp64).
 
     Sec. 4.2: the per-block products all accumulate into one output; Eq. 9
     gives the clustered activations.  ``rows`` restricts the output to a
     subset of output channels.  Row chunks bound memory; the product of each
-    chunk is one BLAS matmul.
+    chunk is one BLAS matmul.  ``xscale`` ([k], clustered order): the layer was
+    quantized as Q_b(diag(s) W) (Eq. 1, Sec. 3.4) and xscale[k'] = 1/s of
+    clustered channel k', so the layer is x diag(s)^-1 Q_b(diag(s) W): the
+    clustered activations are multiplied by xscale (and the bound weighs the
+    products the same way).
     """
     codes = np.asarray(codes).view(np.uint16)
     scales = np.asarray(scales)
     zeros = np.asarray(zeros)
     xp = permute_activations(x, perm)
+    if xscale is not None:
+        xp = xp * np.asarray(xscale, dtype=np.float64)[None, :]
     ridx = np.arange(codes.shape[0]) if rows is None else np.asarray(rows, dtype=np.int64)
     m = xp.shape[0]
     y = np.empty((m, ridx.size), dtype=np.float64)

@@ -5,5 +5,6 @@ tensors for device memory and run on torch's current HIP stream.
 """
 from ._lib import (Block, Layout, PolyQError, EXPORTS, LIB_PATH, lib, plan, pack, pack_rows, unpack,  # noqa
                    permute, gemv, gemv_batch, gemm, gemm_batch, gemv_workspace_bytes, gemm_workspace_bytes,
-                   PreparedBatch, read_probe, channel_error, waterfill, quanta_match, cluster, allocate)
+                   PreparedBatch, read_probe, channel_error, waterfill, quanta_match, cluster, allocate, bit_scaling,
+                   SCALE_GRID)
 from .layer import PackedLinear, decode_batch, prefill_batch  # noqa: F401

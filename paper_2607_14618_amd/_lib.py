@@ -33,7 +33,7 @@ EXPORTS = ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq
            "polyq_gemv_batch",
            "polyq_gemm_workspace_bytes", "polyq_gemm", "polyq_gemm_batch_workspace_bytes",
            "polyq_gemm_batch", "polyq_read_probe", "polyq_gemv_batch_noalloc", "polyq_channel_error",
-           "polyq_waterfill", "polyq_quanta_match", "polyq_cluster", "polyq_status_str")
+           "polyq_waterfill", "polyq_quanta_match", "polyq_cluster", "polyq_bit_scaling", "polyq_status_str")
 
 
 class Block(ctypes.Structure):
@@ -66,7 +66,21 @@ class Layout(ctypes.Structure):
 
 class GemvItem(ctypes.Structure):
     _fields_ = [("layout", ctypes.POINTER(Layout)), ("packed", ctypes.c_void_p),
-                ("perm", ctypes.c_void_p), ("x", ctypes.c_void_p), ("y", ctypes.c_void_p)]
+                ("perm", ctypes.c_void_p), ("x", ctypes.c_void_p), ("y", ctypes.c_void_p),
+                ("xscale", ctypes.c_void_p)]
+
+
+def _item6(item):
+    """(layout, packed, perm, x, y[, xscale]) -> the six fields (xscale None if absent)."""
+    if len(item) == 5:
+        return (*item, None)
+    return tuple(item)
+
+
+def _check_xscale(xscale, layout) -> None:
+    if xscale is not None and (xscale.dtype != torch.float16 or xscale.numel() != layout.k
+                               or not xscale.is_contiguous()):
+        raise ValueError("xscale must be a contiguous fp16 [k] tensor")
 
 
 class PolyQError(RuntimeError):
@@ -118,12 +132,13 @@ def lib() -> ctypes.CDLL:
             L.polyq_waterfill.argtypes = [vp, i32, ctypes.c_double, vp]
             L.polyq_quanta_match.argtypes = [vp, i32, i32, ctypes.c_double, vp, vp]
             L.polyq_cluster.argtypes = [vp, i32, vp, ctypes.POINTER(Block), ctypes.POINTER(i32)]
+            L.polyq_bit_scaling.argtypes = [vp, i32, i32, vp, vp, vp, vp, i32, vp, vp]
             L.polyq_status_str.argtypes = [ctypes.c_int]
             L.polyq_status_str.restype = ctypes.c_char_p
             for name in ("polyq_plan", "polyq_pack", "polyq_pack_rows", "polyq_unpack", "polyq_permute",
                          "polyq_gemv", "polyq_gemv_batch", "polyq_gemm", "polyq_gemm_batch",
                          "polyq_read_probe", "polyq_gemv_batch_noalloc", "polyq_channel_error",
-                         "polyq_waterfill", "polyq_quanta_match", "polyq_cluster"):
+                         "polyq_waterfill", "polyq_quanta_match", "polyq_cluster", "polyq_bit_scaling"):
                 getattr(L, name).restype = ctypes.c_int
             _lib = L
     return _lib
@@ -320,9 +335,11 @@ def gemv_batch(items: Sequence[Tuple[Layout, torch.Tensor, Optional[torch.Tensor
         raise ValueError(f"1..{MAX_BATCH} items per batch")
     arr = (GemvItem * len(items))()
     keep, ys, m, dev = [], [], None, None
-    for i, (layout, packed, perm, x, y) in enumerate(items):
+    for i, item in enumerate(items):
+        layout, packed, perm, x, y, xscale = _item6(item)
+        _check_xscale(xscale, layout)
         x2 = x if x.dim() == 2 else x.reshape(1, -1)
-        d = _need_cuda(packed, perm, x2, y, workspace)
+        d = _need_cuda(packed, perm, xscale, x2, y, workspace)
         dev = d if dev is None else dev
         if d != dev:
             raise ValueError("all tensors must be on the same device")
@@ -336,7 +353,7 @@ def gemv_batch(items: Sequence[Tuple[Layout, torch.Tensor, Optional[torch.Tensor
             raise ValueError("perm must be int32 [k]")
         if y is None:
             y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
-        arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y))
+        arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y), _ptr(xscale))
         keep.append(x2)
         ys.append(y)
     if 1 <= m <= MAX_M_GEMV:
@@ -378,9 +395,11 @@ def gemm_batch(items: Sequence[Tuple[Layout, torch.Tensor, Optional[torch.Tensor
         raise ValueError(f"1..{MAX_BATCH} items per batch")
     arr = (GemvItem * len(items))()
     keep, ys, m, dev = [], [], None, None
-    for i, (layout, packed, perm, x, y) in enumerate(items):
+    for i, item in enumerate(items):
+        layout, packed, perm, x, y, xscale = _item6(item)
+        _check_xscale(xscale, layout)
         x2 = x if x.dim() == 2 else x.reshape(1, -1)
-        d = _need_cuda(packed, perm, x2, y, workspace)
+        d = _need_cuda(packed, perm, xscale, x2, y, workspace)
         dev = d if dev is None else dev
         if d != dev:
             raise ValueError("all tensors must be on the same device")
@@ -394,7 +413,7 @@ def gemm_batch(items: Sequence[Tuple[Layout, torch.Tensor, Optional[torch.Tensor
             raise ValueError("perm must be int32 [k]")
         if y is None:
             y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
-        arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y))
+        arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y), _ptr(xscale))
         keep.append(x2)
         ys.append(y)
     need = int(lib().polyq_gemm_batch_workspace_bytes(arr, len(items), m))
@@ -423,9 +442,11 @@ class PreparedBatch:
         self.arr = (GemvItem * len(items))()
         self.keep, self.ys, self.layouts = [], [], []
         m, dev = None, None
-        for i, (layout, packed, perm, x, y) in enumerate(items):
+        for i, item in enumerate(items):
+            layout, packed, perm, x, y, xscale = _item6(item)
+            _check_xscale(xscale, layout)
             x2 = x if x.dim() == 2 else x.reshape(1, -1)
-            d = _need_cuda(packed, perm, x2, y, workspace)
+            d = _need_cuda(packed, perm, xscale, x2, y, workspace)
             dev = d if dev is None else dev
             if d != dev:
                 raise ValueError("all tensors must be on the same device")
@@ -439,8 +460,8 @@ class PreparedBatch:
                 raise ValueError("perm must be int32 [k]")
             if y is None:
                 y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
-            self.arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y))
-            self.keep += [layout, packed, perm, x2]
+            self.arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y), _ptr(xscale))
+            self.keep += [layout, packed, perm, x2, xscale]
             self.ys.append(y)
         self.m, self.count, self.dev = m, len(items), dev
         L = lib()
@@ -490,9 +511,11 @@ def gemv_batch_noalloc(items):
         raise ValueError(f"1..{MAX_BATCH} items per batch")
     arr = (GemvItem * len(items))()
     keep, ys, m, dev = [], [], None, None
-    for i, (layout, packed, perm, x, y) in enumerate(items):
+    for i, item in enumerate(items):
+        layout, packed, perm, x, y, xscale = _item6(item)
+        _check_xscale(xscale, layout)
         x2 = x if x.dim() == 2 else x.reshape(1, -1)
-        d = _need_cuda(packed, perm, x2, y)
+        d = _need_cuda(packed, perm, xscale, x2, y)
         dev = d if dev is None else dev
         if d != dev:
             raise ValueError("all tensors must be on the same device")
@@ -504,7 +527,7 @@ def gemv_batch_noalloc(items):
             raise ValueError("every item of a batch has the same m")
         if y is None:
             y = torch.empty((m, layout.n), dtype=torch.float32, device=dev)
-        arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y))
+        arr[i] = GemvItem(ctypes.pointer(layout), _ptr(packed), _ptr(perm), _ptr(x2), _ptr(y), _ptr(xscale))
         keep.append(x2)
         ys.append(y)
     _check(lib().polyq_gemv_batch_noalloc(arr, len(items), m, _stream(dev)), "polyq_gemv_batch_noalloc")
@@ -572,3 +595,23 @@ def allocate(w, x2, budget: float, quantum: int = QUANTUM, scale=None):
     bits, counts = quanta_match(err, waterfill(err, budget), quantum, budget)
     perm, blocks = cluster(bits)
     return bits, perm, blocks, counts
+
+
+SCALE_GRID = tuple(i / 10 for i in range(11))
+
+
+def bit_scaling(w, x2, saliency, bits, grid=SCALE_GRID):
+    """Eq. 8 (polyq_bit_scaling): per-channel power-of-two scales s [k] (fp32)
+    and the chosen exponent per bit-width {b: alpha_b}."""
+    import numpy as np
+    wa, wp = _host(w, np.float32)
+    n, k = wa.shape
+    xa, xp = _host(x2, np.float64)
+    ma, mp = _host(saliency, np.float64)
+    ba, bp = _host(bits, np.int32)
+    ga, gp = _host(np.asarray(grid, dtype=np.float32), np.float32)
+    scale = np.empty(k, dtype=np.float32)
+    alpha = np.empty(len(BITS), dtype=np.float32)
+    _check(lib().polyq_bit_scaling(wp, n, k, xp, mp, bp, gp, ga.size, scale.ctypes.data, alpha.ctypes.data),
+           "polyq_bit_scaling")
+    return scale, {b: float(a) for b, a in zip(BITS, alpha)}

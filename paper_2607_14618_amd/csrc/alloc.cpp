@@ -1,6 +1,7 @@
-// Compile-time bit allocation (Sec. 3.1-3.3): the activation-aware error
+// Compile-time bit allocation (Sec. 3.1-3.4): the activation-aware error
 // proxy (Eq. 1-2), per-layer waterfilling under a fractional budget (Eq. 3-5),
-// ISA-aware quanta matching (Eq. 6-7) and channel clustering (Sec. 4.1).
+// ISA-aware quanta matching (Eq. 6-7), channel clustering (Sec. 4.1) and the
+// bit-specific activation-aware scales (Eq. 8).
 // Host code on host memory; no HIP calls in this file.
 #include <math.h>
 #include <stdint.h>
@@ -41,6 +42,40 @@ double round_to_half(double v) {
 inline double gain(const double* err, int32_t k, int i, int32_t j) {
   return (err[static_cast<int64_t>(i) * k + j] - err[static_cast<int64_t>(i + 1) * k + j]) /
          static_cast<double>(kBits[i + 1] - kBits[i]);
+}
+
+// Squared reconstruction error, weighted by x2 and summed over the channels
+// `idx` (in that order) and the n rows, of Q_b applied to W[:, idx] diag(s)
+// in groups of 128 consecutive listed channels per row (b = kBits[bi]).
+double block_error(const float* w, int32_t n, int32_t k, const double* x2, const int32_t* idx,
+                   int32_t cnt, const double* s, int bi) {
+  const double qmax = static_cast<double>((1 << kBits[bi]) - 1);
+  std::vector<double> sq(cnt, 0.0), ws(kProxyGroup);
+  for (int32_t r = 0; r < n; ++r) {
+    const float* row = w + static_cast<int64_t>(r) * k;
+    for (int32_t a = 0; a < cnt; a += kProxyGroup) {
+      const int32_t len = std::min(kProxyGroup, cnt - a);
+      double mn = INFINITY, mx = -INFINITY;
+      for (int32_t t = 0; t < len; ++t) {
+        ws[t] = static_cast<double>(row[idx[a + t]]) * s[a + t];
+        mn = std::min(mn, ws[t]);
+        mx = std::max(mx, ws[t]);
+      }
+      const double s16 = round_to_half((mx - mn) / qmax);
+      const bool dead = s16 == 0.0;
+      const double st = dead ? 1.0 : s16;
+      const double z = std::min(std::max(rint(-mn / st), 0.0), qmax);
+      for (int32_t t = 0; t < len; ++t) {
+        const double q = std::min(std::max(rint(ws[t] / st) + z, 0.0), qmax);
+        const double val = dead ? 0.0 : st * (q - z);
+        const double d = val / s[a + t] - static_cast<double>(row[idx[a + t]]);
+        sq[a + t] += d * d;
+      }
+    }
+  }
+  double e = 0.0;
+  for (int32_t t = 0; t < cnt; ++t) e += sq[t] * x2[idx[t]];
+  return e;
 }
 
 }  // namespace
@@ -214,5 +249,49 @@ extern "C" polyq_status polyq_cluster(const int32_t* bits, int32_t k, int32_t* p
   }
   for (int i = nb; i < POLYQ_MAX_BLOCKS; ++i) blocks[i] = polyq_block{0, 0};
   *nblocks = nb;
+  return POLYQ_OK;
+}
+
+extern "C" polyq_status polyq_bit_scaling(const float* w, int32_t n, int32_t k, const double* x2,
+                                          const double* saliency, const int32_t* bits, const float* grid,
+                                          int32_t ngrid, float* scale, float* alpha) {
+  if (w == nullptr || x2 == nullptr || saliency == nullptr || bits == nullptr || grid == nullptr ||
+      scale == nullptr || n < 1 || k < 1 || ngrid < 1)
+    return POLYQ_ERR_ARG;
+  if (static_cast<int64_t>(n) * k > (int64_t{1} << 31)) return POLYQ_ERR_SHAPE;
+  for (int32_t j = 0; j < k; ++j) {
+    if (bit_index(bits[j]) < 0) return POLYQ_ERR_ARG;
+    if (!(x2[j] >= 0.0) || !isfinite(x2[j])) return POLYQ_ERR_ARG;
+    if (!(saliency[j] > 0.0) || !isfinite(saliency[j])) return POLYQ_ERR_ARG;
+  }
+  for (int32_t g = 0; g < ngrid; ++g)
+    if (!(grid[g] >= 0.0f && grid[g] <= 1.0f)) return POLYQ_ERR_ARG;
+  for (int32_t j = 0; j < k; ++j) scale[j] = 1.0f;
+  float al[POLYQ_NUM_BITS] = {0.f, 0.f, 0.f, 0.f, 0.f};
+  std::vector<int32_t> idx;
+  std::vector<double> s, best_s;
+  for (int bi = 0; bi + 1 < POLYQ_NUM_BITS; ++bi) {  // 16-bit channels are unquantized: s = 1
+    idx.clear();
+    for (int32_t j = 0; j < k; ++j)
+      if (bits[j] == kBits[bi]) idx.push_back(j);
+    if (idx.empty()) continue;
+    const int32_t cnt = static_cast<int32_t>(idx.size());
+    s.assign(cnt, 1.0);
+    double best = INFINITY;
+    for (int32_t g = 0; g < ngrid; ++g) {
+      // s_j = 2^rint(alpha log2 m_j): Eq. 8's power law, kept to powers of two
+      for (int32_t t = 0; t < cnt; ++t)
+        s[t] = ldexp(1.0, static_cast<int>(rint(static_cast<double>(grid[g]) * log2(saliency[idx[t]]))));
+      const double e = block_error(w, n, k, x2, idx.data(), cnt, s.data(), bi);
+      if (e < best) {  // ties keep the earlier grid point
+        best = e;
+        best_s = s;
+        al[bi] = grid[g];
+      }
+    }
+    for (int32_t t = 0; t < cnt; ++t) scale[idx[t]] = static_cast<float>(best_s[t]);
+  }
+  if (alpha != nullptr)
+    for (int i = 0; i < POLYQ_NUM_BITS; ++i) alpha[i] = al[i];
   return POLYQ_OK;
 }

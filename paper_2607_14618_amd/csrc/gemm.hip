@@ -605,9 +605,10 @@ int plan_splits(const polyq_layout& L, int32_t m, int32_t count) {
   return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>({256 / wg, kMaxSplits, groups / 4})));
 }
 
-// Workspace of a batch: one permuted copy per distinct (x, perm) pair with
-// perm != NULL (region[i] = byte offset of item i's copy, or -1), then the
-// split partial sums of a single-linear launch (at *partial_off).
+// Workspace of a batch: one clustered copy x' = x[:, perm] (times the channel
+// factors of Eq. 8) per distinct (x, perm, factors) of the items with a
+// permutation or factors (region[i] = byte offset of item i's copy, or -1),
+// then the split partial sums of a single-linear launch (at *partial_off).
 polyq_status plan_gemm_batch(const polyq_gemv_item* items, int32_t count, int32_t m,
                              int64_t* region, size_t* partial_off, int* splits, size_t* total) {
   if (items == nullptr || count < 1 || m < 1) return POLYQ_ERR_ARG;
@@ -617,10 +618,10 @@ polyq_status plan_gemm_batch(const polyq_gemv_item* items, int32_t count, int32_
     if (!layout_is_valid(items[i].layout)) return POLYQ_ERR_ARG;
     if (static_cast<int64_t>(m) * items[i].layout->k * 2 > 0x7FFFFFFFll) return POLYQ_ERR_CAPACITY;
     region[i] = -1;
-    if (items[i].perm == nullptr) continue;
+    if (items[i].perm == nullptr && items[i].xscale == nullptr) continue;
     for (int j = 0; j < i; ++j)
-      if (items[j].perm == items[i].perm && items[j].x == items[i].x &&
-          items[j].layout->k == items[i].layout->k) {
+      if (region[j] >= 0 && items[j].perm == items[i].perm && items[j].x == items[i].x &&
+          items[j].xscale == items[i].xscale && items[j].layout->k == items[i].layout->k) {
         region[i] = region[j];
         break;
       }
@@ -651,7 +652,7 @@ extern "C" size_t polyq_gemm_batch_workspace_bytes(const polyq_gemm_item* items,
 extern "C" size_t polyq_gemm_workspace_bytes(const polyq_layout* layout, int32_t m, int perm_given) {
   if (!layout_is_valid(layout) || m < 1) return 0;
   const int32_t dummy = 0;
-  const polyq_gemm_item item{layout, nullptr, perm_given ? &dummy : nullptr, nullptr, nullptr};
+  const polyq_gemm_item item{layout, nullptr, perm_given ? &dummy : nullptr, nullptr, nullptr, nullptr};
   return polyq_gemm_batch_workspace_bytes(&item, 1, m);
 }
 
@@ -678,7 +679,7 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
     if (reinterpret_cast<uintptr_t>(itm.packed) % 256 != 0 || reinterpret_cast<uintptr_t>(itm.y) % 4 != 0)
       return POLYQ_ERR_ARG;
     if (L.packed_bytes > 0x7FFFFFFFll) return POLYQ_ERR_CAPACITY;
-    if (itm.perm == nullptr && reinterpret_cast<uintptr_t>(itm.x) % 16 != 0)
+    if (itm.perm == nullptr && itm.xscale == nullptr && reinterpret_cast<uintptr_t>(itm.x) % 16 != 0)
       return POLYQ_ERR_ARG;  // clustered activations are read as 16-byte vectors
   }
   // Every check above and here comes before the first launch.
@@ -694,11 +695,16 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
     const polyq_gemv_item& itm = items[i];
     const polyq_layout& L = *itm.layout;
     const uint16_t* xp = itm.x;
-    if (itm.perm != nullptr) {
+    if (region[i] >= 0) {
       uint16_t* out = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(workspace) + region[i]);
       bool first = true;
       for (int j = 0; j < i; ++j) first = first && region[j] != region[i];
-      if (first) launch_permute_rows(itm.perm, itm.x, out, m, L.k, st);
+      if (first) {
+        if (itm.xscale != nullptr)
+          launch_scale_rows(itm.perm, itm.xscale, itm.x, out, m, L.k, true, st);
+        else
+          launch_permute_rows(itm.perm, itm.x, out, m, L.k, st);
+      }
       xp = out;
     }
     GemmItem& g = a.item[i];
@@ -747,6 +753,6 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
 extern "C" polyq_status polyq_gemm(const polyq_layout* layout, const void* packed,
                                    const int32_t* perm, const uint16_t* x, int32_t m, float* y,
                                    void* workspace, size_t workspace_bytes, void* stream) {
-  const polyq_gemm_item item{layout, packed, perm, x, y};
+  const polyq_gemm_item item{layout, packed, perm, x, y, nullptr};
   return polyq_gemm_batch(&item, 1, m, workspace, workspace_bytes, stream);
 }

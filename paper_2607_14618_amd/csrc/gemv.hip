@@ -54,9 +54,10 @@ struct GemvItem {
   const int32_t* perm;
   const uint16_t* x;
   float* y;
-  float* partial;     // [S][m][rows_pad], only when S > 1
+  float* partial;     // [S][m][n_tiles * 64], only when S > 1
   uint32_t* counter;  // [n_tiles], only when S > 1
-  int32_t n, k, m, nblocks, rows_pad, S;
+  const uint16_t* xscale;  // fp16 [k] factors on x' (one token only), or NULL
+  int32_t n, k, m, nblocks, S;
   int32_t wave_lds;       // LDS bytes of one wave's staging region
   int32_t n_tiles, n_chunks;
   uint32_t tiles_magic;   // div_magic(n_tiles)
@@ -67,7 +68,6 @@ struct GemvItem {
   int32_t waves[POLYQ_MAX_BLOCKS];       // waves per tile given to each block
   uint32_t magic[POLYQ_MAX_BLOCKS];      // div_magic(waves)
   int32_t tile_bytes[POLYQ_MAX_BLOCKS];
-  int32_t pad1;
   int64_t block_offset[POLYQ_MAX_BLOCKS];
 };
 
@@ -552,6 +552,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   const int fast_end = min(range, kFastRounds * kRound);
   const int rounds = max((fast_end + kRound - 1) / kRound, 1);
   const bool use_perm = perm != nullptr;
+  const uint16_t* xsc = ITEM(const uint16_t*, xscale);
+  const bool use_scale = xsc != nullptr;  // one token only (the host makes sure)
   // Token 0's activations as a raw buffer of k halves: a byte offset at or
   // past 2k (an index outside [0, k)) reads 0.
   const __amdgpu_buffer_rsrc_t xrs =
@@ -604,8 +606,15 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       *reinterpret_cast<uint4*>(zs16 + kk) = uint4{0u, 0u, 0u, 0u};
     }
   };
-  auto stage_fast = [&](auto rounds_tag, auto perm_tag) {
+  // x' times the channel factors (Eq. 8's 1/s_j; packed fp16 products, exact
+  // for powers of two)
+  auto scale8 = [&](uint4 q, uint4 f) {
+    return uint4{as_u32(as_h2(q.x) * as_h2(f.x)), as_u32(as_h2(q.y) * as_h2(f.y)),
+                 as_u32(as_h2(q.z) * as_h2(f.z)), as_u32(as_h2(q.w) * as_h2(f.w))};
+  };
+  auto stage_fast = [&](auto rounds_tag, auto perm_tag, auto scale_tag) {
     constexpr int R = decltype(rounds_tag)::value;
+    constexpr bool SC = decltype(scale_tag)::value;
     // lanes past the range load the range's first channels again; their
     // values are never stored
     int kp[R];
@@ -616,21 +625,29 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     }
     if constexpr (!decltype(perm_tag)::value) {
       // x already clustered: 8 consecutive channels per lane and round.
-      uint4 xv[R];
+      uint4 xv[R], fv[R];
 #pragma unroll
       for (int u = 0; u < R; ++u) xv[u] = ldg16(xg + kp[u]);
+      if constexpr (SC) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) fv[u] = ldg16(xsc + kp[u]);
+      }
       issue_meta_and_weights(rounds_tag);
 #pragma unroll
-      for (int u = 0; u < R; ++u) store_x(u, xv[u]);
+      for (int u = 0; u < R; ++u) store_x(u, SC ? scale8(xv[u], fv[u]) : xv[u]);
       store_meta(rounds_tag);
     } else {
       // (1) The permutation of the lane's 8 channels per round, then (2) one
       // 2-byte gather per channel (one memory round trip each).
-      uint4 pv[R][2];
+      uint4 pv[R][2], fv[R];
 #pragma unroll
       for (int u = 0; u < R; ++u) {
         pv[u][0] = ldg16(perm + kp[u]);
         pv[u][1] = ldg16(perm + kp[u] + 4);
+      }
+      if constexpr (SC) {
+#pragma unroll
+        for (int u = 0; u < R; ++u) fv[u] = ldg16(xsc + kp[u]);
       }
       uint32_t h[R][8];
 #pragma unroll
@@ -643,9 +660,11 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       }
       issue_meta_and_weights(rounds_tag);
 #pragma unroll
-      for (int u = 0; u < R; ++u)
-        store_x(u, uint4{h[u][0] | (h[u][1] << 16), h[u][2] | (h[u][3] << 16),
-                         h[u][4] | (h[u][5] << 16), h[u][6] | (h[u][7] << 16)});
+      for (int u = 0; u < R; ++u) {
+        const uint4 q{h[u][0] | (h[u][1] << 16), h[u][2] | (h[u][3] << 16), h[u][4] | (h[u][5] << 16),
+                      h[u][6] | (h[u][7] << 16)};
+        store_x(u, SC ? scale8(q, fv[u]) : q);
+      }
       store_meta(rounds_tag);
     }
   };
@@ -658,20 +677,26 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   // A wave without work stages nothing (and waits for nothing).
   bool exact = true;
   if (has_work) {
+    // one copy of the staging per count of rounds, form of x and scaling, so
+    // that the unscaled forms issue exactly the loads they did without it
+    auto stage = [&](auto perm_tag, auto scale_tag) {
+      switch (rounds) {
+        case 4: stage_fast(I4{}, perm_tag, scale_tag); break;
+        case 3: stage_fast(I3{}, perm_tag, scale_tag); break;
+        case 2: stage_fast(I2{}, perm_tag, scale_tag); break;
+        default: stage_fast(I1{}, perm_tag, scale_tag); break;
+      }
+    };
     if (use_perm) {
-      switch (rounds) {
-        case 4: stage_fast(I4{}, Gather{}); break;
-        case 3: stage_fast(I3{}, Gather{}); break;
-        case 2: stage_fast(I2{}, Gather{}); break;
-        default: stage_fast(I1{}, Gather{}); break;
-      }
+      if (use_scale)
+        stage(Gather{}, std::true_type{});
+      else
+        stage(Gather{}, std::false_type{});
     } else {
-      switch (rounds) {
-        case 4: stage_fast(I4{}, Clustered{}); break;
-        case 3: stage_fast(I3{}, Clustered{}); break;
-        case 2: stage_fast(I2{}, Clustered{}); break;
-        default: stage_fast(I1{}, Clustered{}); break;
-      }
+      if (use_scale)
+        stage(Clustered{}, std::true_type{});
+      else
+        stage(Clustered{}, std::false_type{});
     }
     // (6) More tokens, or channels past the fast rounds (these loads wait behind
     // the weight slots).  Clustered x: tokens go in batches of kTokBatch, every
@@ -681,6 +706,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     // buffer (indices outside [0, k) read 0).
     auto stage_slow = [&](int k_lo, int k_hi, int t_lo, bool zero_row) {
       for (int kk = k_lo + lane * 8; kk < k_hi; kk += kRound) {
+        // channel factors (one token only: several come scaled by the host's shuffle)
+        const uint4 f = use_scale ? ldg16(xsc + kbase + kk) : uint4{0u, 0u, 0u, 0u};
         if (!use_perm) {
           for (int t0 = t_lo; t0 < m; t0 += kTokBatch) {
             uint4 v[kTokBatch];
@@ -689,7 +716,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
               v[j] = ldg16(xg + static_cast<int64_t>(min(t0 + j, m - 1)) * kdim + kbase + kk);
 #pragma unroll
             for (int j = 0; j < kTokBatch; ++j)
-              if (t0 + j < m) *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) = v[j];
+              if (t0 + j < m)
+                *reinterpret_cast<uint4*>(xs16 + (t0 + j) * range + kk) = use_scale ? scale8(v[j], f) : v[j];
           }
         } else {
           // a permutation comes with one token (several take the explicit
@@ -700,8 +728,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
 #pragma unroll
           for (int e = 0; e < 8; ++e)
             h[e] = __builtin_amdgcn_raw_buffer_load_b16(xrs, min(p8[e], static_cast<uint32_t>(kdim)) << 1, 0, 0);
-          *reinterpret_cast<uint4*>(xs16 + kk) =
-              uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+          const uint4 q{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+          *reinterpret_cast<uint4*>(xs16 + kk) = use_scale ? scale8(q, f) : q;
         }
         if (zero_row) *reinterpret_cast<uint4*>(zs16 + kk) = uint4{0u, 0u, 0u, 0u};
       }
@@ -784,7 +812,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   // invalidates the XCD's whole L2 -- and was measured to read stale partials.)
   float* partial = ITEM(float*, partial);
   uint32_t* counter = ITEM(uint32_t*, counter);
-  const int rows_pad = ITEM(int32_t, rows_pad);
+  const int rows_pad = n_tiles * kTileRows;
   auto wg_sum = [&](int mi) {
     float v = 0.f;
 #pragma unroll
@@ -874,10 +902,11 @@ namespace {
 // Plans of a batch: every linear's splits are sized for the whole launch.
 // Workspace: per item its split-K region (counters, partials; the part that
 // must be zero on entry and is zero again on return), then one clustered copy
-// x' = x[:, perm] per distinct (x, perm) of the items that take Eq. 9's
-// explicit shuffle (several tokens with a permutation: each wave then stages
-// its tokens' activations with 16-byte loads instead of one 2-byte gather per
-// channel and token).
+// x' = x[:, perm] (times the channel factors of Eq. 8, if any) per distinct
+// (x, perm, factors) of the items that take Eq. 9's explicit shuffle (several
+// tokens with a permutation or factors: each wave then stages its tokens'
+// activations with 16-byte loads instead of one 2-byte gather per channel and
+// token).
 struct BatchPlan {
   GemvPlan plans[POLYQ_MAX_BATCH];
   size_t split_off[POLYQ_MAX_BATCH];
@@ -908,10 +937,10 @@ polyq_status plan_batch(const polyq_gemv_item* items, int32_t count, int32_t m, 
   for (int i = 0; i < count; ++i) {
     bp->xp_off[i] = -1;
     bp->xp_first[i] = false;
-    if (m == 1 || items[i].perm == nullptr) continue;
+    if (m == 1 || (items[i].perm == nullptr && items[i].xscale == nullptr)) continue;
     for (int j = 0; j < i; ++j)
       if (bp->xp_off[j] >= 0 && items[j].perm == items[i].perm && items[j].x == items[i].x &&
-          items[j].layout->k == items[i].layout->k) {
+          items[j].xscale == items[i].xscale && items[j].layout->k == items[i].layout->k) {
         bp->xp_off[i] = bp->xp_off[j];
         break;
       }
@@ -934,8 +963,8 @@ polyq_status check_items(const polyq_gemv_item* items, int32_t count) {
     if (t.packed == nullptr || t.x == nullptr || t.y == nullptr) return POLYQ_ERR_ARG;
     if (reinterpret_cast<uintptr_t>(t.packed) % 256 != 0) return POLYQ_ERR_ARG;
     if (reinterpret_cast<uintptr_t>(t.x) % 16 != 0 || reinterpret_cast<uintptr_t>(t.y) % 4 != 0 ||
-        reinterpret_cast<uintptr_t>(t.perm) % 16 != 0)
-      return POLYQ_ERR_ARG;  // activations and permutation are read as 16-byte vectors
+        reinterpret_cast<uintptr_t>(t.perm) % 16 != 0 || reinterpret_cast<uintptr_t>(t.xscale) % 16 != 0)
+      return POLYQ_ERR_ARG;  // activations, permutation and factors are read as 16-byte vectors
     for (int b = 0; b < t.layout->nblocks; ++b)
       if (t.layout->tile_bytes[b] > INT32_MAX) return POLYQ_ERR_UNSUPPORTED;
   }
@@ -996,11 +1025,12 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
     const bool shuffled = bp.xp_off[i] >= 0;
     g.packed = static_cast<const uint8_t*>(t.packed);
     g.perm = shuffled ? nullptr : t.perm;
+    g.xscale = shuffled ? nullptr : t.xscale;
     g.x = shuffled ? reinterpret_cast<const uint16_t*>(ws + bp.xp_off[i]) : t.x;
     g.y = t.y;
     g.partial = nullptr;
     g.counter = nullptr;
-    if (p.S > 1) {  // [counters: n_tiles x u32, 256-aligned][partials: S x m x rows_pad fp32]
+    if (p.S > 1) {  // [counters: n_tiles x u32, 256-aligned][partials: S x m x n_tiles*64 fp32]
       uint8_t* w = ws + bp.split_off[i];
       g.counter = reinterpret_cast<uint32_t*>(w);
       g.partial = reinterpret_cast<float*>(w + align_up(static_cast<int64_t>(L.n_tiles) * 4, 256));
@@ -1009,7 +1039,6 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
     g.k = L.k;
     g.m = m;
     g.nblocks = L.nblocks;
-    g.rows_pad = L.n_tiles * kTileRows;
     g.S = p.S;
     g.wave_lds = static_cast<int32_t>(gemv_wave_lds_bytes(p, m));
     g.zero_offset = static_cast<int32_t>(gemv_zero_offset(p, m));
@@ -1031,11 +1060,16 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
     wgs = std::max(wgs, L.n_tiles * p.S);
   }
   hipStream_t hs = static_cast<hipStream_t>(stream);
-  // Eq. 9's explicit shuffle first, once per distinct (x, perm) of several tokens
-  for (int i = 0; i < count; ++i)
-    if (bp.xp_first[i])
-      launch_permute_rows(items[i].perm, items[i].x, reinterpret_cast<uint16_t*>(ws + bp.xp_off[i]), m,
-                          items[i].layout->k, hs);
+  // Eq. 9's explicit shuffle first (with Eq. 8's factors folded in), once per
+  // distinct (x, perm, factors) of several tokens
+  for (int i = 0; i < count; ++i) {
+    if (!bp.xp_first[i]) continue;
+    uint16_t* xp = reinterpret_cast<uint16_t*>(ws + bp.xp_off[i]);
+    if (items[i].xscale != nullptr)
+      launch_scale_rows(items[i].perm, items[i].xscale, items[i].x, xp, m, items[i].layout->k, false, hs);
+    else
+      launch_permute_rows(items[i].perm, items[i].x, xp, m, items[i].layout->k, hs);
+  }
   hipLaunchKernelGGL(gemv_kernel, dim3(wgs, count), dim3(kWaves * 64), bp.lds, hs, a);
   return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
 }
@@ -1043,6 +1077,6 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
 extern "C" polyq_status polyq_gemv(const polyq_layout* layout, const void* packed,
                                    const int32_t* perm, const uint16_t* x, int32_t m, float* y,
                                    void* workspace, size_t workspace_bytes, void* stream) {
-  const polyq_gemv_item item{layout, packed, perm, x, y};
+  const polyq_gemv_item item{layout, packed, perm, x, y, nullptr};
   return polyq_gemv_batch(&item, 1, m, workspace, workspace_bytes, stream);
 }

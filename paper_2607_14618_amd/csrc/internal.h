@@ -109,6 +109,13 @@ polyq_status gemv_batch_workspace_status(const polyq_gemv_item* items, int32_t c
 void launch_permute_rows(const int32_t* perm, const uint16_t* x, uint16_t* out, int32_t m, int32_t k,
                          hipStream_t stream);
 
+// x'[i][j] = x[i][perm[j]] * f[j] for m rows of k 2-byte activations (fp16,
+// or bf16 when `bf16`); perm may be NULL (identity), an entry outside [0, k)
+// yields 0; f: fp16 channel factors (Eq. 8's 1/s_j), the product rounded to the
+// activation type.  Launch only: the caller has validated the arguments.
+void launch_scale_rows(const int32_t* perm, const uint16_t* f, const uint16_t* x, uint16_t* out, int32_t m,
+                       int32_t k, bool bf16, hipStream_t stream);
+
 // Block accessor of a layout for wave_range (host side).
 struct LayoutBlocks {
   const polyq_layout* L;

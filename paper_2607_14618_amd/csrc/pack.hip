@@ -192,6 +192,43 @@ __global__ __launch_bounds__(256) void permute_rows_kernel(const int32_t* __rest
   out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
 }
 
+// x'[i][j] = x[i][perm[j]] * f[j] (perm NULL: the identity), f the fp16
+// channel factors of Eq. 8 (1/s_j).  The product is formed in fp32 and
+// rounded to the activation type (fp16, or bf16 when `bf16`), nearest even:
+// exact for a power-of-two factor.  One thread per 8 channels of a row.
+__device__ __forceinline__ float act_to_f32(uint16_t h, bool bf16) {
+  return bf16 ? __builtin_bit_cast(float, static_cast<uint32_t>(h) << 16)
+              : static_cast<float>(__builtin_bit_cast(_Float16, h));
+}
+__device__ __forceinline__ uint16_t f32_to_act(float v, bool bf16) {
+  if (!bf16) return __builtin_bit_cast(uint16_t, static_cast<_Float16>(v));
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);  // NaN stays NaN
+  return static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+__global__ __launch_bounds__(256) void scale_rows_kernel(const int32_t* __restrict__ perm,
+                                                         const uint16_t* __restrict__ f,
+                                                         const uint16_t* __restrict__ x,
+                                                         uint16_t* __restrict__ out, int m, int k, int bf16) {
+  const int kp = (k + 7) / 8;  // pieces per row
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (t >= static_cast<int64_t>(m) * kp) return;
+  const int i = static_cast<int>(t / kp), j0 = static_cast<int>(t % kp) * 8;
+  const uint16_t* row = x + static_cast<int64_t>(i) * k;
+  uint16_t* dst = out + static_cast<int64_t>(i) * k;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int j = j0 + e;
+    if (j < k) {
+      const int src = perm != nullptr ? perm[j] : j;
+      const float v = static_cast<unsigned>(src) < static_cast<unsigned>(k) ? act_to_f32(row[src], bf16 != 0) : 0.f;
+      const float fj = static_cast<float>(__builtin_bit_cast(_Float16, f[j]));
+      dst[j] = f32_to_act(v * fj, bf16 != 0);
+    }
+  }
+}
+
 template <int B>
 void launch_pack(const polyq_layout& L, int i, const uint16_t* codes, const int32_t* row_perm,
                  uint8_t* region, hipStream_t st) {
@@ -225,6 +262,13 @@ void launch_permute_rows(const int32_t* perm, const uint16_t* x, uint16_t* out, 
     hipLaunchKernelGGL(permute_rows_kernel, dim3(static_cast<unsigned>((n_el + 255) / 256)), dim3(256), 0,
                        st, perm, x, out, m, k);
   }
+}
+
+void launch_scale_rows(const int32_t* perm, const uint16_t* f, const uint16_t* x, uint16_t* out, int32_t m,
+                       int32_t k, bool bf16, hipStream_t st) {
+  const int64_t threads = static_cast<int64_t>(m) * ((k + 7) / 8);
+  hipLaunchKernelGGL(scale_rows_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st,
+                     perm, f, x, out, m, k, bf16 ? 1 : 0);
 }
 
 }  // namespace polyq

@@ -20,7 +20,8 @@ class PackedLinear:
     """
 
     def __init__(self, blocks: Sequence[Tuple[int, int]], codes: torch.Tensor,
-                 scales: torch.Tensor, zeros: torch.Tensor, perm, device="cuda", out_perm=None):
+                 scales: torch.Tensor, zeros: torch.Tensor, perm, device="cuda", out_perm=None,
+                 xscale=None):
         n, k = codes.shape
         self.layout = _lib.plan(n, k, blocks)
         dev = torch.device(device)
@@ -34,6 +35,10 @@ class PackedLinear:
             row_perm = torch.as_tensor(np.asarray(out_perm, dtype=np.int32)).to(dev).contiguous()
             self.packed = _lib.pack_rows(self.layout, codes, scales, zeros, row_perm)
         self.perm = torch.as_tensor(np.asarray(perm, dtype=np.int32)).to(dev)
+        # Eq. 8: fp16 [k] factors 1/s_j per clustered channel, applied to x' (weights
+        # packed from Q_b(diag(s) W)); None for an unscaled layer
+        self.xscale = None if xscale is None else \
+            torch.as_tensor(np.asarray(xscale, dtype=np.float16)).to(dev).contiguous()
         self.n, self.k = n, k
 
     @property
@@ -42,10 +47,16 @@ class PackedLinear:
 
     def decode(self, x: torch.Tensor, pre_permuted: bool = False,
                y: Optional[torch.Tensor] = None) -> torch.Tensor:
+        if self.xscale is not None:
+            return _lib.gemv_batch([(self.layout, self.packed, None if pre_permuted else self.perm, x, y,
+                                     self.xscale)])[0]
         return _lib.gemv(self.layout, self.packed, None if pre_permuted else self.perm, x, y)
 
     def prefill(self, x: torch.Tensor, pre_permuted: bool = False,
                 y: Optional[torch.Tensor] = None) -> torch.Tensor:
+        if self.xscale is not None:
+            return _lib.gemm_batch([(self.layout, self.packed, None if pre_permuted else self.perm, x, y,
+                                     self.xscale)])[0]
         return _lib.gemm(self.layout, self.packed, None if pre_permuted else self.perm, x, y)
 
     def permute(self, x: torch.Tensor) -> torch.Tensor:
@@ -57,7 +68,7 @@ def decode_batch(linears: Sequence["PackedLinear"], xs: Sequence[torch.Tensor],
     """One polyq_gemv_batch launch over several linears (same token count):
     e.g. the q/k/v projections of a layer, which share x and the permutation."""
     ys = list(ys) if ys is not None else [None] * len(linears)
-    items = [(pl.layout, pl.packed, None if pre_permuted else pl.perm, x, y)
+    items = [(pl.layout, pl.packed, None if pre_permuted else pl.perm, x, y, pl.xscale)
              for pl, x, y in zip(linears, xs, ys)]
     return _lib.gemv_batch(items)
 
@@ -68,6 +79,6 @@ def prefill_batch(linears: Sequence["PackedLinear"], xs: Sequence[torch.Tensor],
     the q/k/v projections of a layer, which share x and the permutation (one
     permuted copy of x serves all of them)."""
     ys = list(ys) if ys is not None else [None] * len(linears)
-    items = [(pl.layout, pl.packed, None if pre_permuted else pl.perm, x, y)
+    items = [(pl.layout, pl.packed, None if pre_permuted else pl.perm, x, y, pl.xscale)
              for pl, x, y in zip(linears, xs, ys)]
     return _lib.gemm_batch(items)

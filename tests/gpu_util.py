@@ -24,11 +24,12 @@ def packed_linear(lin) -> pq.PackedLinear:
                            device=dev())
 
 
-def oracle_ref(lin, x, rows=None, pre_permuted=False):
+def oracle_ref(lin, x, rows=None, pre_permuted=False, xscale=None):
     codes = np_(lin.codes).view(np.uint16)
     perm = None if pre_permuted else lin.perm
     return oracle.linear(lin.blocks, codes, np_(lin.scales), np_(lin.zeros), perm,
-                         np_(x.float()), rows=rows)
+                         np_(x.float()), rows=rows,
+                         xscale=None if xscale is None else np_(xscale).astype(np.float64))
 
 
 def assert_parity(y_gpu, y_ref, bound, what=""):

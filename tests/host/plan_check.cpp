@@ -179,6 +179,22 @@ void check_alloc(Rng& r, int iter) {
   for (int j = 0; j < k; ++j) CHECK(seen[j] == 1, "perm is not a permutation");
   polyq_layout L;
   CHECK(polyq_plan(n, k, blocks, nb, &L) == POLYQ_OK, "clustered blocks plan");
+  // Eq. 8 scales on the final bit map: powers of two, 16-bit channels at 1
+  std::vector<double> sal(k);
+  for (int j = 0; j < k; ++j) sal[j] = 0.05 + static_cast<double>(r.next() % 4000) / 100.0;
+  const float grid[4] = {0.0f, 0.3f, 0.7f, 1.0f};
+  float alpha[POLYQ_NUM_BITS];
+  CHECK(polyq_bit_scaling(w.data(), n, k, x2.data(), sal.data(), bits.data(), grid, 4, s.data(), alpha) ==
+            POLYQ_OK, "bit_scaling");
+  for (int j = 0; j < k; ++j) {
+    int e = 0;
+    CHECK(frexpf(s[j], &e) == 0.5f, "scale %g is not a power of two", static_cast<double>(s[j]));
+    CHECK(bits[j] != 16 || s[j] == 1.0f, "16-bit channel scaled");
+  }
+  CHECK(alpha[POLYQ_NUM_BITS - 1] == 0.0f, "alpha_16 = 0");
+  const float bad_grid[1] = {1.5f};
+  CHECK(polyq_bit_scaling(w.data(), n, k, x2.data(), sal.data(), bits.data(), bad_grid, 1, s.data(), nullptr) ==
+            POLYQ_ERR_ARG, "grid out of [0, 1] refused");
   CHECK(polyq_waterfill(err.data(), k, NAN, bits.data()) == POLYQ_ERR_ARG, "NaN budget refused");
   CHECK(polyq_quanta_match(err.data(), k, 7, budget, bits.data(), counts) ==
             (k % 7 ? POLYQ_ERR_QUANTUM : POLYQ_OK), "quantum check");

@@ -1,5 +1,5 @@
 """The library's bit allocation (polyq_channel_error, polyq_waterfill,
-polyq_quanta_match, polyq_cluster: host code behind the C ABI) against the
+polyq_quanta_match, polyq_cluster, polyq_bit_scaling: host code behind the C ABI) against the
 CPU oracle on the same seeded inputs.  Bit maps, counts and permutations must
 be identical; the proxy's values equal to the last bit (both sum the rows in
 order), checked within 1e-12 relative.  CPU only: these entry points do no
@@ -97,6 +97,28 @@ def test_end_to_end_allocation_matches_and_plans():
     assert layout.k == 1280 and abs(layout.code_bits / (64 * 1280) - 3.0) <= 8 * 32 / 2 / 1280
 
 
+@pytest.mark.parametrize("n,k,seed", [(64, 320, 1), (37, 1000, 2), (8, 4096, 3)])
+def test_bit_scaling_matches_the_oracle(n, k, seed):
+    """Scales and exponents identical; bits from the allocation itself, so
+    blocks span several groups with ragged tails."""
+    w, x2, _ = _inputs(n, k, seed)
+    mag = np.sqrt(x2)
+    m = mag / mag.mean()
+    bits, _, _, _ = pq.allocate(w, x2, 3.0, 8)
+    s, alpha = pq.bit_scaling(w, x2, m, bits)
+    rs, ralpha = ao.bit_scaling(w.astype(np.float64), x2, m, bits)
+    assert s.dtype == np.float32 and np.array_equal(s.astype(np.float64), rs)
+    assert alpha == ralpha
+    assert any(a > 0 for a in alpha.values())
+
+
+def test_bit_scaling_hand_example_matches():
+    w = np.array([[0.25, -1.5, 10.0, 0.0, 1.5]], dtype=np.float32)
+    s, alpha = pq.bit_scaling(w, np.array([100.0, 1, 1, 1, 1]), np.array([4.0, 1, 8, 1, 1]),
+                              [2, 2, 8, 2, 2], grid=[0.0, 0.5, 1.0])
+    assert s.tolist() == [4.0, 1.0, 1.0, 1.0, 1.0] and alpha[2] == 1.0 and alpha[8] == 0.0
+
+
 @pytest.mark.parametrize("call", [
     lambda: pq.channel_error(np.zeros((2, 4), np.float32), np.array([1.0, -1.0, 1.0, 1.0])),
     lambda: pq.channel_error(np.zeros((2, 4), np.float32), np.ones(4), np.array([1, 0, 1, 1], np.float32)),
@@ -104,6 +126,10 @@ def test_end_to_end_allocation_matches_and_plans():
     lambda: pq.waterfill(np.zeros((5, 4)), 17.0),
     lambda: pq.quanta_match(np.zeros((5, 4)), [2, 5, 2, 2], 4, 3.0),
     lambda: pq.cluster([2, 3, 7]),
+    lambda: pq.bit_scaling(np.zeros((2, 4), np.float32), np.ones(4), np.array([1.0, 0, 1, 1]), [2] * 4),
+    lambda: pq.bit_scaling(np.zeros((2, 4), np.float32), np.ones(4), np.ones(4), [2, 5, 2, 2]),
+    lambda: pq.bit_scaling(np.zeros((2, 4), np.float32), np.ones(4), np.ones(4), [2] * 4, grid=[0.0, 1.5]),
+    lambda: pq.bit_scaling(np.zeros((2, 4), np.float32), np.ones(4), np.ones(4), [2] * 4, grid=[]),
 ])
 def test_invalid_arguments_are_refused(call):
     with pytest.raises(pq.PolyQError, match="POLYQ_ERR_ARG"):

@@ -1,7 +1,8 @@
-"""Pins for the bit-allocation oracle (Sec. 3.1-3.3), CPU only: hand-derived
-fixtures, exact special cases of the error proxy, and the invariants the paper
+"""Pins for the bit-allocation oracle (Sec. 3.1-3.4), CPU only: hand-derived
+fixtures, exact special cases of the error proxy, the invariants the paper
 states for waterfilling (budget never exceeded, nothing that fits is left) and
-for quanta matching (counts on the quantum, total kept, neighbour moves)."""
+for quanta matching (counts on the quantum, total kept, neighbour moves), and
+a hand-derived case of the bit-specific scaling search (Eq. 8)."""
 import json
 import os
 
@@ -218,3 +219,65 @@ def test_a_salient_channel_gets_more_bits():
     # three channels do not make a 32-channel block: they stay in the top level left
     assert all(bits[j] == bits.max() for j in (5, 77, 200))
     assert sum(l for _, l in blocks) == 256 and sorted(perm.tolist()) == list(range(256))
+
+
+# --------------------------------------------------------------------------- Eq. 8
+def test_scaling_hand_example():
+    """One output row; channels 0, 1, 3, 4 at 2 bits (one group: [0.25, -1.5, 0, 1.5]
+    in index order), channel 2 alone at 8 bits; x2 = [100, 1, 1, 1, 1],
+    m = [4, 1, 8, 1, 1], grid {0, 0.5, 1}.
+    alpha = 0 or 0.5 (s_0 = 1 or 2): range 3, step 1, z = 2; w_0 s_0 = 0.25 or
+    0.5 rounds to code 2 (half to even), value 0, error 0.25^2 * 100 = 6.25;
+    -1.5 -> code 0 (value -2) and 1.5 -> code 4 clamped to 3 (value 1) err
+    0.25 each; 0 is exact: total 6.75.
+    alpha = 1 (s_0 = 2^rint(log2 4) = 4): w_0 s_0 = 1.0 is exact (value 1 / 4 =
+    0.25): total 0.5, so alpha_2 = 1.
+    The lone 8-bit channel is a constant group (step 0), which quantizes to 0
+    whatever its scale: equal errors at every grid point keep alpha = 0."""
+    w = np.array([[0.25, -1.5, 10.0, 0.0, 1.5]])
+    x2 = np.array([100.0, 1, 1, 1, 1])
+    m = np.array([4.0, 1, 8, 1, 1])
+    bits = np.array([2, 2, 8, 2, 2])
+    idx = np.array([0, 1, 3, 4])
+    assert ao.block_scale_error(w, x2, idx, np.ones(4), 2) == 6.75
+    assert ao.block_scale_error(w, x2, idx, np.array([2.0, 1, 1, 1]), 2) == 6.75
+    assert ao.block_scale_error(w, x2, idx, np.array([4.0, 1, 1, 1]), 2) == 0.5
+    s, alpha = ao.bit_scaling(w, x2, m, bits, grid=[0.0, 0.5, 1.0])
+    assert s.tolist() == [4.0, 1.0, 1.0, 1.0, 1.0]
+    assert alpha == {2: 1.0, 3: 0.0, 4: 0.0, 8: 0.0, 16: 0.0}
+
+
+def test_scaling_with_uniform_saliency_or_a_zero_grid_is_identity():
+    r = np.random.default_rng(7)
+    w = r.standard_normal((8, 300)) * 0.02
+    x2 = r.uniform(0.1, 5.0, 300)
+    bits = r.choice([2, 3, 4, 8, 16], 300)
+    s, alpha = ao.bit_scaling(w, x2, np.ones(300), bits)
+    assert (s == 1).all() and set(alpha.values()) == {0.0}
+    s, alpha = ao.bit_scaling(w, x2, r.uniform(0.1, 30.0, 300), bits, grid=[0.0])
+    assert (s == 1).all()
+
+
+def test_scaling_on_one_bit_width_is_the_argmin_of_the_eq2_proxy():
+    """With every channel at one bit-width the block's stored grouping is the
+    proxy's (128 consecutive channels in index order), so the chosen alpha is
+    the grid point minimizing sum_j E_b[j] from channel_error (pinned on its
+    own above), the scales are powers of two, and the result is never worse
+    than alpha = 0."""
+    r = np.random.default_rng(8)
+    n, k = 16, 384
+    w = r.standard_normal((n, k)) * 0.02
+    mag = r.uniform(0.5, 1.5, k)
+    mag[r.choice(k, 8, replace=False)] *= 40.0                  # salient channels
+    x2 = mag ** 2
+    m = mag / mag.mean()
+    grid = [0.0, 0.25, 0.5, 0.75, 1.0]
+    for b in (2, 3, 4, 8):
+        s, alpha = ao.bit_scaling(w, x2, m, np.full(k, b), grid=grid)
+        sums = [ao.channel_error(w, x2, np.exp2(np.rint(float(np.float32(a)) * np.log2(m))))[ao.BITS.index(b)].sum()
+                for a in grid]
+        assert alpha[b] == grid[int(np.argmin(sums))]
+        assert np.array_equal(np.log2(s), np.rint(np.log2(s)))
+        assert min(sums) <= sums[0]
+    # at 2 and 3 bits these salient channels make some alpha > 0 pay off
+    assert ao.bit_scaling(w, x2, m, np.full(k, 2), grid=grid)[1][2] > 0
