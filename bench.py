@@ -132,12 +132,15 @@ def build_layer(torch, pq, synth, config, layer=0, mix=None, target_bits=None, m
     lins, groups = synth.make_layer(config, layer=layer, mix=mix, target_bits=target_bits, m=m,
                                     x_dtype=x_dtype or torch.float16, device=dev)
     down_perm = {lin.name: lin.perm for lin in lins}.get("down_proj")
+    # one device copy of each group's input: the linears of a group read the
+    # same x (and, through PackedLinear, the same permutation tensor)
+    xs = {name: grp.x.to(dev) for name, grp in groups.items()}
     out = []
     for lin in lins:
         out_perm = down_perm if emit and lin.name in EMIT_TO_DOWN else None
         pl = pq.PackedLinear(lin.blocks, lin.codes, lin.scales, lin.zeros, lin.perm, device=dev,
                              out_perm=out_perm)
-        out.append((lin.name, pl, groups[lin.group].x.to(dev)))
+        out.append((lin.name, pl, xs[lin.group]))
         lin.codes = lin.scales = lin.zeros = None
     return out
 
@@ -253,7 +256,14 @@ def decode_launches(torch, pq, copies, variant, grouped=True):
     ys = [torch.empty((x.shape[0], pl.n), dtype=torch.float32, device=dev) for _, pl, x in copies[0]]
     pres = [variant in ("P", "S") or (variant == "M" and nm == "down_proj") for nm, _, _ in copies[0]]
     xsc = [channel_factors(torch, pl.k, j) if variant == "X" else None for j, (_, pl, _) in enumerate(copies[0])]
-    xs = [pl.permute(x) if p else x for (_, pl, x), p in zip(copies[0], pres)]
+    clustered = {}   # one clustered copy per (input, permutation), as the library would share
+
+    def cl(pl, x):
+        key = (x.data_ptr(), pl.perm.data_ptr())
+        if key not in clustered:
+            clustered[key] = pl.permute(x)
+        return clustered[key]
+    xs = [cl(pl, x) if p else x for (_, pl, x), p in zip(copies[0], pres)]
     torch.cuda.synchronize()
     sched = schedule(copies[0], grouped)
     workspaces = [None] * len(sched)

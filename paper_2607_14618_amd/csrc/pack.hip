@@ -142,6 +142,7 @@ __global__ __launch_bounds__(kThreads) void permute_kernel(const int32_t* __rest
 // in LDS with 16-byte loads, then gathered there and written with 16-byte
 // stores (k <= kPermLdsK, rows 16-byte aligned).
 constexpr int kPermLdsK = 32768;
+constexpr int kPermLdsMinRows = 64;
 
 __global__ __launch_bounds__(256) void permute_rows_lds_kernel(const int32_t* __restrict__ perm,
                                                                const uint16_t* __restrict__ x,
@@ -195,7 +196,8 @@ __global__ __launch_bounds__(256) void permute_rows_kernel(const int32_t* __rest
 // x'[i][j] = x[i][perm[j]] * f[j] (perm NULL: the identity), f the fp16
 // channel factors of Eq. 8 (1/s_j).  The product is formed in fp32 and
 // rounded to the activation type (fp16, or bf16 when `bf16`), nearest even:
-// exact for a power-of-two factor.  One thread per 8 channels of a row.
+// exact for a power-of-two factor.  One thread per E channels of a row (E = 8
+// for many rows, 1 for a few decode tokens, so that the grid fills the chip).
 __device__ __forceinline__ float act_to_f32(uint16_t h, bool bf16) {
   return bf16 ? __builtin_bit_cast(float, static_cast<uint32_t>(h) << 16)
               : static_cast<float>(__builtin_bit_cast(_Float16, h));
@@ -207,18 +209,19 @@ __device__ __forceinline__ uint16_t f32_to_act(float v, bool bf16) {
   return static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
+template <int E>
 __global__ __launch_bounds__(256) void scale_rows_kernel(const int32_t* __restrict__ perm,
                                                          const uint16_t* __restrict__ f,
                                                          const uint16_t* __restrict__ x,
                                                          uint16_t* __restrict__ out, int m, int k, int bf16) {
-  const int kp = (k + 7) / 8;  // pieces per row
+  const int kp = (k + E - 1) / E;  // pieces per row
   const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (t >= static_cast<int64_t>(m) * kp) return;
-  const int i = static_cast<int>(t / kp), j0 = static_cast<int>(t % kp) * 8;
+  const int i = static_cast<int>(t / kp), j0 = static_cast<int>(t % kp) * E;
   const uint16_t* row = x + static_cast<int64_t>(i) * k;
   uint16_t* dst = out + static_cast<int64_t>(i) * k;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
+  for (int e = 0; e < E; ++e) {
     const int j = j0 + e;
     if (j < k) {
       const int src = perm != nullptr ? perm[j] : j;
@@ -253,7 +256,9 @@ void launch_unpack(const polyq_layout& L, int i, const uint8_t* region, uint16_t
 
 void launch_permute_rows(const int32_t* perm, const uint16_t* x, uint16_t* out, int32_t m, int32_t k,
                          hipStream_t st) {
-  if (k <= kPermLdsK && k % 8 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+  // one work-group per row only when there are enough rows to fill the chip;
+  // a few decode tokens spread one element per thread over the whole chip
+  if (m >= kPermLdsMinRows && k <= kPermLdsK && k % 8 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
       reinterpret_cast<uintptr_t>(perm) % 16 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) {
     hipLaunchKernelGGL(permute_rows_lds_kernel, dim3(static_cast<unsigned>(m)), dim3(256),
                        static_cast<size_t>(k) * 2, st, perm, x, out, k);
@@ -266,9 +271,15 @@ void launch_permute_rows(const int32_t* perm, const uint16_t* x, uint16_t* out, 
 
 void launch_scale_rows(const int32_t* perm, const uint16_t* f, const uint16_t* x, uint16_t* out, int32_t m,
                        int32_t k, bool bf16, hipStream_t st) {
-  const int64_t threads = static_cast<int64_t>(m) * ((k + 7) / 8);
-  hipLaunchKernelGGL(scale_rows_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st,
-                     perm, f, x, out, m, k, bf16 ? 1 : 0);
+  if (m >= kPermLdsMinRows) {
+    const int64_t threads = static_cast<int64_t>(m) * ((k + 7) / 8);
+    hipLaunchKernelGGL(scale_rows_kernel<8>, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st,
+                       perm, f, x, out, m, k, bf16 ? 1 : 0);
+  } else {
+    const int64_t threads = static_cast<int64_t>(m) * k;
+    hipLaunchKernelGGL(scale_rows_kernel<1>, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st,
+                       perm, f, x, out, m, k, bf16 ? 1 : 0);
+  }
 }
 
 }  // namespace polyq

@@ -1,12 +1,33 @@
 """A packed mixed-bit linear layer on one GPU (thin holder around the C ABI)."""
 from __future__ import annotations
 
+import hashlib
+import weakref
 from typing import Optional, Sequence, Tuple
 
 import numpy as np
 import torch
 
 from . import _lib
+
+# Device copies of permutations, one per (device, content): linears that share
+# an input share its permutation (Sec. 4.1 clusters each input once), and a
+# batch whose items have the same x and the same perm pointer stages one
+# clustered copy of x for all of them.
+_PERMS: "weakref.WeakValueDictionary" = weakref.WeakValueDictionary()
+
+
+def device_perm(perm, dev: torch.device) -> torch.Tensor:
+    """The int32 [k] device tensor holding `perm`, shared with every other
+    linear whose permutation has the same content on the same device."""
+    host = np.ascontiguousarray(np.asarray(perm.cpu() if isinstance(perm, torch.Tensor) else perm,
+                                           dtype=np.int32))
+    key = (str(dev), host.size, hashlib.blake2b(host.tobytes(), digest_size=16).hexdigest())
+    t = _PERMS.get(key)
+    if t is None:
+        t = torch.as_tensor(host).to(dev)
+        _PERMS[key] = t
+    return t
 
 
 class PackedLinear:
@@ -34,7 +55,7 @@ class PackedLinear:
             # Eq. 10: output rows stored in a consumer's basis (y'[:, r] = y[:, out_perm[r]])
             row_perm = torch.as_tensor(np.asarray(out_perm, dtype=np.int32)).to(dev).contiguous()
             self.packed = _lib.pack_rows(self.layout, codes, scales, zeros, row_perm)
-        self.perm = torch.as_tensor(np.asarray(perm, dtype=np.int32)).to(dev)
+        self.perm = device_perm(perm, dev)
         # Eq. 8: fp16 [k] factors 1/s_j per clustered channel, applied to x' (weights
         # packed from Q_b(diag(s) W)); None for an unscaled layer
         self.xscale = None if xscale is None else \
