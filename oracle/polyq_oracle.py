@@ -11,7 +11,8 @@ What it computes (fp64, from the *stored* values):
   b <= 8 bits is the group-quantized value  w_hat = s * (q - z)  with the fp16
   scale s and fp16 zero point z of its (row, group); a 16-bit channel is the
   unquantized fp16 weight (the paper sets E_16 = 0: no quantization).
-  Groups have 128 channels and are counted from the start of each block.
+  Groups have g_b channels (Sec. 3.1's per-bit group size; 128 unless given
+  otherwise) and are counted from the start of each block.
 * Eq. 9 (Sec. 4.1):  O = A W = (A P^T)(P W).  Weights are stored clustered
   (input channels permuted into ascending-bit blocks); the activations are
   permuted the same way, x'[m, k'] = x[m, perm[k']].
@@ -35,7 +36,7 @@ distributions (Eq. 7), and hand-computed fixtures under tests/golden/.
 from __future__ import annotations
 
 import math
-from typing import List, Optional, Sequence, Tuple
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -43,13 +44,19 @@ BITS = (2, 3, 4, 8, 16)
 GROUP = 128
 
 Blocks = Sequence[Tuple[int, int]]
+GroupSizes = Optional[Dict[int, int]]     # bit-width -> g_b (absent: 128)
 
 
-def block_table(blocks: Blocks) -> List[Tuple[int, int, int, int]]:
+def group_size(b: int, group_sizes: GroupSizes = None) -> int:
+    """g_b of Sec. 3.1 (Eq. 1): the channels sharing one scale and zero point."""
+    return GROUP if group_sizes is None else int(group_sizes.get(b, GROUP))
+
+
+def block_table(blocks: Blocks, group_sizes: GroupSizes = None) -> List[Tuple[int, int, int, int]]:
     """(bits, k_begin, k_end, first_group) per block; groups only for b <= 8.
 
     Blocks are bit-homogeneous runs of clustered input channels (Sec. 4.1-4.2);
-    each b <= 8 block has ceil(len / 128) quantization groups counted from its
+    each b <= 8 block has ceil(len / g_b) quantization groups counted from its
     start.
     """
     out, k0, g0 = [], 0, 0
@@ -59,12 +66,12 @@ def block_table(blocks: Blocks) -> List[Tuple[int, int, int, int]]:
         out.append((b, k0, k0 + ln, g0))
         k0 += ln
         if b != 16:
-            g0 += -(-ln // GROUP)
+            g0 += -(-ln // group_size(b, group_sizes))
     return out
 
 
-def num_groups(blocks: Blocks) -> int:
-    return sum(-(-ln // GROUP) for b, ln in blocks if b != 16)
+def num_groups(blocks: Blocks, group_sizes: GroupSizes = None) -> int:
+    return sum(-(-ln // group_size(b, group_sizes)) for b, ln in blocks if b != 16)
 
 
 def average_bits(counts: Sequence[Tuple[int, float]]) -> float:
@@ -82,12 +89,12 @@ def fp16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
     return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float64)
 
 
-def dequantize(blocks: Blocks, codes: np.ndarray, scales: np.ndarray, zeros: np.ndarray
-               ) -> np.ndarray:
+def dequantize(blocks: Blocks, codes: np.ndarray, scales: np.ndarray, zeros: np.ndarray,
+               group_sizes: GroupSizes = None) -> np.ndarray:
     """w_hat [n][k] in fp64, clustered channel order.
 
     b <= 8: w_hat[n, k'] = s[n, g] * (q[n, k'] - z[n, g]) with
-    g = first_group(block) + (k' - k_begin(block)) // 128 (group-wise
+    g = first_group(block) + (k' - k_begin(block)) // g_b (group-wise
     quantization at the assigned bit-width, Sec. 3.4).
     b = 16: w_hat[n, k'] = the fp16 value whose bits are stored (unquantized).
     """
@@ -96,12 +103,13 @@ def dequantize(blocks: Blocks, codes: np.ndarray, scales: np.ndarray, zeros: np.
     z = np.asarray(zeros, dtype=np.float16).astype(np.float64)
     n, k = codes.shape
     w = np.empty((n, k), dtype=np.float64)
-    for b, k0, k1, g0 in block_table(blocks):
+    for b, k0, k1, g0 in block_table(blocks, group_sizes):
         if b == 16:
             w[:, k0:k1] = fp16_bits_to_f64(codes[:, k0:k1])
             continue
+        gb = group_size(b, group_sizes)
         for j in range(k0, k1):
-            g = g0 + (j - k0) // GROUP
+            g = g0 + (j - k0) // gb
             w[:, j] = s[:, g] * (codes[:, j].astype(np.float64) - z[:, g])
     return w
 
@@ -117,7 +125,8 @@ def permute_activations(x: np.ndarray, perm: Optional[np.ndarray]) -> np.ndarray
 
 
 def linear(blocks: Blocks, codes, scales, zeros, perm, x, rows: Optional[np.ndarray] = None,
-           chunk: int = 2048, xscale: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+           chunk: int = 2048, xscale: Optional[np.ndarray] = None,
+           group_sizes: GroupSizes = None) -> Tuple[np.ndarray, np.ndarray]:
     """y[m, n] = sum_k' w_hat[n, k'] x'[m, k'] and bound[m, n] = sum_k' |w_hat x'| (fp64).
 
     Sec. 4.2: the per-block products all accumulate into one output; Eq. 9
@@ -143,7 +152,7 @@ def linear(blocks: Blocks, codes, scales, zeros, perm, x, rows: Optional[np.ndar
     for a in range(0, ridx.size, chunk):
         r = ridx[a:a + chunk]
         w = dequantize(blocks, codes[r], scales[r] if scales.size else scales,
-                       zeros[r] if zeros.size else zeros)
+                       zeros[r] if zeros.size else zeros, group_sizes)
         y[:, a:a + r.size] = xp @ w.T
         bound[:, a:a + r.size] = axp @ np.abs(w).T
     return y, bound
@@ -170,7 +179,8 @@ def linear_emitting(blocks: Blocks, codes, scales, zeros, perm, x, out_perm
     return linear(blocks, codes_s, scales_s, zeros_s, perm, x)
 
 
-def linear_scalar(blocks: Blocks, codes, scales, zeros, perm, x) -> np.ndarray:
+def linear_scalar(blocks: Blocks, codes, scales, zeros, perm, x, group_sizes: GroupSizes = None
+                  ) -> np.ndarray:
     """The same product with scalar loops and math.fsum, for tiny layers.
 
     Independent of ``dequantize``/``linear``: it walks the block list element
@@ -192,12 +202,12 @@ def linear_scalar(blocks: Blocks, codes, scales, zeros, perm, x) -> np.ndarray:
                     if b == 16:
                         wv = float(np.uint16(c).view(np.float16))
                     else:
-                        g = gg + t // GROUP
+                        g = gg + t // (group_sizes or {}).get(b, GROUP)
                         wv = float(np.float16(scales[r, g])) * (c - float(np.float16(zeros[r, g])))
                     terms.append(wv * float(xs[mi, j]))
                     kk += 1
                 if b != 16:
-                    gg += -(-ln // GROUP)
+                    gg += -(-ln // (group_sizes or {}).get(b, GROUP))
             y[mi, r] = math.fsum(terms)
     return y
 
@@ -220,6 +230,6 @@ def check_tolerance(y_gpu: np.ndarray, y_ref: np.ndarray, bound: np.ndarray, rel
     return bool(np.all(err <= rel * bound)), worst
 
 
-def effective_weight_bytes(n: int, blocks: Blocks) -> int:
+def effective_weight_bytes(n: int, blocks: Blocks, group_sizes: GroupSizes = None) -> int:
     """Algorithmic bytes one pass must read: codes (fp16 for 16-bit) + fp16 scale and zero."""
-    return code_bits(n, blocks) // 8 + n * num_groups(blocks) * 4
+    return code_bits(n, blocks) // 8 + n * num_groups(blocks, group_sizes) * 4

@@ -7,4 +7,4 @@ from ._lib import (Block, Layout, PolyQError, EXPORTS, LIB_PATH, lib, plan, pack
                    permute, gemv, gemv_batch, gemm, gemm_batch, gemv_workspace_bytes, gemm_workspace_bytes,
                    PreparedBatch, read_probe, channel_error, waterfill, quanta_match, cluster, allocate, bit_scaling,
                    SCALE_GRID)
-from .layer import PackedLinear, decode_batch, prefill_batch  # noqa: F401
+from .layer import PackedLinear, decode_batch, prefill_batch, group_index, device_perm  # noqa: F401

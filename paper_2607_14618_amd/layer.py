@@ -30,6 +30,29 @@ def device_perm(perm, dev: torch.device) -> torch.Tensor:
     return t
 
 
+STORED_GROUP = 128   # channels per stored (scale, zero) pair: the packed layout's group
+
+
+def group_index(blocks: Sequence[Tuple[int, int]], group_sizes=None) -> np.ndarray:
+    """Per-bit group sizes g_b (Sec. 3.1, Eq. 1) in the stored layout: for every
+    stored 128-channel group of a b <= 8 block, the index of the g_b-group whose
+    (scale, zero) it repeats.  g_b must be a multiple of 128, so that no stored
+    group straddles two g_b-groups; a larger g_b is stored as its 128-channel
+    pieces, each carrying the same pair (the metadata bytes are those of
+    g = 128)."""
+    idx, g0 = [], 0
+    for b, ln in blocks:
+        if b == 16:
+            continue
+        gb = int((group_sizes or {}).get(b, STORED_GROUP))
+        if gb < STORED_GROUP or gb % STORED_GROUP != 0:
+            raise ValueError(f"group size {gb} for {b}-bit channels: a multiple of {STORED_GROUP} is required")
+        for i in range(-(-ln // STORED_GROUP)):
+            idx.append(g0 + i * STORED_GROUP // gb)
+        g0 += -(-ln // gb)
+    return np.asarray(idx, dtype=np.int64)
+
+
 class PackedLinear:
     """Clustered, packed weights of one linear plus its channel permutation.
 
@@ -38,17 +61,24 @@ class PackedLinear:
     ``out_perm`` (optional, [n]) stores the output rows in another basis
     (polyq_pack_rows): the layer then emits y[:, out_perm], which is a
     consumer's clustered input when out_perm is that consumer's permutation.
+    ``group_sizes`` ({bits: g_b}, multiples of 128): scales and zeros are given
+    per g_b-group of each block and stored per 128-channel piece
+    (``group_index``).
     """
 
     def __init__(self, blocks: Sequence[Tuple[int, int]], codes: torch.Tensor,
                  scales: torch.Tensor, zeros: torch.Tensor, perm, device="cuda", out_perm=None,
-                 xscale=None):
+                 xscale=None, group_sizes=None):
         n, k = codes.shape
         self.layout = _lib.plan(n, k, blocks)
         dev = torch.device(device)
         codes = codes.to(dev).contiguous()
-        scales = scales.to(dev, torch.float16).contiguous()
-        zeros = zeros.to(dev, torch.float16).contiguous()
+        scales = scales.to(dev, torch.float16)
+        zeros = zeros.to(dev, torch.float16)
+        if group_sizes:
+            gi = torch.as_tensor(group_index(blocks, group_sizes), device=dev)
+            scales, zeros = scales.index_select(1, gi), zeros.index_select(1, gi)
+        scales, zeros = scales.contiguous(), zeros.contiguous()
         if out_perm is None:
             self.packed = _lib.pack(self.layout, codes, scales, zeros)
         else:

@@ -248,15 +248,17 @@ def _fp16_from_f64(a: np.ndarray) -> np.ndarray:
     return np.asarray(a, dtype=np.float64).astype(np.float16)   # direct RNE
 
 
-def quantize_weight(weight: torch.Tensor, blocks: Sequence[Tuple[int, int]], perm: np.ndarray
+def quantize_weight(weight: torch.Tensor, blocks: Sequence[Tuple[int, int]], perm: np.ndarray,
+                    group_sizes: Optional[Dict[int, int]] = None
                     ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """Asymmetric min-max group quantization of an fp32 weight [n][k] (original order).
 
     Returns codes int16 [n][k] (bit patterns of uint16, clustered order),
     scales and zeros fp16 [n][n_groups], on the weight's device.
 
-    Per row and per group of up to 128 clustered channels inside a block of
-    b <= 8 bits: s = fp16_rne((max - min) / (2^b - 1)) computed in fp64,
+    Per row and per group of up to g_b clustered channels inside a block of
+    b <= 8 bits (g_b = group_sizes[b], 128 when absent; groups counted from
+    the block start): s = fp16_rne((max - min) / (2^b - 1)) computed in fp64,
     z = clamp(rint(-min / s), 0, 2^b - 1), q = clamp(rint(w / s) + z, 0, 2^b - 1)
     (rint = round half to even).  A group with s == 0 gets s = 1, z = 0, q = 0.
     16-bit channels store fp16_rne(w).
@@ -265,7 +267,8 @@ def quantize_weight(weight: torch.Tensor, blocks: Sequence[Tuple[int, int]], per
     n, k = weight.shape
     perm_t = torch.as_tensor(perm, dtype=torch.long, device=dev)
     wp = weight.index_select(1, perm_t)
-    n_groups = sum(-(-ln // GROUP) for b, ln in blocks if b != 16)
+    gsz = {b: (group_sizes or {}).get(b, GROUP) for b in BITS}
+    n_groups = sum(-(-ln // gsz[b]) for b, ln in blocks if b != 16)
     codes = torch.empty((n, k), dtype=torch.int16, device=dev)
     scales = np.zeros((n, n_groups), dtype=np.float16)
     zeros = np.zeros((n, n_groups), dtype=np.float16)
@@ -276,8 +279,8 @@ def quantize_weight(weight: torch.Tensor, blocks: Sequence[Tuple[int, int]], per
             k0 += ln
             continue
         qmax = (1 << b) - 1
-        for a in range(k0, k0 + ln, GROUP):
-            e = min(a + GROUP, k0 + ln)
+        for a in range(k0, k0 + ln, gsz[b]):
+            e = min(a + gsz[b], k0 + ln)
             w = wp[:, a:e]
             mn = w.amin(dim=1).double().cpu().numpy()
             mx = w.amax(dim=1).double().cpu().numpy()
@@ -361,6 +364,7 @@ class QuantLinear:
     zeros: torch.Tensor              # fp16 [n][n_groups]
     weight: Optional[torch.Tensor] = None   # fp32 [n][k] original order, if kept
     group: str = ""
+    group_sizes: Optional[Dict[int, int]] = None   # g_b per bit-width (absent: 128)
 
 
 def make_group(config: int, layer: int, name: str, k: int, mix, target_bits, m: int,
@@ -409,9 +413,10 @@ def make_layer(config: int, layer: int = 0, specs: Optional[Sequence[LinearSpec]
 
 
 def random_quant_linear(n: int, k: int, blocks: Sequence[Tuple[int, int]], seed: int,
-                        device="cpu", mode: str = "gauss", identity_perm: bool = False
-                        ) -> QuantLinear:
-    """A small linear with explicit blocks, for tests.
+                        device="cpu", mode: str = "gauss", identity_perm: bool = False,
+                        group_sizes: Optional[Dict[int, int]] = None) -> QuantLinear:
+    """A small linear with explicit blocks, for tests (groups of g_b channels,
+    ``group_sizes``, 128 by default).
 
     mode "gauss": N(0, 0.02^2) weights through the quantizer above.
     mode "codes": uniform random codes in [0, 2^b), random fp16 scales in
@@ -422,12 +427,14 @@ def random_quant_linear(n: int, k: int, blocks: Sequence[Tuple[int, int]], seed:
     if mode == "gauss":
         g = _gen(child_seed(seed, 3), device)
         w = torch.randn((n, k), generator=g, dtype=torch.float32, device=device) * WEIGHT_STD
-        codes, scales, zeros = quantize_weight(w, blocks, perm)
-        return QuantLinear("rand", n, k, list(blocks), perm, codes, scales, zeros, w)
+        codes, scales, zeros = quantize_weight(w, blocks, perm, group_sizes)
+        return QuantLinear("rand", n, k, list(blocks), perm, codes, scales, zeros, w,
+                           group_sizes=group_sizes)
     if mode != "codes":
         raise ValueError(mode)
     rng = np.random.Generator(np.random.PCG64(child_seed(seed, 5)))
-    n_groups = sum(-(-ln // GROUP) for b, ln in blocks if b != 16)
+    gsz = {b: (group_sizes or {}).get(b, GROUP) for b in BITS}
+    n_groups = sum(-(-ln // gsz[b]) for b, ln in blocks if b != 16)
     codes = np.zeros((n, k), dtype=np.uint16)
     scales = np.zeros((n, n_groups), dtype=np.float16)
     zeros = np.zeros((n, n_groups), dtype=np.float16)
@@ -438,11 +445,12 @@ def random_quant_linear(n: int, k: int, blocks: Sequence[Tuple[int, int]], seed:
                 np.float16).view(np.uint16)
         else:
             codes[:, k0:k0 + ln] = rng.integers(0, 1 << b, size=(n, ln), dtype=np.uint16)
-            ng = -(-ln // GROUP)
+            ng = -(-ln // gsz[b])
             scales[:, gi:gi + ng] = np.exp2(rng.uniform(-10, -4, size=(n, ng))).astype(np.float16)
             zeros[:, gi:gi + ng] = rng.integers(0, 1 << b, size=(n, ng)).astype(np.float16)
             gi += ng
         k0 += ln
     return QuantLinear("rand", n, k, list(blocks), perm,
                        torch.from_numpy(codes.view(np.int16)).to(device),
-                       torch.from_numpy(scales).to(device), torch.from_numpy(zeros).to(device))
+                       torch.from_numpy(scales).to(device), torch.from_numpy(zeros).to(device),
+                       group_sizes=group_sizes)

@@ -21,7 +21,7 @@ def np_(t):
 
 def packed_linear(lin) -> pq.PackedLinear:
     return pq.PackedLinear(lin.blocks, lin.codes.to(dev()), lin.scales, lin.zeros, lin.perm,
-                           device=dev())
+                           device=dev(), group_sizes=getattr(lin, "group_sizes", None))
 
 
 def oracle_ref(lin, x, rows=None, pre_permuted=False, xscale=None):
@@ -29,7 +29,8 @@ def oracle_ref(lin, x, rows=None, pre_permuted=False, xscale=None):
     perm = None if pre_permuted else lin.perm
     return oracle.linear(lin.blocks, codes, np_(lin.scales), np_(lin.zeros), perm,
                          np_(x.float()), rows=rows,
-                         xscale=None if xscale is None else np_(xscale).astype(np.float64))
+                         xscale=None if xscale is None else np_(xscale).astype(np.float64),
+                         group_sizes=getattr(lin, "group_sizes", None))
 
 
 def assert_parity(y_gpu, y_ref, bound, what=""):

@@ -387,3 +387,72 @@ def test_symmetric_quantizer_is_the_zero_point_special_case():
             assert np.all(np.abs(w_hat[:, a:e] - wp[:, a:e]) <= 0.5 * sg * (1 + 1e-3) + 1e-12)
             g += 1
         k0 += ln
+
+
+# ----------------------------------------------------------------- per-bit group size g_b
+def test_group_size_hand_example():
+    """One row, one 2-bit block of 384 channels, g_2 = 256: groups [0, 256) and
+    [256, 384).  Codes 1, x = 1: y = 256 s0 (1 - z0) + 128 s1 (1 - z1) with
+    (s0, z0) = (0.5, 0), (s1, z1) = (0.25, 3): 128 - 64 = 64; bound 128 + 64."""
+    blocks = [(2, 384)]
+    codes = np.ones((1, 384), np.uint16)
+    s = np.array([[0.5, 0.25]], np.float16)
+    z = np.array([[0.0, 3.0]], np.float16)
+    x = np.ones((1, 384), np.float16)
+    y, bound = oracle.linear(blocks, codes, s, z, None, x, group_sizes={2: 256})
+    assert y[0, 0] == 64.0 and bound[0, 0] == 192.0
+    assert oracle.num_groups(blocks, {2: 256}) == 2 and oracle.num_groups(blocks) == 3
+    assert oracle.linear_scalar(blocks, codes, s, z, None, x, group_sizes={2: 256})[0, 0] == 64.0
+
+
+@pytest.mark.parametrize("gs", [{2: 256, 3: 512, 8: 384}, {4: 1024, 8: 128}, {2: 64, 3: 32}])
+def test_larger_groups_are_repeated_pairs_of_smaller_groups(gs):
+    """A g_b-group equals g_b / g consecutive g-groups carrying the same (s, z):
+    the g_b layout dequantizes like the 128-channel (or, for g_b < 128, the
+    g_b-channel) layout with every pair repeated, built here channel by channel."""
+    blocks = [(2, 640), (3, 544), (4, 1152), (8, 96), (16, 32)]
+    k = sum(l for _, l in blocks)
+    lin = random_quant_linear(6, k, blocks, seed=41, mode="codes", group_sizes=gs)
+    codes = lin.codes.numpy().view(np.uint16)
+    w_g = oracle.dequantize(blocks, codes, lin.scales.numpy(), lin.zeros.numpy(), gs)
+    # per-channel (s, z) from the compact arrays, then one "group" per channel
+    s_ch, z_ch = [], []
+    g0 = 0
+    for b, ln in blocks:
+        if b == 16:
+            continue
+        gb = gs.get(b, 128)
+        for t in range(ln):
+            s_ch.append(lin.scales.numpy()[:, g0 + t // gb])
+            z_ch.append(lin.zeros.numpy()[:, g0 + t // gb])
+        g0 += -(-ln // gb)
+    s_ch, z_ch = np.stack(s_ch, 1), np.stack(z_ch, 1)
+    ones = {b: 1 for b in (2, 3, 4, 8)}
+    w_1 = oracle.dequantize(blocks, codes, s_ch, z_ch, ones)
+    assert np.array_equal(w_g, w_1)
+    x = np.random.default_rng(3).standard_normal((2, k)).astype(np.float16)
+    y, _ = oracle.linear(blocks, codes, lin.scales.numpy(), lin.zeros.numpy(), lin.perm, x, group_sizes=gs)
+    ys = oracle.linear_scalar(blocks, codes, lin.scales.numpy(), lin.zeros.numpy(), lin.perm, x, group_sizes=gs)
+    np.testing.assert_allclose(y, ys, rtol=1e-12, atol=1e-15)
+
+
+def test_group_size_quantizer_error_bound():
+    """Against the fp32 weights: with g_b = 512 every weight is within 1.5 s of
+    its own 512-channel group (s from that group's range), and the stored
+    arrays have ceil(len / g_b) columns per block."""
+    blocks = [(2, 1024), (4, 640), (16, 32)]
+    k = sum(l for _, l in blocks)
+    gs = {2: 512, 4: 256}
+    lin = random_quant_linear(5, k, blocks, seed=43, mode="gauss", group_sizes=gs)
+    assert lin.scales.shape == (5, 2 + 3)
+    w = oracle.dequantize(blocks, lin.codes.numpy(), lin.scales.numpy(), lin.zeros.numpy(), gs)
+    wp = lin.weight.numpy().astype(np.float64)[:, lin.perm]
+    k0 = 0
+    for b, ln in blocks:
+        if b != 16:
+            gb = gs[b]
+            for a in range(k0, k0 + ln, gb):
+                e = min(a + gb, k0 + ln)
+                s = (wp[:, a:e].max(1) - wp[:, a:e].min(1)) / ((1 << b) - 1)
+                assert (np.abs(w[:, a:e] - wp[:, a:e]) <= 1.5 * s[:, None] * (1 + 1e-3)).all()
+        k0 += ln
