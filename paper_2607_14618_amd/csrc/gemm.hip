@@ -52,7 +52,7 @@ typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 constexpr int kTokWG = 256;                 // tokens per work-group
 constexpr int kRowsWG = 2 * kTileRows;      // weight rows per work-group (two packed tiles)
 constexpr int kThreads = 512;               // 8 waves
-constexpr int kLdsRow = 40;                 // bf16 per LDS row: 32 channels + 8 pad against bank conflicts
+constexpr int kLdsRow = 48;                 // bf16 per LDS row: 32 channels + 16 pad (96-byte rows: fewest bank conflicts measured among 16-byte-aligned strides)
 constexpr int kStageA = kTokWG * kLdsRow;   // bf16 of one activation stage
 constexpr int kStageB = kRowsWG * kLdsRow;  // bf16 of one weight tile (hi or lo) of a stage
 
