@@ -269,9 +269,60 @@ void launch_permute_rows(const int32_t* perm, const uint16_t* x, uint16_t* out, 
   }
 }
 
+// The same for many rows: one token row per work-group, staged in LDS with
+// 16-byte loads (k <= kPermLdsK, k % 8 == 0, 16-byte aligned rows, factors and
+// permutation), then 8 channels per thread: the permutation and factors as
+// 16-byte loads, one 16-byte store.
+template <bool HasPerm>
+__global__ __launch_bounds__(256) void scale_rows_lds_kernel(const int32_t* __restrict__ perm,
+                                                             const uint16_t* __restrict__ f,
+                                                             const uint16_t* __restrict__ x,
+                                                             uint16_t* __restrict__ out, int k, int bf16) {
+  extern __shared__ uint4 row4[];
+  const uint16_t* row = reinterpret_cast<const uint16_t*>(row4);
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * k;
+  const uint4* src = reinterpret_cast<const uint4*>(x + base);
+  for (int j = threadIdx.x; j < k / 8; j += 256) row4[j] = src[j];
+  __syncthreads();
+  const int4* p4 = reinterpret_cast<const int4*>(perm);
+  const uint4* f4 = reinterpret_cast<const uint4*>(f);
+  uint4* dst = reinterpret_cast<uint4*>(out + base);
+  for (int j = threadIdx.x; j < k / 8; j += 256) {
+    int p[8];
+    if constexpr (HasPerm) {
+      const int4 a = p4[2 * j], b = p4[2 * j + 1];
+      p[0] = a.x; p[1] = a.y; p[2] = a.z; p[3] = a.w; p[4] = b.x; p[5] = b.y; p[6] = b.z; p[7] = b.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) p[e] = 8 * j + e;
+    }
+    const uint4 fv = f4[j];
+    const uint32_t fw[4] = {fv.x, fv.y, fv.z, fv.w};
+    uint32_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float v = static_cast<unsigned>(p[e]) < static_cast<unsigned>(k) ? act_to_f32(row[p[e]], bf16 != 0) : 0.f;
+      const float fj = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(fw[e / 2] >> (16 * (e & 1)))));
+      h[e] = f32_to_act(v * fj, bf16 != 0);
+    }
+    dst[j] = uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+  }
+}
+
 void launch_scale_rows(const int32_t* perm, const uint16_t* f, const uint16_t* x, uint16_t* out, int32_t m,
                        int32_t k, bool bf16, hipStream_t st) {
-  if (m >= kPermLdsMinRows) {
+  const bool lds = m >= kPermLdsMinRows && k <= kPermLdsK && k % 8 == 0 &&
+                   reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(f) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(perm) % 16 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0;
+  if (lds) {
+    const size_t shm = static_cast<size_t>(k) * 2;
+    if (perm != nullptr)
+      hipLaunchKernelGGL(scale_rows_lds_kernel<true>, dim3(static_cast<unsigned>(m)), dim3(256), shm, st, perm, f, x,
+                         out, k, bf16 ? 1 : 0);
+    else
+      hipLaunchKernelGGL(scale_rows_lds_kernel<false>, dim3(static_cast<unsigned>(m)), dim3(256), shm, st, perm, f,
+                         x, out, k, bf16 ? 1 : 0);
+  } else if (m >= kPermLdsMinRows) {
     const int64_t threads = static_cast<int64_t>(m) * ((k + 7) / 8);
     hipLaunchKernelGGL(scale_rows_kernel<8>, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st,
                        perm, f, x, out, m, k, bf16 ? 1 : 0);
