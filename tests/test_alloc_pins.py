@@ -281,3 +281,25 @@ def test_scaling_on_one_bit_width_is_the_argmin_of_the_eq2_proxy():
         assert min(sums) <= sums[0]
     # at 2 and 3 bits these salient channels make some alpha > 0 pay off
     assert ao.bit_scaling(w, x2, m, np.full(k, 2), grid=grid)[1][2] > 0
+
+
+def test_scaling_error_is_the_eq2_proxy_on_the_blocks_own_columns():
+    """With bit-widths interleaved (2, 3, 2, 3, ...), a block's error is the Eq. 2
+    proxy (channel_error, pinned above) of the block's columns taken out in
+    index order, so that its groups are the 128 consecutive channels of the
+    stored block, not 128-channel windows of the original order."""
+    r = np.random.default_rng(9)
+    n, k = 4, 1024
+    w = r.standard_normal((n, k)) * 0.02
+    w[:, :256] *= 30.0                        # a wide first window in the original order
+    x2 = r.uniform(0.5, 2.0, k)
+    bits = np.where(np.arange(k) % 2 == 0, 2, 3)
+    s = np.exp2(r.integers(-1, 3, k)).astype(np.float64)
+    for b in (2, 3):
+        idx = np.nonzero(bits == b)[0]
+        got = ao.block_scale_error(w, x2, idx, s[idx], b)
+        ref = ao.channel_error(w[:, idx], x2[idx], s[idx])[ao.BITS.index(b)].sum()
+        assert got == pytest.approx(ref, rel=1e-12)
+        # the original-order windows give a different number here
+        wrong = ao.channel_error(w, x2, s)[ao.BITS.index(b)][idx].sum()
+        assert abs(wrong - ref) > 1e-3 * ref
