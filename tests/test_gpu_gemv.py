@@ -243,6 +243,26 @@ def test_gemv_config4_qwen3_32b_layers(layer):
         assert_parity(yy, y_ref, bound, f"config 4 layer {layer} {lin.name}")
 
 
+@pytest.mark.parametrize("first", [0, 16, 32, 48])
+def test_gemv_config4_every_layer_sampled_rows(first):
+    """Qwen3-32B stack, layers first .. first + 15 of 64: 256 seeded rows of every
+    linear (gathered activations) against the oracle."""
+    for layer in range(first, first + 16):
+        lins, groups = make_layer(4, layer=layer, device=dev())
+        rng = np.random.default_rng(1000 + layer)
+        for lin in lins:
+            x = groups[lin.group].x
+            pl = packed_linear(lin)
+            y = pl.decode(x.to(dev()))
+            torch.cuda.synchronize()
+            rows = np.sort(rng.choice(lin.n, 256, replace=False))
+            y_ref, bound = oracle_ref(lin, x, rows=rows)
+            assert_parity(np_(y)[:, rows], y_ref, bound, f"config 4 layer {layer} {lin.name}")
+            del pl
+        del lins, groups
+        torch.cuda.empty_cache()
+
+
 def test_gemv_capacity_errors():
     lin = random_quant_linear(64, 64, [(2, 64)], seed=1, mode="codes")
     pl = packed_linear(lin)
