@@ -408,7 +408,8 @@ polyq_status polyq_cluster(const int32_t* bits, int32_t k, int32_t* perm, polyq_
  * Eq. 8), run after the bit map is fixed: for every bit-width b <= 8 present,
  * one exponent alpha_b from `grid` (values in [0, 1]) for all its channels,
  * s_j = 2^rint(alpha_b log2 m_j) (Eq. 8's power law kept to powers of two,
- * so that the runtime fold of 1/s_j into x' is exact), chosen to minimize the
+ * so that the runtime fold of 1/s_j into x' is exact; the exponent is clamped
+ * to [-14, 14], so that 1/s_j is a normal fp16 value), chosen to minimize the
  * block's proxy error sum_j E_b[j] (Eq. 2, x2 weights) with W~ =
  * diag(s)^-1 Q_b(diag(s) W) and Q_b applied as deployed: to the block's
  * channels in ascending index order, groups of 128 per row.  Ties keep the

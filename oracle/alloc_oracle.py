@@ -34,12 +34,13 @@ What it computes (fp64, NumPy; Sec. 3.1-3.4 of the paper):
 * Eq. 8 (Sec. 3.4): bit-specific activation-aware scaling, after the bit map
   is fixed: one exponent alpha_b per bit-width b <= 8 from a grid in [0, 1],
   s_j = 2^rint(alpha_b log2 m_j) for the channels of bit-width b (the power
-  law m_j^alpha_b kept to powers of two), alpha_b minimizing the block's
-  summed proxy error sum_j E_b[j] with Q_b applied as the block is stored: to
-  the block's channels in ascending index order, 128 per group; ties keep the
-  earlier grid point; 16-bit channels keep s = 1.
+  law m_j^alpha_b kept to powers of two, the exponent clamped to [-14, 14]),
+  alpha_b minimizing the block's summed proxy error sum_j E_b[j] with Q_b
+  applied as the block is stored: to the block's channels in ascending index
+  order, 128 per group; ties keep the earlier grid point; 16-bit channels keep
+  s = 1.
 
-Readings where the paper is silent (listed in the design doc): the proxy's groups
+Readings where the paper is silent: the proxy's groups
 run along the input channels in original order; ties in the heap go to the
 lower channel index; a candidate that does not fit the remaining budget is
 dropped (the budget only shrinks); the rounding and repair rules of the
@@ -246,6 +247,7 @@ def allocate(w: np.ndarray, x2: np.ndarray, budget: float, quantum: int,
 
 # --------------------------------------------------------------------------- Eq. 8
 SCALE_GRID = tuple(i / 10 for i in range(11))
+SCALE_EXP = 14      # |log2 s| at most 14: the factor 1/s is then a normal fp16 value
 
 
 def block_scale_error(w: np.ndarray, x2: np.ndarray, idx: np.ndarray, s: np.ndarray, b: int) -> float:
@@ -273,7 +275,7 @@ def bit_scaling(w: np.ndarray, x2: np.ndarray, saliency: np.ndarray, bits: np.nd
         best = math.inf
         for a in grid:
             a = float(np.float32(a))
-            sb = np.exp2(np.rint(a * np.log2(m[idx])))
+            sb = np.exp2(np.clip(np.rint(a * np.log2(m[idx])), -SCALE_EXP, SCALE_EXP))
             e = block_scale_error(w, x2, idx, sb, b)
             if e < best:
                 best, alpha[b], s[idx] = e, a, sb

@@ -17,6 +17,7 @@ namespace {
 
 constexpr int kBits[POLYQ_NUM_BITS] = {2, 3, 4, 8, 16};
 constexpr int kProxyGroup = 128;  // input channels per quantization group of the proxy
+constexpr int kScaleExp = 14;     // |log2 s| of the Eq. 8 scales: 1/s stays a normal fp16 value
 
 int bit_index(int b) {
   for (int i = 0; i < POLYQ_NUM_BITS; ++i)
@@ -279,9 +280,13 @@ extern "C" polyq_status polyq_bit_scaling(const float* w, int32_t n, int32_t k, 
     s.assign(cnt, 1.0);
     double best = INFINITY;
     for (int32_t g = 0; g < ngrid; ++g) {
-      // s_j = 2^rint(alpha log2 m_j): Eq. 8's power law, kept to powers of two
-      for (int32_t t = 0; t < cnt; ++t)
-        s[t] = ldexp(1.0, static_cast<int>(rint(static_cast<double>(grid[g]) * log2(saliency[idx[t]]))));
+      // s_j = 2^rint(alpha log2 m_j): Eq. 8's power law, kept to powers of two,
+      // the exponent clamped to [-kScaleExp, kScaleExp] so that 1/s_j is a
+      // normal fp16 value
+      for (int32_t t = 0; t < cnt; ++t) {
+        const double e = rint(static_cast<double>(grid[g]) * log2(saliency[idx[t]]));
+        s[t] = ldexp(1.0, static_cast<int>(std::min(std::max(e, -1.0 * kScaleExp), 1.0 * kScaleExp)));
+      }
       const double e = block_error(w, n, k, x2, idx.data(), cnt, s.data(), bi);
       if (e < best) {  // ties keep the earlier grid point
         best = e;

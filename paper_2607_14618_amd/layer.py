@@ -19,7 +19,8 @@ _PERMS: "weakref.WeakValueDictionary" = weakref.WeakValueDictionary()
 
 def device_perm(perm, dev: torch.device) -> torch.Tensor:
     """The int32 [k] device tensor holding `perm`, shared with every other
-    linear whose permutation has the same content on the same device."""
+    linear whose permutation has the same content on the same device (so it
+    must not be modified in place)."""
     host = np.ascontiguousarray(np.asarray(perm.cpu() if isinstance(perm, torch.Tensor) else perm,
                                            dtype=np.int32))
     key = (str(dev), host.size, hashlib.blake2b(host.tobytes(), digest_size=16).hexdigest())

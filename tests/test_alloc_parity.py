@@ -112,6 +112,14 @@ def test_bit_scaling_matches_the_oracle(n, k, seed):
     assert any(a > 0 for a in alpha.values())
 
 
+def test_bit_scaling_clamps_the_exponent_like_the_oracle():
+    w = np.array([[0.5, -0.25, 0.125, 1.0]], dtype=np.float32)
+    m = np.array([2.0 ** -40, 2.0 ** 40, 1.0, 8.0])
+    s, _ = pq.bit_scaling(w, np.ones(4), m, [2, 2, 2, 2], grid=[1.0])
+    rs, _ = ao.bit_scaling(w.astype(np.float64), np.ones(4), m, np.array([2, 2, 2, 2]), grid=[1.0])
+    assert np.array_equal(s.astype(np.float64), rs) and s.tolist() == [2.0 ** -14, 2.0 ** 14, 1.0, 8.0]
+
+
 def test_bit_scaling_hand_example_matches():
     w = np.array([[0.25, -1.5, 10.0, 0.0, 1.5]], dtype=np.float32)
     s, alpha = pq.bit_scaling(w, np.array([100.0, 1, 1, 1, 1]), np.array([4.0, 1, 8, 1, 1]),

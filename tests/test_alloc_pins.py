@@ -303,3 +303,13 @@ def test_scaling_error_is_the_eq2_proxy_on_the_blocks_own_columns():
         # the original-order windows give a different number here
         wrong = ao.channel_error(w, x2, s)[ao.BITS.index(b)][idx].sum()
         assert abs(wrong - ref) > 1e-3 * ref
+
+
+def test_scaling_exponent_is_clamped_to_normal_fp16_factors():
+    """Saliencies of 2^-40 and 2^40 at alpha = 1 would give scales 2^-40 and
+    2^40; the exponent stops at -14 and 14, so that 1/s is a normal fp16."""
+    w = np.array([[0.5, -0.25, 0.125, 1.0]])
+    s, alpha = ao.bit_scaling(w, np.ones(4), np.array([2.0 ** -40, 2.0 ** 40, 1.0, 8.0]),
+                              np.array([2, 2, 2, 2]), grid=[1.0])
+    assert s.tolist() == [2.0 ** -14, 2.0 ** 14, 1.0, 8.0] and alpha[2] == 1.0
+    assert np.all(np.isfinite((1.0 / s).astype(np.float16))) and (1.0 / s).min() >= 2.0 ** -14
