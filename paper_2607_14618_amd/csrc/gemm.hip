@@ -690,23 +690,25 @@ extern "C" polyq_status polyq_gemm_batch(const polyq_gemm_item* items, int32_t c
     if (wg > 0x7FFFFFFF) return POLYQ_ERR_CAPACITY;
   }
   for (int i = count; i <= POLYQ_MAX_BATCH; ++i) a.wg_begin[i] = static_cast<int32_t>(wg);
-  // Permuted copies (one per distinct (x, perm)), then the products.
+  // Permuted copies (one per distinct (x, perm, factors), all in one launch),
+  // then the products.
+  ShuffleJob jobs[POLYQ_MAX_BATCH];
+  int njobs = 0;
+  for (int i = 0; i < count; ++i) {
+    if (region[i] < 0) continue;
+    bool first = true;
+    for (int j = 0; j < i; ++j) first = first && region[j] != region[i];
+    if (first)
+      jobs[njobs++] = ShuffleJob{items[i].perm, items[i].xscale, items[i].x,
+                                 reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(workspace) + region[i]),
+                                 items[i].layout->k, 0};
+  }
+  launch_shuffle(jobs, njobs, m, true, st);
   for (int i = 0; i < count; ++i) {
     const polyq_gemv_item& itm = items[i];
     const polyq_layout& L = *itm.layout;
     const uint16_t* xp = itm.x;
-    if (region[i] >= 0) {
-      uint16_t* out = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(workspace) + region[i]);
-      bool first = true;
-      for (int j = 0; j < i; ++j) first = first && region[j] != region[i];
-      if (first) {
-        if (itm.xscale != nullptr)
-          launch_scale_rows(itm.perm, itm.xscale, itm.x, out, m, L.k, true, st);
-        else
-          launch_permute_rows(itm.perm, itm.x, out, m, L.k, st);
-      }
-      xp = out;
-    }
+    if (region[i] >= 0) xp = reinterpret_cast<const uint16_t*>(static_cast<uint8_t*>(workspace) + region[i]);
     GemmItem& g = a.item[i];
     g.packed = static_cast<const uint8_t*>(itm.packed);
     g.x = xp;

@@ -1062,14 +1062,13 @@ extern "C" polyq_status polyq_gemv_batch(const polyq_gemv_item* items, int32_t c
   hipStream_t hs = static_cast<hipStream_t>(stream);
   // Eq. 9's explicit shuffle first (with Eq. 8's factors folded in), once per
   // distinct (x, perm, factors) of several tokens
-  for (int i = 0; i < count; ++i) {
-    if (!bp.xp_first[i]) continue;
-    uint16_t* xp = reinterpret_cast<uint16_t*>(ws + bp.xp_off[i]);
-    if (items[i].xscale != nullptr)
-      launch_scale_rows(items[i].perm, items[i].xscale, items[i].x, xp, m, items[i].layout->k, false, hs);
-    else
-      launch_permute_rows(items[i].perm, items[i].x, xp, m, items[i].layout->k, hs);
-  }
+  ShuffleJob jobs[kMaxItems];
+  int njobs = 0;
+  for (int i = 0; i < count; ++i)
+    if (bp.xp_first[i])
+      jobs[njobs++] = ShuffleJob{items[i].perm, items[i].xscale, items[i].x,
+                                 reinterpret_cast<uint16_t*>(ws + bp.xp_off[i]), items[i].layout->k, 0};
+  launch_shuffle(jobs, njobs, m, false, hs);
   hipLaunchKernelGGL(gemv_kernel, dim3(wgs, count), dim3(kWaves * 64), bp.lds, hs, a);
   return hipGetLastError() == hipSuccess ? POLYQ_OK : POLYQ_ERR_DEVICE;
 }

@@ -102,19 +102,23 @@ size_t gemv_lds_bytes(const GemvPlan& p, int32_t m);
 polyq_status gemv_batch_workspace_status(const polyq_gemv_item* items, int32_t count, int32_t m,
                                          size_t* need, size_t* zero);
 
-// Explicit activation shuffle out[i][j] = x[i][perm[j]] (Eq. 9) for m rows of
-// k 2-byte values on `stream` (an entry outside [0, k) yields 0); rows are
-// staged in LDS when k and the alignments allow.  Launch only: the caller has
-// validated the arguments.
-void launch_permute_rows(const int32_t* perm, const uint16_t* x, uint16_t* out, int32_t m, int32_t k,
-                         hipStream_t stream);
-
-// x'[i][j] = x[i][perm[j]] * f[j] for m rows of k 2-byte activations (fp16,
-// or bf16 when `bf16`); perm may be NULL (identity), an entry outside [0, k)
-// yields 0; f: fp16 channel factors (Eq. 8's 1/s_j), the product rounded to the
-// activation type.  Launch only: the caller has validated the arguments.
-void launch_scale_rows(const int32_t* perm, const uint16_t* f, const uint16_t* x, uint16_t* out, int32_t m,
-                       int32_t k, bool bf16, hipStream_t stream);
+// One copy of the explicit activation shuffle (Eq. 9, with Eq. 8's channel
+// factors): out[i][j] = x[i][perm[j]] * f[j] for m rows of k 2-byte
+// activations.  perm NULL: the identity; an entry outside [0, k) yields 0;
+// f NULL: no factors (the values are copied bit for bit); otherwise fp16
+// factors, the product rounded to the activation type.
+struct ShuffleJob {
+  const int32_t* perm;
+  const uint16_t* f;
+  const uint16_t* x;
+  uint16_t* out;
+  int32_t k, pad;
+};
+// All `count` (<= POLYQ_MAX_BATCH) copies in one launch on `stream` (fp16
+// activations, or bf16 when `bf16`); rows are staged in LDS when there are
+// many and k and the alignments allow.  Launch only: the caller has validated
+// the arguments.
+void launch_shuffle(const ShuffleJob* jobs, int count, int32_t m, bool bf16, hipStream_t stream);
 
 // Block accessor of a layout for wave_range (host side).
 struct LayoutBlocks {

@@ -138,66 +138,20 @@ __global__ __launch_bounds__(kThreads) void permute_kernel(const int32_t* __rest
   out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
 }
 
-// x'[i][j] = x[i][perm[j]] for one token row per work-group: the row is staged
-// in LDS with 16-byte loads, then gathered there and written with 16-byte
-// stores (k <= kPermLdsK, rows 16-byte aligned).
-constexpr int kPermLdsK = 32768;
+// The explicit shuffle x'[i][j] = x[i][perm[j]] * f[j] of several copies in one
+// launch (grid.y = copy).  perm NULL: the identity; an entry outside [0, k)
+// yields 0; f NULL: no factors, the 2-byte values are copied as they are;
+// otherwise f holds Eq. 8's fp16 channel factors 1/s_j and the product is
+// formed in fp32 and rounded (nearest even) to the activation type (fp16, or
+// bf16 when `bf16`): exact for a power-of-two factor.
+constexpr int kPermLdsK = 32768;   // longest row staged in LDS
 constexpr int kPermLdsMinRows = 64;
 
-__global__ __launch_bounds__(256) void permute_rows_lds_kernel(const int32_t* __restrict__ perm,
-                                                               const uint16_t* __restrict__ x,
-                                                               uint16_t* __restrict__ out, int k) {
-  extern __shared__ uint4 row4[];
-  const uint16_t* row = reinterpret_cast<const uint16_t*>(row4);
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * k;
-  const uint4* src = reinterpret_cast<const uint4*>(x + base);
-  const int4* p4 = reinterpret_cast<const int4*>(perm);
-  // The indices of the first kPre passes are loaded together with the row (one
-  // memory round trip for both).
-  constexpr int kPre = 4;
-  int4 pp[kPre][2];
-#pragma unroll
-  for (int u = 0; u < kPre; ++u) {
-    const int j = threadIdx.x + u * 256;
-    if (j < k / 8) {
-      pp[u][0] = p4[2 * j];
-      pp[u][1] = p4[2 * j + 1];
-    }
-  }
-  for (int j = threadIdx.x; j < k / 8; j += 256) row4[j] = src[j];
-  __syncthreads();
-  uint4* dst = reinterpret_cast<uint4*>(out + base);
-  auto gather = [&](int j, int4 p0, int4 p1) {
-    const int p[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-    uint32_t h[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) h[e] = static_cast<unsigned>(p[e]) < static_cast<unsigned>(k) ? row[p[e]] : 0u;
-    dst[j] = uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
-  };
-#pragma unroll
-  for (int u = 0; u < kPre; ++u) {
-    const int j = threadIdx.x + u * 256;
-    if (j < k / 8) gather(j, pp[u][0], pp[u][1]);
-  }
-  for (int j = threadIdx.x + kPre * 256; j < k / 8; j += 256) gather(j, p4[2 * j], p4[2 * j + 1]);
-}
+struct ShuffleArgs {
+  ShuffleJob job[POLYQ_MAX_BATCH];
+  int32_t m, bf16;
+};
 
-// Fallback gather, one element per thread (any k, any alignment).
-__global__ __launch_bounds__(256) void permute_rows_kernel(const int32_t* __restrict__ perm,
-                                                           const uint16_t* __restrict__ x,
-                                                           uint16_t* __restrict__ out, int m, int k) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (idx >= static_cast<int64_t>(m) * k) return;
-  const int i = static_cast<int>(idx / k), kp = static_cast<int>(idx % k);
-  const int p = perm[kp];
-  out[idx] = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? x[static_cast<int64_t>(i) * k + p] : 0;
-}
-
-// x'[i][j] = x[i][perm[j]] * f[j] (perm NULL: the identity), f the fp16
-// channel factors of Eq. 8 (1/s_j).  The product is formed in fp32 and
-// rounded to the activation type (fp16, or bf16 when `bf16`), nearest even:
-// exact for a power-of-two factor.  One thread per E channels of a row (E = 8
-// for many rows, 1 for a few decode tokens, so that the grid fills the chip).
 __device__ __forceinline__ float act_to_f32(uint16_t h, bool bf16) {
   return bf16 ? __builtin_bit_cast(float, static_cast<uint32_t>(h) << 16)
               : static_cast<float>(__builtin_bit_cast(_Float16, h));
@@ -208,28 +162,80 @@ __device__ __forceinline__ uint16_t f32_to_act(float v, bool bf16) {
   if ((u & 0x7FFFFFFFu) > 0x7F800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);  // NaN stays NaN
   return static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
+__device__ __forceinline__ uint16_t scaled(uint16_t v, uint16_t f, bool bf16) {
+  return f32_to_act(act_to_f32(v, bf16) * static_cast<float>(__builtin_bit_cast(_Float16, f)), bf16);
+}
 
-template <int E>
-__global__ __launch_bounds__(256) void scale_rows_kernel(const int32_t* __restrict__ perm,
-                                                         const uint16_t* __restrict__ f,
-                                                         const uint16_t* __restrict__ x,
-                                                         uint16_t* __restrict__ out, int m, int k, int bf16) {
-  const int kp = (k + E - 1) / E;  // pieces per row
-  const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (t >= static_cast<int64_t>(m) * kp) return;
-  const int i = static_cast<int>(t / kp), j0 = static_cast<int>(t % kp) * E;
-  const uint16_t* row = x + static_cast<int64_t>(i) * k;
-  uint16_t* dst = out + static_cast<int64_t>(i) * k;
+// A few rows (decode tokens): one element per thread, spread over the chip.
+__global__ __launch_bounds__(256) void shuffle_elems_kernel(const ShuffleArgs a) {
+  const ShuffleJob& jb = a.job[blockIdx.y];
+  const int k = jb.k;
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (idx >= static_cast<int64_t>(a.m) * k) return;
+  const int i = static_cast<int>(idx / k), j = static_cast<int>(idx % k);
+  const int p = jb.perm != nullptr ? jb.perm[j] : j;
+  uint16_t v = static_cast<unsigned>(p) < static_cast<unsigned>(k) ? jb.x[static_cast<int64_t>(i) * k + p] : 0;
+  if (jb.f != nullptr) v = scaled(v, jb.f[j], a.bf16 != 0);
+  jb.out[idx] = v;
+}
+
+// Many rows (prefill): one row per work-group, staged in LDS with 16-byte loads
+// (k <= kPermLdsK, k % 8 == 0, 16-byte aligned rows, permutation and
+// factors), then 8 channels per thread and pass: the permutation and factors
+// as 16-byte loads, one 16-byte store.  The indices and factors of the first
+// kPre passes are loaded together with the row (one memory round trip).
+__global__ __launch_bounds__(256) void shuffle_rows_lds_kernel(const ShuffleArgs a) {
+  extern __shared__ uint4 row4[];
+  const ShuffleJob& jb = a.job[blockIdx.y];
+  const int k = jb.k, k8 = k / 8;
+  const bool has_perm = jb.perm != nullptr, has_f = jb.f != nullptr, bf16 = a.bf16 != 0;
+  const uint16_t* row = reinterpret_cast<const uint16_t*>(row4);
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * k;
+  const uint4* src = reinterpret_cast<const uint4*>(jb.x + base);
+  const int4* p4 = reinterpret_cast<const int4*>(jb.perm);
+  const uint4* f4 = reinterpret_cast<const uint4*>(jb.f);
+  constexpr int kPre = 4;
+  int4 pp[kPre][2];
+  uint4 ff[kPre];
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int j = j0 + e;
-    if (j < k) {
-      const int src = perm != nullptr ? perm[j] : j;
-      const float v = static_cast<unsigned>(src) < static_cast<unsigned>(k) ? act_to_f32(row[src], bf16 != 0) : 0.f;
-      const float fj = static_cast<float>(__builtin_bit_cast(_Float16, f[j]));
-      dst[j] = f32_to_act(v * fj, bf16 != 0);
+  for (int u = 0; u < kPre; ++u) {
+    const int j = threadIdx.x + u * 256;
+    if (j < k8) {
+      if (has_perm) {
+        pp[u][0] = p4[2 * j];
+        pp[u][1] = p4[2 * j + 1];
+      }
+      if (has_f) ff[u] = f4[j];
     }
   }
+  for (int j = threadIdx.x; j < k8; j += 256) row4[j] = src[j];
+  __syncthreads();
+  uint4* dst = reinterpret_cast<uint4*>(jb.out + base);
+  auto gather = [&](int j, int4 p0, int4 p1, uint4 fv) {
+    int p[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+    if (!has_perm) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) p[e] = 8 * j + e;
+    }
+    const uint32_t fw[4] = {fv.x, fv.y, fv.z, fv.w};
+    uint32_t h[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint16_t v = static_cast<unsigned>(p[e]) < static_cast<unsigned>(k) ? row[p[e]] : 0;
+      if (has_f) v = scaled(v, static_cast<uint16_t>(fw[e / 2] >> (16 * (e & 1))), bf16);
+      h[e] = v;
+    }
+    dst[j] = uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+  };
+  const int4 z4{0, 0, 0, 0};
+  const uint4 zf{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int u = 0; u < kPre; ++u) {
+    const int j = threadIdx.x + u * 256;
+    if (j < k8) gather(j, has_perm ? pp[u][0] : z4, has_perm ? pp[u][1] : z4, has_f ? ff[u] : zf);
+  }
+  for (int j = threadIdx.x + kPre * 256; j < k8; j += 256)
+    gather(j, has_perm ? p4[2 * j] : z4, has_perm ? p4[2 * j + 1] : z4, has_f ? f4[j] : zf);
 }
 
 template <int B>
@@ -254,82 +260,28 @@ void launch_unpack(const polyq_layout& L, int i, const uint8_t* region, uint16_t
 
 }  // namespace
 
-void launch_permute_rows(const int32_t* perm, const uint16_t* x, uint16_t* out, int32_t m, int32_t k,
-                         hipStream_t st) {
-  // one work-group per row only when there are enough rows to fill the chip;
-  // a few decode tokens spread one element per thread over the whole chip
-  if (m >= kPermLdsMinRows && k <= kPermLdsK && k % 8 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
-      reinterpret_cast<uintptr_t>(perm) % 16 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) {
-    hipLaunchKernelGGL(permute_rows_lds_kernel, dim3(static_cast<unsigned>(m)), dim3(256),
-                       static_cast<size_t>(k) * 2, st, perm, x, out, k);
-  } else {
-    const int64_t n_el = static_cast<int64_t>(m) * k;
-    hipLaunchKernelGGL(permute_rows_kernel, dim3(static_cast<unsigned>((n_el + 255) / 256)), dim3(256), 0,
-                       st, perm, x, out, m, k);
+void launch_shuffle(const ShuffleJob* jobs, int count, int32_t m, bool bf16, hipStream_t st) {
+  if (count < 1) return;
+  ShuffleArgs a{};
+  bool lds = m >= kPermLdsMinRows;
+  int kmax = 0;
+  for (int i = 0; i < count; ++i) {
+    const ShuffleJob& j = jobs[i];
+    a.job[i] = j;
+    kmax = std::max(kmax, static_cast<int>(j.k));
+    lds = lds && j.k <= kPermLdsK && j.k % 8 == 0 && reinterpret_cast<uintptr_t>(j.x) % 16 == 0 &&
+          reinterpret_cast<uintptr_t>(j.perm) % 16 == 0 && reinterpret_cast<uintptr_t>(j.f) % 16 == 0 &&
+          reinterpret_cast<uintptr_t>(j.out) % 16 == 0;
   }
-}
-
-// The same for many rows: one token row per work-group, staged in LDS with
-// 16-byte loads (k <= kPermLdsK, k % 8 == 0, 16-byte aligned rows, factors and
-// permutation), then 8 channels per thread: the permutation and factors as
-// 16-byte loads, one 16-byte store.
-template <bool HasPerm>
-__global__ __launch_bounds__(256) void scale_rows_lds_kernel(const int32_t* __restrict__ perm,
-                                                             const uint16_t* __restrict__ f,
-                                                             const uint16_t* __restrict__ x,
-                                                             uint16_t* __restrict__ out, int k, int bf16) {
-  extern __shared__ uint4 row4[];
-  const uint16_t* row = reinterpret_cast<const uint16_t*>(row4);
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * k;
-  const uint4* src = reinterpret_cast<const uint4*>(x + base);
-  for (int j = threadIdx.x; j < k / 8; j += 256) row4[j] = src[j];
-  __syncthreads();
-  const int4* p4 = reinterpret_cast<const int4*>(perm);
-  const uint4* f4 = reinterpret_cast<const uint4*>(f);
-  uint4* dst = reinterpret_cast<uint4*>(out + base);
-  for (int j = threadIdx.x; j < k / 8; j += 256) {
-    int p[8];
-    if constexpr (HasPerm) {
-      const int4 a = p4[2 * j], b = p4[2 * j + 1];
-      p[0] = a.x; p[1] = a.y; p[2] = a.z; p[3] = a.w; p[4] = b.x; p[5] = b.y; p[6] = b.z; p[7] = b.w;
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) p[e] = 8 * j + e;
-    }
-    const uint4 fv = f4[j];
-    const uint32_t fw[4] = {fv.x, fv.y, fv.z, fv.w};
-    uint32_t h[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float v = static_cast<unsigned>(p[e]) < static_cast<unsigned>(k) ? act_to_f32(row[p[e]], bf16 != 0) : 0.f;
-      const float fj = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(fw[e / 2] >> (16 * (e & 1)))));
-      h[e] = f32_to_act(v * fj, bf16 != 0);
-    }
-    dst[j] = uint4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
-  }
-}
-
-void launch_scale_rows(const int32_t* perm, const uint16_t* f, const uint16_t* x, uint16_t* out, int32_t m,
-                       int32_t k, bool bf16, hipStream_t st) {
-  const bool lds = m >= kPermLdsMinRows && k <= kPermLdsK && k % 8 == 0 &&
-                   reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(f) % 16 == 0 &&
-                   reinterpret_cast<uintptr_t>(perm) % 16 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0;
+  a.m = m;
+  a.bf16 = bf16 ? 1 : 0;
   if (lds) {
-    const size_t shm = static_cast<size_t>(k) * 2;
-    if (perm != nullptr)
-      hipLaunchKernelGGL(scale_rows_lds_kernel<true>, dim3(static_cast<unsigned>(m)), dim3(256), shm, st, perm, f, x,
-                         out, k, bf16 ? 1 : 0);
-    else
-      hipLaunchKernelGGL(scale_rows_lds_kernel<false>, dim3(static_cast<unsigned>(m)), dim3(256), shm, st, perm, f,
-                         x, out, k, bf16 ? 1 : 0);
-  } else if (m >= kPermLdsMinRows) {
-    const int64_t threads = static_cast<int64_t>(m) * ((k + 7) / 8);
-    hipLaunchKernelGGL(scale_rows_kernel<8>, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st,
-                       perm, f, x, out, m, k, bf16 ? 1 : 0);
+    hipLaunchKernelGGL(shuffle_rows_lds_kernel, dim3(static_cast<unsigned>(m), static_cast<unsigned>(count)),
+                       dim3(256), static_cast<size_t>(kmax) * 2, st, a);
   } else {
-    const int64_t threads = static_cast<int64_t>(m) * k;
-    hipLaunchKernelGGL(scale_rows_kernel<1>, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, st,
-                       perm, f, x, out, m, k, bf16 ? 1 : 0);
+    const int64_t n_el = static_cast<int64_t>(m) * kmax;
+    hipLaunchKernelGGL(shuffle_elems_kernel, dim3(static_cast<unsigned>((n_el + 255) / 256), static_cast<unsigned>(count)),
+                       dim3(256), 0, st, a);
   }
 }
 
