@@ -354,21 +354,28 @@ def probe_figure(torch, pq, sizes, steps):
     return out
 
 
+def prefill_launches(torch, pq, layer, grouped=True, scaled=False):
+    """Prepared polyq_gemm_batch launches of one prefill step over `layer`
+    ([(name, PackedLinear, x)]): one per group of linears sharing an input.
+    Returns (calls, ys, sched, prepared batches)."""
+    dev = torch.device("cuda", 0)
+    ys = [torch.empty((x.shape[0], pl.n), dtype=torch.float32, device=dev) for _, pl, x in layer]
+    sched = schedule(layer, grouped)
+    xsc = [channel_factors(torch, pl.k, j) if scaled else None for j, (_, pl, _) in enumerate(layer)]
+    preps = [pq.PreparedBatch("gemm", [(layer[j][1].layout, layer[j][1].packed, layer[j][1].perm,
+                                        layer[j][2], ys[j], xsc[j]) for j in idx]) for idx in sched]
+    return [p.run for p in preps], ys, sched, preps
+
+
 def prefill_figure(torch, pq, synth, steps, warmup, m=512, grouped=True, scaled=False):
     """Config: Llama2-13B layer, 4.0-bit prefill mix, bf16 activations, M=512,
     permutation applied by the library (gather kernel + GEMM); one launch per
     group of linears that share an input (one permuted copy per group).  Timed
     as one graph of `steps` steps (and eagerly).  scaled: every linear carries
     Eq. 8's factors 1/s, applied while the library permutes x."""
-    dev = torch.device("cuda", 0)
     layer = build_layer(torch, pq, synth, 3, m=m, x_dtype=torch.bfloat16)
     flops = sum(2.0 * m * pl.n * pl.k for _, pl, _ in layer)
-    ys = [torch.empty((m, pl.n), dtype=torch.float32, device=dev) for _, pl, _ in layer]
-    sched = schedule(layer, grouped)
-    xsc = [channel_factors(torch, pl.k, j) if scaled else None for j, (_, pl, _) in enumerate(layer)]
-    preps = [pq.PreparedBatch("gemm", [(layer[j][1].layout, layer[j][1].packed, layer[j][1].perm,
-                                        layer[j][2], ys[j], xsc[j]) for j in idx]) for idx in sched]
-    calls = [p.run for p in preps]
+    calls, ys, sched, preps = prefill_launches(torch, pq, layer, grouped, scaled)
     ms, reps = graph_region(torch, steps, warmup, lambda i: calls, replays=3)
     ms_eager = eager_region(torch, steps, 1, lambda i: calls)
     per = {}
