@@ -819,8 +819,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     for (int w = 0; w < kWaves; ++w) v += red[(w * m + mi) * 64 + lane];
     return v;
   };
-  // Tokens go in batches of TB (1, 4 or 16), all swaps of a batch in flight at
-  // once.
+  // Tokens go in batches of TB (1, 4, 8 or 16), all swaps of a batch in flight
+  // at once.
   // Indices past the last token are clamped to it: a repeated swap writes the
   // same value again, and in the finisher a repeated read-and-zero (issued
   // after the real one, from the same lane) returns 0.
@@ -846,7 +846,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       for (int j = 0; j < TB; ++j) v[j] = 0.f;
       // SB splits of TB tokens in flight at a time (64 swaps per lane, or 16
       // for one token)
-      constexpr int SB = TB == 16 ? 4 : 16;
+      constexpr int SB = TB == 16 ? 4 : TB == 8 ? 8 : 16;
       for (int s0 = 0; s0 < S; s0 += SB) {
         float t[TB][SB];
 #pragma unroll
@@ -868,11 +868,14 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   };
   using One = std::integral_constant<int, 1>;
   using Four = std::integral_constant<int, 4>;
+  using Eight = std::integral_constant<int, 8>;
   using Sixteen = std::integral_constant<int, 16>;
   if (m == 1)
     write_partials(One{});
   else if (m <= 4)
     write_partials(Four{});
+  else if (m <= 8)
+    write_partials(Eight{});
   else
     write_partials(Sixteen{});
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -887,6 +890,8 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     finish(One{});
   else if (m <= 4)
     finish(Four{});
+  else if (m <= 8)
+    finish(Eight{});
   else
     finish(Sixteen{});
   if (lane == 0) __hip_atomic_store(&counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
