@@ -477,6 +477,13 @@ template <class T>
 __device__ __forceinline__ const __attribute__((address_space(1))) T* gl(const T* p) {
   return (const __attribute__((address_space(1))) T*)(p);
 }
+// 16 bytes per lane from global memory straight into LDS (no registers): lane
+// i writes lds + 16 i; `lds` must be wave-uniform.  Completion is counted like
+// any other vector load.
+__device__ __forceinline__ void ldg16_to_lds(const void* p, void* lds) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(p),
+                                   (__attribute__((address_space(3))) void*)(lds), 16, 0, 0);
+}
 __device__ __forceinline__ uint4 ldg16(const void* p) {
   const u4v v = *gl(reinterpret_cast<const u4v*>(p));
   return uint4{v.x, v.y, v.z, v.w};
@@ -612,9 +619,10 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
     return uint4{as_u32(as_h2(q.x) * as_h2(f.x)), as_u32(as_h2(q.y) * as_h2(f.y)),
                  as_u32(as_h2(q.z) * as_h2(f.z)), as_u32(as_h2(q.w) * as_h2(f.w))};
   };
-  auto stage_fast = [&](auto rounds_tag, auto perm_tag, auto scale_tag) {
+  auto stage_fast = [&](auto rounds_tag, auto perm_tag, auto scale_tag, auto multi_tag) {
     constexpr int R = decltype(rounds_tag)::value;
     constexpr bool SC = decltype(scale_tag)::value;
+    constexpr bool MT = decltype(multi_tag)::value;  // several tokens (clustered x, no factors)
     // lanes past the range load the range's first channels again; their
     // values are never stored
     int kp[R];
@@ -632,10 +640,25 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
 #pragma unroll
         for (int u = 0; u < R; ++u) fv[u] = ldg16(xsc + kp[u]);
       }
+      // the other tokens' x' goes straight into LDS, in the same round trip
+      // as token 0's (several tokens come without factors: the host's
+      // shuffle applied them)
+      if constexpr (MT) {
+        for (int t = 1; t < m; ++t) {
+#pragma unroll
+          for (int u = 0; u < R; ++u)
+            if (u * kRound + lane * 8 < fast_end)
+              ldg16_to_lds(xg + static_cast<int64_t>(t) * kdim + kbase + u * kRound + lane * 8,
+                           xs16 + t * range + u * kRound);
+        }
+      }
       issue_meta_and_weights(rounds_tag);
 #pragma unroll
       for (int u = 0; u < R; ++u) store_x(u, SC ? scale8(xv[u], fv[u]) : xv[u]);
       store_meta(rounds_tag);
+      // every load of this form done before the common code: no LDS write of
+      // the copies above is left in flight past this point
+      if constexpr (MT) __builtin_amdgcn_s_waitcnt(0);
     } else {
       // (1) The permutation of the lane's 8 channels per round, then (2) one
       // 2-byte gather per channel (one memory round trip each).
@@ -679,24 +702,28 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
   if (has_work) {
     // one copy of the staging per count of rounds, form of x and scaling, so
     // that the unscaled forms issue exactly the loads they did without it
-    auto stage = [&](auto perm_tag, auto scale_tag) {
+    auto stage = [&](auto perm_tag, auto scale_tag, auto multi_tag) {
       switch (rounds) {
-        case 4: stage_fast(I4{}, perm_tag, scale_tag); break;
-        case 3: stage_fast(I3{}, perm_tag, scale_tag); break;
-        case 2: stage_fast(I2{}, perm_tag, scale_tag); break;
-        default: stage_fast(I1{}, perm_tag, scale_tag); break;
+        case 4: stage_fast(I4{}, perm_tag, scale_tag, multi_tag); break;
+        case 3: stage_fast(I3{}, perm_tag, scale_tag, multi_tag); break;
+        case 2: stage_fast(I2{}, perm_tag, scale_tag, multi_tag); break;
+        default: stage_fast(I1{}, perm_tag, scale_tag, multi_tag); break;
       }
     };
+    using One = std::false_type;
+    using Several = std::true_type;
     if (use_perm) {
       if (use_scale)
-        stage(Gather{}, std::true_type{});
+        stage(Gather{}, std::true_type{}, One{});
       else
-        stage(Gather{}, std::false_type{});
+        stage(Gather{}, std::false_type{}, One{});
+    } else if (m > 1) {
+      stage(Clustered{}, std::false_type{}, Several{});
     } else {
       if (use_scale)
-        stage(Clustered{}, std::true_type{});
+        stage(Clustered{}, std::true_type{}, One{});
       else
-        stage(Clustered{}, std::false_type{});
+        stage(Clustered{}, std::false_type{}, One{});
     }
     // (6) More tokens, or channels past the fast rounds (these loads wait behind
     // the weight slots).  Clustered x: tokens go in batches of kTokBatch, every
@@ -734,7 +761,6 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
         if (zero_row) *reinterpret_cast<uint4*>(zs16 + kk) = uint4{0u, 0u, 0u, 0u};
       }
     };
-    if (m > 1 && !use_perm) stage_slow(0, fast_end, 1, false);
     if (range > fast_end) stage_slow(fast_end, range, 0, true);
 
       // (7) Metadata pieces past the first four rounds (groups beyond the first
