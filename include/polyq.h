@@ -241,7 +241,9 @@ typedef struct {
    * The product is formed in fp32 and rounded to the activation type, so a
    * power of two (what polyq_bit_scaling produces) is applied exactly.  For
    * several tokens, and in the prefill GEMM, the scaled x' is written to the
-   * workspace's scratch part first (also without a permutation). */
+   * workspace's scratch part first (also without a permutation).  Device
+   * memory, 16-byte aligned for polyq_gemv_batch (read as 16-byte vectors;
+   * POLYQ_ERR_ARG otherwise), any alignment for polyq_gemm_batch. */
   const uint16_t* xscale;
 } polyq_gemv_item;
 
