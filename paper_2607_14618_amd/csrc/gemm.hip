@@ -19,6 +19,11 @@
 // compile time and a step's common path has no branch.  The blocks (whose
 // bit-widths ascend) are visited by straight-line code, one copy per
 // bit-width, so that no loop carries the accumulators through every copy.
+// Each block starts in LDS stage 0, so chunk i of a group always sits in
+// stage i & 1 (compile-time addresses).  In the steady part of a block a
+// thread fetches exactly the packed words it unpacks (4, 8, 12 or 16 bytes)
+// and each step's instructions are issued in a fixed interleaving: fragment
+// reads, then every MFMA followed by part of the next chunk's dequantization.
 //
 // Numerics.  The dequantized operand is (q - z), an integer of magnitude
 // <= 255 that bf16 holds exactly when z is an integer in [0, 255]; each
@@ -48,6 +53,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u3v __attribute__((ext_vector_type(3)));
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
 
 constexpr int kTokWG = 256;                 // tokens per work-group
 constexpr int kRowsWG = 2 * kTileRows;      // weight rows per work-group (two packed tiles)
@@ -304,6 +311,33 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
     ++lcl;
     if (lc == lce && lc < C) set_block(lb + 1);
   };
+  // The same for a chunk known to lie in the current block, of bit-width B:
+  // the packed words are fetched with a load of exactly their size (4, 8, 12
+  // or 16 bytes), which the memory pipeline serves faster than a 16-byte load
+  // at a 4-byte offset, and no block boundary is checked.
+  auto load_in_block = [&](auto b_tag, Pre& pr) __attribute__((always_inline)) {
+    constexpr int B = decltype(b_tag)::value;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      pr.av[j] = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, avoff[j], lc * 64, 0));
+    const int rec = (lcl >> 2) * lrb;
+    const int soff = rec + (B <= 8 ? kMetaBytes : 0) + (lcl & 3) * 256 * B;
+    if constexpr (B == 16) {
+      pr.w = __builtin_bit_cast(u4v, __builtin_amdgcn_raw_buffer_load_b128(wrs, lvoff, soff, 0));
+    } else if constexpr (B == 8) {
+      const u2v v = __builtin_bit_cast(u2v, __builtin_amdgcn_raw_buffer_load_b64(wrs, lvoff, soff, 0));
+      pr.w = u4v{v.x, v.y, 0u, 0u};
+    } else if constexpr (B == 3) {
+      const u3v v = __builtin_bit_cast(u3v, __builtin_amdgcn_raw_buffer_load_b96(wrs, lvoff, soff, 0));
+      pr.w = u4v{v.x, v.y, v.z, 0u};
+    } else {
+      pr.w = u4v{__builtin_amdgcn_raw_buffer_load_b32(wrs, lvoff, soff, 0), 0u, 0u, 0u};
+    }
+    pr.z = __builtin_amdgcn_raw_buffer_load_b16(wrs, zvoff, rec, 0);
+    pr.s = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff, rec, 0);
+    ++lc;
+    ++lcl;
+  };
 
   // Group state of the thread's row while its group is being stored: scale,
   // zero point, whether every zero point of the wave is an integer in
@@ -458,7 +492,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
   load(sn);
   if (C - c0 > 1) load(sc);
   __syncthreads();  // the tags and cleared lo slots before the first store
-  int c = c0, par = 0;  // next chunk to multiply, its stage
+  int c = c0;  // next chunk to multiply
 
   // Chunks [c, cend) of one block of bit-width B, from a group boundary.  The
   // loop is compiled per bit-width, one group of four chunks per iteration:
@@ -466,24 +500,45 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
   // and the common path of a step has no branch.
   auto run_block = [&](auto b_tag, int cend) __attribute__((always_inline)) {
     constexpr int B = decltype(b_tag)::value;
-    // entry: the block's first chunk, still in sn, into stage par
-    store_main(b_tag, sn, c, par, true);
-    store_fix(b_tag, sn, c, par);
+    // entry: the block's first chunk, still in sn, into stage 0 (the last
+    // barrier left both stages free), so that stage indices are compile-time
+    // constants: chunk i of a group sits in stage i & 1
+    store_main(b_tag, sn, c, 0, true);
+    store_fix(b_tag, sn, c, 0);
     if (c + 2 < C) load(sn);
     __syncthreads();
     // One step: multiply chunk c (stage st); if `more` (chunk c + 1 is in the
     // block) store chunk c + 1 (`nf`: it starts a group) from `slot` into the
     // other stage and fetch chunk c + 3 into it (`inner`: known to be in the
-    // split); fold a group that ends with chunk c.
-    auto step = [&](Pre& slot, int st, bool first, bool last, bool nf, bool more, bool inner) __attribute__((always_inline)) {
-      const bool two = B == 16 || __builtin_expect(lds_tag[st] == c + 1, 0);
+    // split); fold a group that ends with chunk c.  `two`: the group's chunks
+    // carry lo tiles (every chunk of a group is stored the same way, since its
+    // zero points are the group's, so the tag is read at its first chunk).
+    bool two = B == 16;
+    auto step = [&](Pre& slot, int st, bool first, bool last, bool nf, bool more, bool inner,
+                    bool in_block = false) __attribute__((always_inline)) {
+      if (B != 16 && first) two = __builtin_expect(lds_tag[st] == c + 1, 0);
       mfma_pass(st, first, 0);
       if (more) store_main(b_tag, slot, c + 1, st ^ 1, nf);
+      if (in_block) {
+        // issue order of a steady step: the eight fragment reads, then each
+        // MFMA followed by two VALU instructions of the next chunk's
+        // dequantization and, every few MFMAs, one of its LDS stores (the
+        // wave keeps its VALU and LDS work flowing while the matrix pipe is
+        // busy, instead of leaving it all after the MFMAs)
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+        for (int m = 0; m < 16; ++m) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+          if (m == 3 || m == 7 || m == 11 || m == 13) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        }
+      }
       if (two) mfma_pass(st, false, 1);
       if (last) fold(st);
       if (more) {
         store_fix(b_tag, slot, c + 1, st ^ 1);
-        if (inner || c + 3 < C) load(slot);
+        if (in_block) load_in_block(b_tag, slot);
+        else if (inner || c + 3 < C) load(slot);
       }
       ++c;
       __syncthreads();
@@ -491,24 +546,32 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
     // Every group but the block's last: all four steps have their next chunk
     // in the block and (three chunks ahead) in the split, so every step
     // issues the same loads and each wait leaves the younger slot in flight.
+    // In all but the last two groups the chunk fetched (at most six ahead of
+    // the group's first) is in the block too.
     const int nch = cend - c;
-    for (int g = (nch - 1) / 4; g > 0; --g) {
-      step(sc, par, true, false, false, true, true);
-      step(sn, par ^ 1, false, false, false, true, true);
-      step(sc, par, false, false, false, true, true);
-      step(sn, par ^ 1, false, true, true, true, true);
+    const int full = (nch - 1) / 4;
+    for (int g = full - 1; g > 0; --g) {
+      step(sc, 0, true, false, false, true, true, true);
+      step(sn, 1, false, false, false, true, true, true);
+      step(sc, 0, false, false, false, true, true, true);
+      step(sn, 1, false, true, true, true, true, true);
+    }
+    if (full > 0) {
+      step(sc, 0, true, false, false, true, true);
+      step(sn, 1, false, false, false, true, true);
+      step(sc, 0, false, false, false, true, true);
+      step(sn, 1, false, true, true, true, true);
     }
     // The block's last group: 1 .. 4 chunks.
     const int r = cend - c;
-    step(sc, par, true, r == 1, false, r > 1, false);
-    if (r >= 2) step(sn, par ^ 1, false, r == 2, false, r > 2, false);
-    if (r >= 3) step(sc, par, false, r == 3, false, r > 3, false);
-    if (r >= 4) step(sn, par ^ 1, false, true, false, false, false);
+    step(sc, 0, true, r == 1, false, r > 1, false);
+    if (r >= 2) step(sn, 1, false, r == 2, false, r > 2, false);
+    if (r >= 3) step(sc, 0, false, r == 3, false, r > 3, false);
+    if (r >= 4) step(sn, 1, false, true, false, false, false);
     if (r & 1) {
       const Pre t = sc;
       sc = sn;
       sn = t;
-      par ^= 1;
     }
   };
   // Blocks have strictly ascending bit-widths, so the work-group's blocks are
