@@ -251,3 +251,37 @@ def test_gemm_small_non_integer_zero_points(case):
         assert_parity(y, y_ref, bound, f"gemm small z {case} n={lin.n}")
         # the all-zero-code rows alone (their products are -s z x only)
         assert_parity(np_(y)[:, :10], y_ref[:, :10], bound[:, :10], f"gemm small z rows {case}")
+
+
+# Blocks of 13-16 chunks: every bit-width runs steady groups (exact-width
+# weight fetches, interleaved issue order) before its last two groups, and the
+# block ends in a partial group.
+STEADY = [(2, 416), (3, 448), (4, 480), (8, 512), (16, 416)]
+
+
+@pytest.mark.parametrize("launch", ["split_k", "batch"])
+@pytest.mark.parametrize("zp", ["integer", "small_non_integer"])
+def test_gemm_steady_groups_every_bit_width(launch, zp):
+    """Long blocks of every bit-width: a single linear whose K splits start
+    inside blocks (the steady part then starts at a split's first group), and
+    a two-linear batch (no split); integer zero points, and rows with small
+    non-integer ones (lo tiles inside steady groups).  300 tokens: two token
+    tiles, the second ragged; 130 rows: the second row pair has a tile past
+    the end."""
+    k = sum(ln for _, ln in STEADY)
+    make = _small_z_linear if zp == "small_non_integer" else (
+        lambda n, k_, bl, seed: random_quant_linear(n, k_, bl, seed=seed, mode="codes"))
+    lins = [make(130, k, STEADY, 5100), make(64, k, STEADY, 5101)]
+    lins[1].perm = lins[0].perm
+    pls = [packed_linear(lin) for lin in lins]
+    x = _xb(300, k, seed=51)
+    xd = x.to(dev())
+    if launch == "split_k":
+        ys = [pls[0].prefill(xd)]
+        lins = lins[:1]
+    else:
+        ys = pq.prefill_batch(pls, [xd, xd])
+    torch.cuda.synchronize()
+    for lin, y in zip(lins, ys):
+        y_ref, bound = oracle_ref(lin, x)
+        assert_parity(y, y_ref, bound, f"gemm steady {launch} {zp} n={lin.n}")
