@@ -5,7 +5,8 @@
 // (v_mfma_f32_16x16x32_bf16, fp32 accumulation).  A work-group of 8 waves owns
 // 256 tokens x 128 weight rows (two packed tiles) and walks K one 32-channel
 // chunk at a time through a two-stage LDS ring:
-//   * every thread prefetches, two chunks ahead, 32 bytes of activations and
+//   * every thread prefetches, three chunks ahead of their multiply (two
+//     register slots), 32 bytes of activations and
 //     its share of the packed chunk (8 codes of one row: one row sub-tile of
 //     one lane slice) plus that row's zero point and scale;
 //   * the packed share is dequantized once per work-group into a bf16 tile in
