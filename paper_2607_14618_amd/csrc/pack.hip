@@ -183,7 +183,8 @@ __global__ __launch_bounds__(256) void shuffle_elems_kernel(const ShuffleArgs a)
 // (k <= kPermLdsK, k % 8 == 0, 16-byte aligned rows, permutation and
 // factors), then 8 channels per thread and pass: the permutation and factors
 // as 16-byte loads, one 16-byte store.  The indices and factors of the first
-// kPre passes are loaded together with the row (one memory round trip).
+// kPre passes (k <= 16384) are loaded together with the row (one memory round
+// trip).
 __global__ __launch_bounds__(256) void shuffle_rows_lds_kernel(const ShuffleArgs a) {
   extern __shared__ uint4 row4[];
   const ShuffleJob& jb = a.job[blockIdx.y];
@@ -194,7 +195,7 @@ __global__ __launch_bounds__(256) void shuffle_rows_lds_kernel(const ShuffleArgs
   const uint4* src = reinterpret_cast<const uint4*>(jb.x + base);
   const int4* p4 = reinterpret_cast<const int4*>(jb.perm);
   const uint4* f4 = reinterpret_cast<const uint4*>(jb.f);
-  constexpr int kPre = 4;
+  constexpr int kPre = 8;  // passes whose indices come with the row (k <= 16384 in one round trip)
   int4 pp[kPre][2];
   uint4 ff[kPre];
 #pragma unroll

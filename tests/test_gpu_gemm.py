@@ -285,3 +285,17 @@ def test_gemm_steady_groups_every_bit_width(launch, zp):
     for lin, y in zip(lins, ys):
         y_ref, bound = oracle_ref(lin, x)
         assert_parity(y, y_ref, bound, f"gemm steady {launch} {zp} n={lin.n}")
+
+
+def test_gemm_row_gather_past_the_prefetched_passes():
+    """K = 20480: the prefill row gather stages the row in LDS but loads the
+    indices of its last passes (past the first 16384 channels) in its loop."""
+    blocks = [(2, 8192), (3, 6144), (4, 4096), (8, 1024), (16, 1024)]
+    k = sum(ln for _, ln in blocks)
+    lin = random_quant_linear(80, k, blocks, seed=61, mode="codes")
+    pl = packed_linear(lin)
+    xb = _xb(9, k, seed=62)
+    y = pl.prefill(xb.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, xb)
+    assert_parity(y, y_ref, bound, "gemm k=20480")
