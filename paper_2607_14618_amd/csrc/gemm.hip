@@ -315,8 +315,11 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
   // The same for a chunk known to lie in the current block, of bit-width B:
   // the packed words are fetched with a load of exactly their size (4, 8, 12
   // or 16 bytes), which the memory pipeline serves faster than a 16-byte load
-  // at a 4-byte offset, and no block boundary is checked.
-  auto load_in_block = [&](auto b_tag, Pre& pr) __attribute__((always_inline)) {
+  // at a 4-byte offset, and no block boundary is checked.  The row's z and s
+  // are fetched only for a group's first chunk (`zs`, known at compile time
+  // in the steady loop): their 2-byte loads, four lanes to an address, cost
+  // the memory pipeline about as much as the activations' 16-byte loads.
+  auto load_in_block = [&](auto b_tag, Pre& pr, bool zs) __attribute__((always_inline)) {
     constexpr int B = decltype(b_tag)::value;
 #pragma unroll
     for (int j = 0; j < 2; ++j)
@@ -334,8 +337,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
     } else {
       pr.w = u4v{__builtin_amdgcn_raw_buffer_load_b32(wrs, lvoff, soff, 0), 0u, 0u, 0u};
     }
-    pr.z = __builtin_amdgcn_raw_buffer_load_b16(wrs, zvoff, rec, 0);
-    pr.s = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff, rec, 0);
+    if (zs) {
+      pr.z = __builtin_amdgcn_raw_buffer_load_b16(wrs, zvoff, rec, 0);
+      pr.s = __builtin_amdgcn_raw_buffer_load_b16(wrs, svoff, rec, 0);
+    }
     ++lc;
     ++lcl;
   };
@@ -516,7 +521,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
     // zero points are the group's, so the tag is read at its first chunk).
     bool two = B == 16;
     auto step = [&](Pre& slot, int st, bool first, bool last, bool nf, bool more, bool inner,
-                    bool in_block = false) __attribute__((always_inline)) {
+                    bool in_block = false, bool zs = true) __attribute__((always_inline)) {
       if (B != 16 && first) two = __builtin_expect(lds_tag[st] == c + 1, 0);
       mfma_pass(st, first, 0);
       if (more) store_main(b_tag, slot, c + 1, st ^ 1, nf);
@@ -538,7 +543,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
       if (last) fold(st);
       if (more) {
         store_fix(b_tag, slot, c + 1, st ^ 1);
-        if (in_block) load_in_block(b_tag, slot);
+        if (in_block) load_in_block(b_tag, slot, zs);
         else if (inner || c + 3 < C) load(slot);
       }
       ++c;
@@ -551,11 +556,12 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatchArgs a) {
     // the group's first) is in the block too.
     const int nch = cend - c;
     const int full = (nch - 1) / 4;
+    // (step i fetches chunk i + 3 of the group: only step 1's starts a group)
     for (int g = full - 1; g > 0; --g) {
-      step(sc, 0, true, false, false, true, true, true);
-      step(sn, 1, false, false, false, true, true, true);
-      step(sc, 0, false, false, false, true, true, true);
-      step(sn, 1, false, true, true, true, true, true);
+      step(sc, 0, true, false, false, true, true, true, false);
+      step(sn, 1, false, false, false, true, true, true, true);
+      step(sc, 0, false, false, false, true, true, true, false);
+      step(sn, 1, false, true, true, true, true, true, false);
     }
     if (full > 0) {
       step(sc, 0, true, false, false, true, true);
