@@ -814,49 +814,53 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       for (int e = 0; e < 4; ++e) red[(wave * m + tok) * 64 + 16 * r + 4 * (lane >> 4) + e] = acc[r][e];
   }
   __syncthreads();
-  if (wave != 0) return;
+  // The waves share the output tokens: wave w takes tokens w, w + 4, ... (mw
+  // of them; none for w >= m).
+  const int mw = m > wave ? (m - wave + kWaves - 1) / kWaves : 0;
   const int n = ITEM(int32_t, n);
   float* y = ITEM(float*, y);
   const int row = tile * 64 + lane;
-  if (S == 1) {
-    for (int mi = 0; mi < m; ++mi) {
-      float v = 0.f;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) v += red[(w * m + mi) * 64 + lane];
-      if (row < n) y[static_cast<int64_t>(mi) * n + row] = v;
-    }
-    return;
-  }
-  // Split-K fix-up.  Each partial is written, and later read back and zeroed,
-  // with a returning device-scope atomic swap, and a work-group takes its ticket
-  // only after its swaps have returned: swaps and the ticket add on one address
-  // are ordered at that address's device-wide point of coherence, so the
-  // work-group whose ticket closes the round (ticket mod S == S-1, whatever the
-  // counter held before) reads every partial of the round.  It sums them in
-  // split order (deterministic), leaves them zero and resets the counter.  (A
-  // release/acquire-fence version is both slower -- every fence writes back or
-  // invalidates the XCD's whole L2 -- and was measured to read stale partials.)
-  float* partial = ITEM(float*, partial);
-  uint32_t* counter = ITEM(uint32_t*, counter);
-  const int rows_pad = n_tiles * kTileRows;
   auto wg_sum = [&](int mi) {
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) v += red[(w * m + mi) * 64 + lane];
     return v;
   };
-  // Tokens go in batches of TB (1, 4, 8 or 16), all swaps of a batch in flight
-  // at once.
-  // Indices past the last token are clamped to it: a repeated swap writes the
-  // same value again, and in the finisher a repeated read-and-zero (issued
-  // after the real one, from the same lane) returns 0.
+  if (S == 1) {
+    for (int j = 0; j < mw; ++j) {
+      const int mi = wave + kWaves * j;
+      if (row < n) y[static_cast<int64_t>(mi) * n + row] = wg_sum(mi);
+    }
+    return;
+  }
+  // Split-K fix-up.  Each partial is written, and later read back and zeroed,
+  // with a returning device-scope atomic swap, and a work-group takes its ticket
+  // only after the swaps of all its waves have returned (each wave waits for
+  // its own, then the work-group barrier): swaps and the ticket add on one
+  // address are ordered at that address's device-wide point of coherence, so
+  // the work-group whose ticket closes the round (ticket mod S == S-1, whatever
+  // the counter held before) reads every partial of the round.  Its waves sum
+  // them in split order (deterministic), leave them zero, and one lane resets
+  // the counter.  (A release/acquire-fence version is both slower -- every
+  // fence writes back or invalidates the XCD's whole L2 -- and was measured to
+  // read stale partials.)
+  float* partial = ITEM(float*, partial);
+  uint32_t* counter = ITEM(uint32_t*, counter);
+  const int rows_pad = n_tiles * kTileRows;
+  // the wave's j-th token; indices past its last are clamped to it: a repeated
+  // swap writes the same value again, and in the finisher a repeated
+  // read-and-zero (issued after the real one, from the same lane) returns 0
+  auto tok_of = [&](int j) { return wave + kWaves * min(j, mw - 1); };
+  // A wave's tokens go in batches of TB (1, 2 or 4: no more than it has,
+  // except 3 -> 4), all swaps of a batch in flight at once.  Swaps past the real
+  // tokens or splits repeat one address, and the device serializes those.
   auto write_partials = [&](auto tb_tag) {
     constexpr int TB = decltype(tb_tag)::value;
-    for (int t0 = 0; t0 < m; t0 += TB) {
+    for (int j0 = 0; j0 < mw; j0 += TB) {
       float old[TB];
 #pragma unroll
       for (int j = 0; j < TB; ++j) {
-        const int mi = min(t0 + j, m - 1);
+        const int mi = tok_of(j0 + j);
         old[j] = __hip_atomic_exchange(&partial[(static_cast<int64_t>(s) * m + mi) * rows_pad + row],
                                        wg_sum(mi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
@@ -864,15 +868,14 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       for (int j = 0; j < TB; ++j) asm volatile("" ::"v"(old[j]));  // keep the returning form
     }
   };
-  auto finish = [&](auto tb_tag) {
-    constexpr int TB = decltype(tb_tag)::value;
-    for (int t0 = 0; t0 < m; t0 += TB) {
+  // SB splits of TB tokens in flight at a time (SB: 4, 8, 12 or 16, the
+  // smallest that covers S, else 16)
+  auto finish = [&](auto tb_tag, auto sb_tag) {
+    constexpr int TB = decltype(tb_tag)::value, SB = decltype(sb_tag)::value;
+    for (int j0 = 0; j0 < mw; j0 += TB) {
       float v[TB];
 #pragma unroll
       for (int j = 0; j < TB; ++j) v[j] = 0.f;
-      // SB splits of TB tokens in flight at a time (64 swaps per lane, or 16
-      // for one token)
-      constexpr int SB = TB == 16 ? 4 : TB == 8 ? 8 : 16;
       for (int s0 = 0; s0 < S; s0 += SB) {
         float t[TB][SB];
 #pragma unroll
@@ -880,7 +883,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
 #pragma unroll
           for (int u = 0; u < SB; ++u)
             t[j][u] = __hip_atomic_exchange(
-                &partial[(static_cast<int64_t>(min(s0 + u, S - 1)) * m + min(t0 + j, m - 1)) * rows_pad + row],
+                &partial[(static_cast<int64_t>(min(s0 + u, S - 1)) * m + tok_of(j0 + j)) * rows_pad + row],
                 0.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
         for (int j = 0; j < TB; ++j)
@@ -889,38 +892,45 @@ __global__ __launch_bounds__(kWaves * 64) void gemv_kernel(const GemvBatchArgs a
       }
 #pragma unroll
       for (int j = 0; j < TB; ++j)
-        if (t0 + j < m && row < n) y[static_cast<int64_t>(t0 + j) * n + row] = v[j];
+        if (j0 + j < mw && row < n) y[static_cast<int64_t>(tok_of(j0 + j)) * n + row] = v[j];
     }
   };
+  auto finish_sb = [&](auto tb_tag) {
+    if (S <= 4)
+      finish(tb_tag, std::integral_constant<int, 4>{});
+    else if (S <= 8)
+      finish(tb_tag, std::integral_constant<int, 8>{});
+    else if (S <= 12)
+      finish(tb_tag, std::integral_constant<int, 12>{});
+    else
+      finish(tb_tag, std::integral_constant<int, 16>{});
+  };
   using One = std::integral_constant<int, 1>;
+  using Two = std::integral_constant<int, 2>;
   using Four = std::integral_constant<int, 4>;
-  using Eight = std::integral_constant<int, 8>;
-  using Sixteen = std::integral_constant<int, 16>;
-  if (m == 1)
+  if (mw == 1)
     write_partials(One{});
-  else if (m <= 4)
+  else if (mw == 2)
+    write_partials(Two{});
+  else if (mw > 2)
     write_partials(Four{});
-  else if (m <= 8)
-    write_partials(Eight{});
-  else
-    write_partials(Sixteen{});
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0);  // the swaps have returned
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's swaps have returned
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  uint32_t ticket = 0;
-  if (lane == 0)
-    ticket = __hip_atomic_fetch_add(&counter[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  ticket = __shfl(ticket, 0);
+  __syncthreads();  // ... and every other wave's (the partial sums in LDS are dead)
+  uint32_t* tk = reinterpret_cast<uint32_t*>(smem);
+  if (wave == 0 && lane == 0)
+    *tk = __hip_atomic_fetch_add(&counter[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  const uint32_t ticket = __builtin_amdgcn_readfirstlane(*tk);
   if (ticket % static_cast<uint32_t>(S) != static_cast<uint32_t>(S - 1)) return;
-  if (m == 1)
-    finish(One{});
-  else if (m <= 4)
-    finish(Four{});
-  else if (m <= 8)
-    finish(Eight{});
-  else
-    finish(Sixteen{});
-  if (lane == 0) __hip_atomic_store(&counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (mw == 1)
+    finish_sb(One{});
+  else if (mw == 2)
+    finish_sb(Two{});
+  else if (mw > 2)
+    finish_sb(Four{});
+  if (wave == 0 && lane == 0) __hip_atomic_store(&counter[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 }  // namespace
