@@ -182,17 +182,19 @@ def capture(torch, steps, launches, offset=0):
     return g
 
 
-def graph_region(torch, steps, warmup, launches, replays=1):
+def graph_region(torch, steps, warmup, launches, replays=1, warm_replays=1):
     """Eager warmup (`warmup` steps, at least one per rotation copy is the
-    caller's choice of `warmup`), one graph of exactly `steps` steps, one
-    untimed replay, then `replays` timed replays each bracketed by HIP events on
-    the replay stream.  Returns (ms/step of the first timed replay, all)."""
+    caller's choice of `warmup`), one graph of exactly `steps` steps,
+    `warm_replays` untimed replays, then `replays` timed replays each bracketed
+    by HIP events on the replay stream.  Returns (ms/step of the first timed
+    replay, all)."""
     for i in range(warmup):
         for f in launches(i):
             f()
     torch.cuda.synchronize()
     g = capture(torch, steps, launches)
-    g.replay()
+    for _ in range(warm_replays):
+        g.replay()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     out = []
@@ -376,7 +378,9 @@ def prefill_figure(torch, pq, synth, steps, warmup, m=512, grouped=True, scaled=
     layer = build_layer(torch, pq, synth, 3, m=m, x_dtype=torch.bfloat16)
     flops = sum(2.0 * m * pl.n * pl.k for _, pl, _ in layer)
     calls, ys, sched, preps = prefill_launches(torch, pq, layer, grouped, scaled)
-    ms, reps = graph_region(torch, steps, warmup, lambda i: calls, replays=3)
+    # replays right after the capture ran up to 7 % slower than later ones:
+    # about 50 ms of untimed replays before the timed ones
+    ms, reps = graph_region(torch, steps, warmup, lambda i: calls, replays=3, warm_replays=8)
     ms_eager = eager_region(torch, steps, 1, lambda i: calls)
     per = {}
     for pos, idx in enumerate(sched):
