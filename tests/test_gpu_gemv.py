@@ -50,6 +50,44 @@ def test_gemv_parity_small(n, blocks, m, mode):
     assert torch.equal(y, y2)
 
 
+# Split-K fix-up: the four waves of a work-group share the output tokens (one to
+# four each) and keep one batch of 4, 8, 12 or 16 splits in flight; these shapes
+# (one to three row tiles) reach every batch size, S = 32 (two batches), and
+# every number of tokens per wave.
+FIXUP = [
+    (64, [(2, 768), (4, 768)], 3),
+    (64, [(2, 2048), (3, 1024), (8, 1024)], 8),
+    (130, [(2, 2400), (3, 1728), (4, 768), (8, 160), (16, 64)], 10),
+    (64, [(2, 6144), (4, 2048)], 16),
+    (64, [(2, 8192), (4, 8192)], 32),
+]
+
+
+def _splits(layout, m):
+    """Split count of the plan, from the workspace size: counters (padded to
+    256 B), the partials [S][m][tiles * 64] fp32, and for m > 1 the clustered
+    copy of x."""
+    pad = lambda v: (v + 255) // 256 * 256
+    tiles = (layout.n + 63) // 64
+    rest = pq.gemv_workspace_bytes(layout, m) - (pad(m * layout.k * 2) if m > 1 else 0)
+    return 1 if rest == 0 else (rest - pad(tiles * 4)) // (m * tiles * 256)
+
+
+@pytest.mark.parametrize("n,blocks,splits", FIXUP)
+@pytest.mark.parametrize("m", [2, 6, 9, 12, 13])
+def test_gemv_fixup_token_shares_and_split_batches(n, blocks, splits, m):
+    k = sum(l for _, l in blocks)
+    lin = random_quant_linear(n, k, blocks, seed=3000 + n + k + m, mode="gauss")
+    pl = packed_linear(lin)
+    assert _splits(pl.layout, m) == splits
+    x = _x(m, k, seed=7 * n + m)
+    y = pl.decode(x.to(dev()))
+    torch.cuda.synchronize()
+    y_ref, bound = oracle_ref(lin, x)
+    assert_parity(y, y_ref, bound, f"n={n} S={splits} m={m}")
+    assert torch.equal(y, pl.decode(x.to(dev())))
+
+
 @pytest.mark.parametrize("m", [1, 2, 5])
 def test_gemv_is_deterministic_and_reuses_its_workspace(m):
     lin = random_quant_linear(384, 5120, [(2, 2400), (3, 1728), (4, 768), (8, 160), (16, 64)],
