@@ -73,6 +73,8 @@ def _args():
     p.add_argument("--prefill-only", action="store_true", help="time only the prefill GEMM")
     p.add_argument("--decode-only", action="store_true",
                    help="time only the headline decode step (for profiling)")
+    p.add_argument("--tokens", type=int, default=1,
+                   help="with --decode-only: tokens per decode step (1..16, for profiling)")
     p.add_argument("--sweep", action="store_true")
     p.add_argument("--qwen", action="store_true")
     p.add_argument("--qwen-layers", type=int, default=64)
@@ -511,8 +513,10 @@ def main_default(a, torch, pq, synth):
         return
     _log("building the synthetic Llama2-13B layer")
     t0 = time.time()
+    if a.tokens != 1 and not (a.decode_only and 1 <= a.tokens <= 16):
+        raise SystemExit("--tokens M (1..16) only with --decode-only")
     d = decode_figure(torch, pq, synth, a.steps, a.warmup, a.variant, grouped=not a.per_linear,
-                      per_launch=not a.decode_only)
+                      per_launch=not a.decode_only, m=a.tokens)
     _log(f"{d['copies']} copies x {d['step_bytes'] / 1e6:.2f} MB ({time.time() - t0:.1f} s); "
          f"decode: {d['ms_step'] * 1e3:.2f} us/step (graph), {d['gbs']:.1f} GB/s; "
          f"eager {d['ms_step_eager'] * 1e3:.2f} us/step")
@@ -531,7 +535,10 @@ def main_default(a, torch, pq, synth):
              "ms_per_step_replays": [round(r, 6) for r in d["ms_replays"]]}
     if a.decode_only:
         line(d["gbs"], "GB/s", a.steps, a.warmup, d["ms_step"], "f16",
-             {"workload": DECODE_WORKLOAD + "channel permutation gathered in-kernel", "m": 1},
+             {"workload": DECODE_WORKLOAD.replace("decode M=1", f"decode M={a.tokens}") +
+                          ("channel permutation gathered in-kernel" if a.tokens == 1
+                           else "activations shuffled by the library first"),
+              "m": a.tokens},
              **extra)
         return
     roof["per_launch_graph"] = d["per_launch"]
