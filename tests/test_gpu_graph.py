@@ -22,7 +22,7 @@ def _layer(ns, seed):
                   for l in lins]
 
 
-@pytest.mark.parametrize("kind,m", [("gemv", 1), ("gemv", 5), ("gemm", 300)])
+@pytest.mark.parametrize("kind,m", [("gemv", 1), ("gemv", 5), ("gemv", 16), ("gemm", 300)])
 def test_graph_replays_match_eager(kind, m):
     lins, pls = _layer((320, 64, 130), seed=510)
     g = torch.Generator().manual_seed(7)
