@@ -513,8 +513,6 @@ def main_default(a, torch, pq, synth):
         return
     _log("building the synthetic Llama2-13B layer")
     t0 = time.time()
-    if a.tokens != 1 and not (a.decode_only and 1 <= a.tokens <= 16):
-        raise SystemExit("--tokens M (1..16) only with --decode-only")
     d = decode_figure(torch, pq, synth, a.steps, a.warmup, a.variant, grouped=not a.per_linear,
                       per_launch=not a.decode_only, m=a.tokens)
     _log(f"{d['copies']} copies x {d['step_bytes'] / 1e6:.2f} MB ({time.time() - t0:.1f} s); "
@@ -687,6 +685,9 @@ def main():
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(a sharded deployment runs one shard of every linear per GPU)", file=sys.stderr)
+        sys.exit(2)
+    if a.tokens != 1 and not (a.decode_only and 1 <= a.tokens <= 16):
+        print("--tokens M (1..16) only with --decode-only", file=sys.stderr)
         sys.exit(2)
     import torch
     if a.copy_probe:
